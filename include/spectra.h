@@ -1,0 +1,212 @@
+/*
+ * spectra.h - C ABI of the SPECTRA KV-cache codec hot path for AMD MI355X (gfx950).
+ *
+ * The codec follows arXiv 2608.07915 (SPECTRA):
+ *   Sec. 3.1  cache a latent in a spectral basis fitted from second-moment
+ *             statistics (Eqs. gsvd, second-moment-latent), centered by the
+ *             measured coordinate means;
+ *   Sec. 3.2  quantize the latent at rate-distortion optimal group widths
+ *             (Eq. waterfill, App. D) with per-token min/max, one fp16 scale
+ *             and zero-point per kept group and token; zero-bit groups are
+ *             dropped (rank reduction);
+ *   Sec. 3.3  Mode A: reconstruct K,V from the latent; App. E Mode B:
+ *             attention carried out in the latent space (q' = q V once per
+ *             step, scores and value accumulation over the kept coefficients,
+ *             one inverse rotation per output);
+ *   App. F    effective compression ratio 16 / b_eff, metadata included.
+ *
+ * Terminology. A *stream* is one (sequence, layer, KV head, tensor) matrix of
+ * T tokens x head_dim channels. A *codec* holds the state of a set of streams
+ * of one tensor kind (keys or values): per-stream basis, mean, variances and
+ * group bit widths. Streams are independent; stream index s addresses every
+ * per-stream array. For attention, stream s = b * n_kv_heads + kv_head.
+ *
+ * Record format. Each token of each stream is stored as a record of W 32-bit
+ * words (W = floor(R / 32), R the per-token bit budget including metadata):
+ *   words [0, k)   one metadata word per kept group (ascending group index):
+ *                  bits 0..15 = fp16 scale s, bits 16..31 = fp16 zero-point z;
+ *   then, per kept group at b bits, g*b/32 payload words: in-group code j
+ *                  occupies payload bits [j*b, (j+1)*b), least significant
+ *                  bit first (payload bit p = bit p%32 of payload word p/32);
+ *   remaining words are 0.
+ * Records are stored in tiles of 64 tokens, word-major inside a tile:
+ *   packed[s*T_cap*W + (t/64)*64*W + w*64 + t%64]   (T_cap % 64 == 0),
+ * so a wavefront reading word w of 64 consecutive tokens reads 256 contiguous
+ * bytes. The dequantized coefficient is z + s*q; dropped groups decode to 0;
+ * the reconstruction is x_hat = (c_hat + m) V^T.
+ *
+ * Ownership and errors. The caller owns every buffer (device memory for the
+ * codec arrays, inputs, outputs, packed records and workspaces); the library
+ * never allocates device memory and keeps no pointer after a call returns.
+ * Every argument is checked on the host before anything is launched: a
+ * non-zero return means nothing ran. Returns are negative spectra_status
+ * values; the text of the last error of the calling thread is available from
+ * spectra_last_error(). encode / decode / decode_attention / pack / unpack
+ * are asynchronous on the given stream; fit_basis synchronizes it.
+ * Buffers must stay alive until the stream has passed the work. Non-finite
+ * inputs give unspecified (but in-bounds) codes.
+ *
+ * GPU support: head_dim = 128, group_size = 32, b_max <= 8, meta_bits = 32,
+ * records of at most 64 words.
+ * The host-only functions (allocation, eigensolver, fit from moments) accept
+ * any head_dim <= 1024 that group_size divides.
+ */
+#ifndef SPECTRA_H
+#define SPECTRA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPECTRA_OK = 0,
+  SPECTRA_EINVAL = -1,       /* bad argument (null pointer, size, alignment, range) */
+  SPECTRA_EUNSUPPORTED = -2, /* valid parameters the GPU path does not implement */
+  SPECTRA_ENUMERIC = -3,     /* non-finite moments or eigensolver non-convergence */
+  SPECTRA_EWORKSPACE = -4,   /* workspace too small */
+  SPECTRA_EHIP = -5          /* a HIP runtime call failed (message in spectra_last_error) */
+} spectra_status;
+
+typedef enum { SPECTRA_F32 = 0, SPECTRA_BF16 = 1 } spectra_dtype;
+
+/* Parameters shared by all streams of a codec. */
+typedef struct {
+  int32_t head_dim;    /* d (128 on the GPU) */
+  int32_t group_size;  /* g: adjacent energy-ordered coefficients sharing one width (32 on the GPU) */
+  int32_t b_max;       /* largest code width, <= 8 */
+  int32_t meta_bits;   /* bits of metadata per kept group per token: 32 (fp16 s + fp16 z) */
+  int32_t centered;    /* 0: basis of the uncentered second moment (Sec. 3.1); 1: of the covariance */
+  double ratio;        /* effective compression vs fp16 (App. F); R = floor(16 d / ratio + 1e-6) bits */
+  int32_t budget_bits; /* > 0 overrides ratio: R bits per token per stream, metadata included */
+} spectra_params;
+
+/* Codec state. Device arrays are caller-owned; a view of a subset of streams is
+ * made by offsetting the four pointers and lowering n_streams. */
+typedef struct {
+  spectra_params p;
+  int64_t n_streams;
+  int32_t record_words; /* W, set by spectra_codec_init */
+  int32_t reserved;
+  float* basis;         /* device [n_streams][d][d] fp32: basis[s][i][j] = channel i of direction j,
+                           directions in descending second-moment energy */
+  float* mean;          /* device [n_streams][d] fp32: coefficient-space mean m = mean_t(x_t) V */
+  float* var;           /* device [n_streams][d] fp32: centered marginal variance of coefficient j */
+  uint8_t* bits;        /* device [n_streams][d/g]: group code widths (0 = dropped) */
+} spectra_codec;
+
+/* Validates p, fills c->p, c->n_streams and c->record_words. Host only. */
+spectra_status spectra_codec_init(spectra_codec* c, const spectra_params* p, int64_t n_streams);
+
+/* R (bits per token per stream, metadata included) and W = floor(R/32). Host only. */
+int32_t spectra_record_budget_bits(const spectra_params* p);
+int32_t spectra_record_words(const spectra_params* p);
+
+/* Number of uint32 words of a packed cache holding t_capacity tokens per stream
+ * (n_streams * t_capacity * W); t_capacity must be a multiple of 64. */
+int64_t spectra_packed_words(const spectra_codec* c, int64_t t_capacity);
+
+/* ---------------------------------------------------------------------------
+ * Fit (Sec. 3.1 basis, Sec. 3.2 / App. D allocation). Off the per-token path.
+ * x[s*stream_stride + i*token_stride + c], i < n_tokens, c < d, dtype dt, on the
+ * device. Computes per stream mu = mean x, S = mean x^T x in fp64 on the GPU,
+ * then on the host the eigenbasis of S (or of the covariance if centered),
+ * sorted by descending eigenvalue with each direction's largest-|.| entry
+ * positive, the coefficient mean m = mu V, the centered variances and the
+ * bit allocation; writes basis/mean/var/bits of the codec. Synchronizes
+ * `stream`. Workspace: device, spectra_fit_workspace_bytes bytes, 256-B aligned.
+ * ------------------------------------------------------------------------- */
+size_t spectra_fit_workspace_bytes(const spectra_codec* c, int64_t n_tokens);
+spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype dt, int64_t n_tokens,
+                                 int64_t stream_stride, int64_t token_stride, void* workspace,
+                                 size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Encode (Sec. 3.2-3.3: every new token is projected, quantized and appended).
+ * Token i < n_tokens of stream s is read from x[s*stream_stride + i*token_stride + c]
+ * (16-byte aligned rows: token_stride and stream_stride multiples of 8 for bf16,
+ * 4 for fp32) and written to record slot t0 + i of `packed` (device, layout in the
+ * file header). Slots outside [t0, t0 + n_tokens) are not touched, so appends of
+ * single tokens (n_tokens = 1) never disturb earlier records. The projection
+ * c = x V - m is computed to fp32 accuracy; per kept group and token:
+ * z = fp16(min), s = fp16((max - z)/(2^b - 1)) (round to nearest even, saturating),
+ * q = clamp(rne((c - z)/s), 0, 2^b - 1), q = 0 when s = 0. Asynchronous.
+ * ------------------------------------------------------------------------- */
+spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dtype dt,
+                              int64_t stream_stride, int64_t token_stride, int64_t t0, int64_t n_tokens,
+                              uint32_t* packed, int64_t t_capacity, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Decode (Sec. 3.3 Mode A: K and V reconstructed from the latent). Reads record slots
+ * [t0, t0 + n_tokens) of every stream and writes out[s][i][c] (fp32, contiguous,
+ * device) = ((z + s q) over kept groups, 0 elsewhere, + m) V^T. Asynchronous.
+ * ------------------------------------------------------------------------- */
+spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, int64_t t_capacity,
+                              int64_t t0, int64_t n_tokens, float* out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Decode-step attention read straight from the packed caches (App. E, Mode B).
+ * q[b][h][c] (device, dtype q_dt, contiguous), b < batch, h < n_q_heads; query head
+ * h reads KV head h / (n_q_heads / n_kv_heads) through streams
+ * s = b*n_kv_heads + kv of both codecs (record slots [0, n_tokens)).
+ * out[b][h][c] (fp32, device) = sum_t softmax_t(scale * q_h . k_hat_t) v_hat_t,
+ * computed as q' = scale q V_K once, scores over the kept key coefficients
+ * (the constant q' . m_K cancels in the softmax), value accumulation over the
+ * kept value coefficients, then one inverse rotation (a + m_V) V_V^T.
+ * softmax_scale <= 0 selects 1/sqrt(d). n_q_heads / n_kv_heads <= 16.
+ * Workspace: device, spectra_attention_workspace_bytes bytes. Asynchronous.
+ * ------------------------------------------------------------------------- */
+size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                         int64_t n_tokens);
+spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_codec* cv,
+                                        const uint32_t* packed_k, const uint32_t* packed_v,
+                                        int64_t t_capacity, int64_t n_tokens, const void* q,
+                                        spectra_dtype q_dt, int32_t batch, int32_t n_q_heads,
+                                        int32_t n_kv_heads, float softmax_scale, float* out,
+                                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Host-side pieces of the fit, exported so they can be checked without a GPU.
+ * ------------------------------------------------------------------------- */
+
+/* Group widths for centered variances var[d] (App. D objective, Sec. 3.2
+ * groups, App. F rate): the exact integer minimiser of
+ * J(b) = sum_G w_G 4^(8-b_G), w_G = floor(2^39 D_G / max D), D_G = sum of the
+ * group's variances (ascending, fp64), subject to
+ * sum_{b_G>0} (g b_G + meta_bits) <= R, b_G in [0, b_max]; ties go to the
+ * smaller cost, then to the lexicographically largest b. bits_out[d/g]. */
+spectra_status spectra_allocate_bits(const double* var, const spectra_params* p, uint8_t* bits_out);
+
+/* Symmetric eigendecomposition of a[n][n] (fp64, row-major, host): eigenvalues
+ * w[n] descending, eigenvectors as columns of v[n][n] (row-major), each with its
+ * largest-|.| entry (lowest index on ties) positive. n <= 1024. */
+spectra_status spectra_eigh_host(const double* a, int32_t n, double* w, double* v);
+
+/* Fit of one stream from its moments (host): gram[d][d] = sum_t x_t^T x_t,
+ * colsum[d] = sum_t x_t over n_tokens tokens. Writes basis[d][d] (fp32), mean[d]
+ * (fp32), var[d] (fp64) and bits[d/g]. */
+spectra_status spectra_fit_from_moments_host(const spectra_params* p, int64_t n_tokens,
+                                             const double* gram, const double* colsum, float* basis,
+                                             float* mean, double* var, uint8_t* bits);
+
+/* ---------------------------------------------------------------------------
+ * Test hooks: the packing and unpacking device code of encode/decode driven by
+ * given codes. codes[s][i][d] uint8 and meta[s][i][d/g] uint32 (device, contiguous;
+ * meta word = s16 | z16 << 16 for kept groups) for record slots [0, n_tokens).
+ * Asynchronous.
+ * ------------------------------------------------------------------------- */
+spectra_status spectra_pack_codes(const spectra_codec* c, const uint8_t* codes, const uint32_t* meta,
+                                  int64_t n_tokens, uint32_t* packed, int64_t t_capacity, void* stream);
+spectra_status spectra_unpack_codes(const spectra_codec* c, const uint32_t* packed, int64_t t_capacity,
+                                    int64_t n_tokens, uint8_t* codes, uint32_t* meta, void* stream);
+
+/* Status text and the calling thread's last error message. */
+const char* spectra_status_string(spectra_status s);
+const char* spectra_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECTRA_H */

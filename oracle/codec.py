@@ -268,6 +268,35 @@ def quantize(coef: np.ndarray, bits: Sequence[int], p: Params):
     return codes, meta
 
 
+def quantize_given_meta(coef: np.ndarray, meta: np.ndarray, bits: Sequence[int], p: Params):
+    """The quantization rule of ``quantize`` with the zero-point and scale taken
+    from given metadata words (low 16 bits s16, high 16 bits z16).
+
+    Returns codes [T, d] (0 in dropped groups) and the unrounded u = (c - z)/s
+    [T, d] (NaN where s = 0 or the group is dropped), so a caller can tell
+    rounding ties from other differences.
+    """
+    coef = np.asarray(coef, dtype=np.float64)
+    T, d = coef.shape
+    g = p.group_size
+    codes = np.zeros((T, d), dtype=np.uint8)
+    u_all = np.full((T, d), np.nan)
+    for G, b in enumerate(bits):
+        if b == 0:
+            continue
+        s = f16_bits_to_f64(meta[:, G] & 0xFFFF)
+        z = f16_bits_to_f64(meta[:, G] >> 16)
+        levels = float((1 << b) - 1)
+        safe = np.where(s > 0, s, 1.0)
+        u = (coef[:, G * g:(G + 1) * g] - z[:, None]) / safe[:, None]
+        q = np.clip(np.rint(u), 0.0, levels)
+        q[s == 0] = 0.0
+        u[s == 0] = np.nan
+        codes[:, G * g:(G + 1) * g] = q.astype(np.uint8)
+        u_all[:, G * g:(G + 1) * g] = u
+    return codes, u_all
+
+
 def dequantize(codes: np.ndarray, meta: np.ndarray, bits: Sequence[int], p: Params) -> np.ndarray:
     """c_hat = z + s q on kept groups, 0 on dropped groups (Sec. 3.2)."""
     T = codes.shape[0]

@@ -1,0 +1,209 @@
+"""Thin Python binding of libspectra: argument marshalling only.
+
+Torch tensors provide device memory and the current stream; every step of the
+codec runs in the HIP library. Function names match the C ABI in
+``include/spectra.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+from . import _lib
+from ._lib import check, spectra_codec, spectra_params
+
+F32, BF16 = 0, 1
+
+
+@dataclass(frozen=True)
+class Params:
+    head_dim: int = 128
+    group_size: int = 32
+    b_max: int = 8
+    meta_bits: int = 32
+    centered: bool = False
+    ratio: float = 8.0
+    budget_bits: int = 0
+
+    def c(self) -> spectra_params:
+        return spectra_params(self.head_dim, self.group_size, self.b_max, self.meta_bits, int(self.centered),
+                              float(self.ratio), int(self.budget_bits))
+
+    @property
+    def n_groups(self) -> int:
+        return self.head_dim // self.group_size
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Codec:
+    """Per-stream codec state (basis, mean, variances, group widths) in device memory."""
+
+    def __init__(self, params: Params, n_streams: int, device="cuda", _views=None):
+        import torch
+        self.params = params
+        self.n_streams = int(n_streams)
+        if _views is None:
+            d, nG = params.head_dim, params.n_groups
+            self.basis = torch.zeros((n_streams, d, d), dtype=torch.float32, device=device)
+            self.mean = torch.zeros((n_streams, d), dtype=torch.float32, device=device)
+            self.var = torch.zeros((n_streams, d), dtype=torch.float32, device=device)
+            self.bits = torch.zeros((n_streams, nG), dtype=torch.uint8, device=device)
+        else:
+            self.basis, self.mean, self.var, self.bits = _views
+        self.struct = spectra_codec()
+        check(_lib.get().spectra_codec_init(ctypes.byref(self.struct), ctypes.byref(params.c()), self.n_streams))
+        self.struct.basis = self.basis.data_ptr()
+        self.struct.mean = self.mean.data_ptr()
+        self.struct.var = self.var.data_ptr()
+        self.struct.bits = self.bits.data_ptr()
+
+    @property
+    def record_words(self) -> int:
+        return int(self.struct.record_words)
+
+    def view(self, start: int, count: int) -> "Codec":
+        """Codec over streams [start, start + count) sharing this codec's memory."""
+        sl = slice(start, start + count)
+        return Codec(self.params, count, _views=(self.basis[sl], self.mean[sl], self.var[sl], self.bits[sl]))
+
+    def packed_words(self, t_capacity: int) -> int:
+        return int(_lib.get().spectra_packed_words(ctypes.byref(self.struct), int(t_capacity)))
+
+    def empty_packed(self, t_capacity: int):
+        import torch
+        n = max(self.packed_words(t_capacity), 1)
+        return torch.zeros(n, dtype=torch.int32, device=self.basis.device)
+
+
+def spectra_record_words(params: Params) -> int:
+    return int(_lib.get().spectra_record_words(ctypes.byref(params.c())))
+
+
+def spectra_record_budget_bits(params: Params) -> int:
+    return int(_lib.get().spectra_record_budget_bits(ctypes.byref(params.c())))
+
+
+def spectra_fit_workspace_bytes(codec: Codec, n_tokens: int) -> int:
+    return int(_lib.get().spectra_fit_workspace_bytes(ctypes.byref(codec.struct), int(n_tokens)))
+
+
+def spectra_fit_basis(codec: Codec, x, n_tokens: Optional[int] = None, workspace=None, stream=None) -> None:
+    """Fit every stream of ``codec`` on x [n_streams, T, d] (device; strides from the tensor)."""
+    import torch
+    n = x.shape[1] if n_tokens is None else int(n_tokens)
+    need = spectra_fit_workspace_bytes(codec, n)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    check(_lib.get().spectra_fit_basis(ctypes.byref(codec.struct), x.data_ptr(), _dtype_code(x), n, x.stride(0),
+                                       x.stride(1), workspace.data_ptr(), workspace.numel(), _stream(stream)))
+
+
+def spectra_encode(codec: Codec, x, t0: int, packed, t_capacity: int, n_tokens: Optional[int] = None,
+                   stream=None) -> None:
+    """Encode tokens x[:, i] of every stream into record slots t0 + i of ``packed``."""
+    n = x.shape[1] if n_tokens is None else int(n_tokens)
+    assert x.stride(2) == 1
+    check(_lib.get().spectra_encode(ctypes.byref(codec.struct), x.data_ptr(), _dtype_code(x), x.stride(0),
+                                    x.stride(1), int(t0), n, packed.data_ptr(), int(t_capacity), _stream(stream)))
+
+
+def spectra_decode(codec: Codec, packed, t_capacity: int, t0: int, n_tokens: int, out=None, stream=None):
+    """Reconstruct record slots [t0, t0 + n_tokens) of every stream -> float32 [n_streams, n_tokens, d]."""
+    import torch
+    if out is None:
+        out = torch.empty((codec.n_streams, n_tokens, codec.params.head_dim), dtype=torch.float32,
+                          device=packed.device)
+    check(_lib.get().spectra_decode(ctypes.byref(codec.struct), packed.data_ptr(), int(t_capacity), int(t0),
+                                    int(n_tokens), out.data_ptr(), _stream(stream)))
+    return out
+
+
+def spectra_attention_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int, n_tokens: int) -> int:
+    return int(_lib.get().spectra_attention_workspace_bytes(batch, n_q_heads, n_kv_heads, int(n_tokens)))
+
+
+def spectra_decode_attention(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, n_tokens: int, q,
+                             n_kv_heads: int, softmax_scale: float = 0.0, out=None, workspace=None, stream=None):
+    """One decode step over the packed caches: q [batch, n_q_heads, d] -> float32 [batch, n_q_heads, d]."""
+    import torch
+    batch, n_q_heads, d = q.shape
+    assert q.is_contiguous()
+    if out is None:
+        out = torch.empty((batch, n_q_heads, d), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        need = spectra_attention_workspace_bytes(batch, n_q_heads, n_kv_heads, n_tokens)
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    check(_lib.get().spectra_decode_attention(ctypes.byref(ck.struct), ctypes.byref(cv.struct), packed_k.data_ptr(),
+                                              packed_v.data_ptr(), int(t_capacity), int(n_tokens), q.data_ptr(),
+                                              _dtype_code(q), batch, n_q_heads, int(n_kv_heads), float(softmax_scale),
+                                              out.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                              _stream(stream)))
+    return out
+
+
+def spectra_pack_codes(codec: Codec, codes, meta, packed, t_capacity: int, stream=None) -> None:
+    check(_lib.get().spectra_pack_codes(ctypes.byref(codec.struct), codes.data_ptr(), meta.data_ptr(),
+                                        codes.shape[1], packed.data_ptr(), int(t_capacity), _stream(stream)))
+
+
+def spectra_unpack_codes(codec: Codec, packed, t_capacity: int, n_tokens: int, stream=None):
+    import torch
+    dev = packed.device
+    codes = torch.empty((codec.n_streams, n_tokens, codec.params.head_dim), dtype=torch.uint8, device=dev)
+    meta = torch.empty((codec.n_streams, n_tokens, codec.params.n_groups), dtype=torch.int32, device=dev)
+    check(_lib.get().spectra_unpack_codes(ctypes.byref(codec.struct), packed.data_ptr(), int(t_capacity),
+                                          int(n_tokens), codes.data_ptr(), meta.data_ptr(), _stream(stream)))
+    return codes, meta
+
+
+# ---------------------------------------------------------------------------
+# Host-only entry points (numpy in, numpy out)
+# ---------------------------------------------------------------------------
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def spectra_allocate_bits(var, params: Params) -> np.ndarray:
+    v = np.ascontiguousarray(var, dtype=np.float64)
+    out = np.zeros(params.n_groups, dtype=np.uint8)
+    check(_lib.get().spectra_allocate_bits(_ptr(v), ctypes.byref(params.c()), _ptr(out)))
+    return out
+
+
+def spectra_eigh_host(a) -> tuple:
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    n = a.shape[0]
+    w = np.zeros(n)
+    v = np.zeros((n, n))
+    check(_lib.get().spectra_eigh_host(_ptr(a), n, _ptr(w), _ptr(v)))
+    return w, v
+
+
+def spectra_fit_from_moments_host(params: Params, n_tokens: int, gram, colsum) -> tuple:
+    d = params.head_dim
+    gram = np.ascontiguousarray(gram, dtype=np.float64)
+    colsum = np.ascontiguousarray(colsum, dtype=np.float64)
+    basis = np.zeros((d, d), dtype=np.float32)
+    mean = np.zeros(d, dtype=np.float32)
+    var = np.zeros(d, dtype=np.float64)
+    bits = np.zeros(params.n_groups, dtype=np.uint8)
+    check(_lib.get().spectra_fit_from_moments_host(ctypes.byref(params.c()), int(n_tokens), _ptr(gram), _ptr(colsum),
+                                                   _ptr(basis), _ptr(mean), _ptr(var), _ptr(bits)))
+    return basis, mean, var, bits

@@ -1,0 +1,317 @@
+// C entry points of libspectra that run on the GPU: argument checks, workspace
+// layout and kernel launches. Host-only entry points live in host_fit.cpp.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <thread>
+#include <vector>
+
+#include "host_common.hpp"
+#include "kernels.hpp"
+
+using namespace spectra;
+using spectra_dev::AttnArgs;
+using spectra_dev::DecodeArgs;
+using spectra_dev::EncodeArgs;
+using spectra_dev::GramArgs;
+using spectra_dev::PackArgs;
+
+namespace {
+
+constexpr int kD = 128;
+constexpr int64_t kMoments = (int64_t)kD * kD + kD;  // gram + column sums per stream
+
+spectra_status hip_fail(hipError_t e, const char* what) {
+  return fail(SPECTRA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+spectra_status check_codec(const spectra_codec* c, const char* name) {
+  if (!c) return fail(SPECTRA_EINVAL, "%s: null codec", name);
+  spectra_status st = check_params_gpu(c->p);
+  if (st != SPECTRA_OK) return st;
+  if (c->record_words != record_words(c->p))
+    return fail(SPECTRA_EINVAL, "%s: record_words %d does not match the parameters (%d); call spectra_codec_init",
+                name, c->record_words, record_words(c->p));
+  if (c->n_streams <= 0 || c->n_streams > 65535)
+    return fail(SPECTRA_EINVAL, "%s: n_streams=%lld out of range [1, 65535]", name, (long long)c->n_streams);
+  if (!c->basis || !c->mean || !c->var || !c->bits) return fail(SPECTRA_EINVAL, "%s: null codec array", name);
+  if (!aligned(c->basis, 4) || !aligned(c->mean, 4) || !aligned(c->var, 4) || !aligned(c->bits, 4))
+    return fail(SPECTRA_EINVAL, "%s: codec arrays must be 4-byte aligned", name);
+  return SPECTRA_OK;
+}
+
+spectra_status check_slots(int64_t t0, int64_t n, int64_t t_cap) {
+  if (t_cap <= 0 || t_cap % 64 != 0) return fail(SPECTRA_EINVAL, "t_capacity=%lld must be a positive multiple of 64", (long long)t_cap);
+  if (t0 < 0 || n < 0 || t0 + n > t_cap)
+    return fail(SPECTRA_EINVAL, "slots [%lld, %lld) exceed t_capacity %lld", (long long)t0, (long long)(t0 + n), (long long)t_cap);
+  return SPECTRA_OK;
+}
+
+spectra_status check_input(const void* x, spectra_dtype dt, int64_t stream_stride, int64_t token_stride, int64_t n_streams,
+                           int64_t n_tokens) {
+  if (dt != SPECTRA_F32 && dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "dtype %d not supported", (int)dt);
+  if (!x) return fail(SPECTRA_EINVAL, "null input");
+  const int64_t vec = dt == SPECTRA_F32 ? 4 : 8;  // elements per 16 bytes
+  if (!aligned(x, 16)) return fail(SPECTRA_EINVAL, "input must be 16-byte aligned");
+  if (stream_stride < 0 || token_stride < 0 || stream_stride % vec || token_stride % vec)
+    return fail(SPECTRA_EINVAL, "strides must be non-negative multiples of %lld elements", (long long)vec);
+  if (n_tokens > 1 && token_stride < kD) return fail(SPECTRA_EINVAL, "token_stride must be >= head_dim");
+  if (n_streams > 1 && stream_stride == 0) return fail(SPECTRA_EINVAL, "stream_stride is 0 for several streams");
+  return SPECTRA_OK;
+}
+
+void moments_layout(int64_t n_streams, int64_t n_tokens, int32_t* n_chunks, int64_t* chunk_tokens) {
+  int64_t want = (1024 + n_streams - 1) / n_streams;
+  const int64_t max_chunks = (n_tokens + 63) / 64;
+  want = std::max<int64_t>(1, std::min(want, max_chunks));
+  int64_t ct = (n_tokens + want - 1) / want;
+  ct = (ct + 63) / 64 * 64;
+  *chunk_tokens = ct;
+  *n_chunks = (int32_t)((n_tokens + ct - 1) / ct);
+}
+
+size_t fit_ws_bytes(int64_t n_streams, int64_t n_tokens) {
+  int32_t nch;
+  int64_t ct;
+  moments_layout(n_streams, n_tokens, &nch, &ct);
+  return (size_t)n_streams * (size_t)(nch + 1) * (size_t)kMoments * sizeof(double);
+}
+
+size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+
+}  // namespace
+
+extern "C" {
+
+size_t spectra_fit_workspace_bytes(const spectra_codec* c, int64_t n_tokens) {
+  if (!c || n_tokens <= 0 || c->n_streams <= 0) return 0;
+  return fit_ws_bytes(c->n_streams, n_tokens);
+}
+
+spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype dt, int64_t n_tokens,
+                                 int64_t stream_stride, int64_t token_stride, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  spectra_status st = check_codec(c, "fit_basis");
+  if (st != SPECTRA_OK) return st;
+  if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "fit_basis needs n_tokens >= 1");
+  st = check_input(x, dt, stream_stride, token_stride, c->n_streams, n_tokens);
+  if (st != SPECTRA_OK) return st;
+  const int64_t S = c->n_streams;
+  if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "fit workspace must be 256-byte aligned");
+  if (ws_bytes < fit_ws_bytes(S, n_tokens))
+    return fail(SPECTRA_EWORKSPACE, "fit workspace %zu < %zu bytes", ws_bytes, fit_ws_bytes(S, n_tokens));
+  hipStream_t hs = (hipStream_t)stream;
+  GramArgs g{};
+  g.x = x;
+  g.stream_stride = stream_stride;
+  g.token_stride = token_stride;
+  g.n = n_tokens;
+  moments_layout(S, n_tokens, &g.n_chunks, &g.chunk_tokens);
+  g.n_streams = (int32_t)S;
+  g.moments = reinterpret_cast<double*>(workspace);
+  g.partial = g.moments + S * kMoments;
+  hipError_t e = launch_gram(g, dt == SPECTRA_F32, hs);
+  if (e != hipSuccess) return hip_fail(e, "fit moments launch");
+  std::vector<double> mom((size_t)(S * kMoments));
+  e = hipMemcpyAsync(mom.data(), g.moments, mom.size() * sizeof(double), hipMemcpyDeviceToHost, hs);
+  if (e != hipSuccess) return hip_fail(e, "fit moments copy");
+  e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "fit moments sync");
+
+  // Host: eigenbasis, mean, variances and allocation per stream, in parallel.
+  std::vector<float> basis((size_t)S * kD * kD), mean((size_t)S * kD), var32((size_t)S * kD);
+  std::vector<double> var((size_t)S * kD);
+  const int nG = kD / c->p.group_size;
+  std::vector<uint8_t> bits((size_t)S * nG);
+  std::vector<spectra_status> res((size_t)S, SPECTRA_OK);
+  std::vector<std::string> msgs((size_t)S);
+  const int nthreads = (int)std::max<int64_t>(1, std::min<int64_t>(S, std::min(16u, std::max(1u, std::thread::hardware_concurrency()))));
+  std::vector<std::thread> pool;
+  for (int w = 0; w < nthreads; ++w) {
+    pool.emplace_back([&, w]() {
+      for (int64_t s = w; s < S; s += nthreads) {
+        const double* m = &mom[(size_t)(s * kMoments)];
+        res[(size_t)s] = fit_from_moments(c->p, n_tokens, m, m + kD * kD, &basis[(size_t)s * kD * kD], &mean[(size_t)s * kD],
+                                          &var[(size_t)s * kD], &bits[(size_t)s * nG]);
+        if (res[(size_t)s] != SPECTRA_OK) msgs[(size_t)s] = spectra_last_error();
+      }
+    });
+  }
+  for (auto& t : pool) t.join();
+  for (int64_t s = 0; s < S; ++s)
+    if (res[(size_t)s] != SPECTRA_OK) return fail(res[(size_t)s], "fit stream %lld: %s", (long long)s, msgs[(size_t)s].c_str());
+  for (size_t i = 0; i < var.size(); ++i) var32[i] = (float)var[i];
+  e = hipMemcpyAsync(c->basis, basis.data(), basis.size() * sizeof(float), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->mean, mean.data(), mean.size() * sizeof(float), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->var, var32.data(), var32.size() * sizeof(float), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->bits, bits.data(), bits.size(), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "fit result copy");
+  return SPECTRA_OK;
+}
+
+spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dtype dt, int64_t stream_stride,
+                              int64_t token_stride, int64_t t0, int64_t n_tokens, uint32_t* packed, int64_t t_capacity,
+                              void* stream) {
+  spectra_status st = check_codec(c, "encode");
+  if (st != SPECTRA_OK) return st;
+  st = check_slots(t0, n_tokens, t_capacity);
+  if (st != SPECTRA_OK) return st;
+  if (n_tokens == 0) return SPECTRA_OK;
+  st = check_input(x, dt, stream_stride, token_stride, c->n_streams, n_tokens);
+  if (st != SPECTRA_OK) return st;
+  if (!packed || !aligned(packed, 4)) return fail(SPECTRA_EINVAL, "packed must be non-null and 4-byte aligned");
+  if (c->record_words == 0) return SPECTRA_OK;
+  EncodeArgs a{};
+  a.x = x;
+  a.stream_stride = stream_stride;
+  a.token_stride = token_stride;
+  a.t0 = t0;
+  a.n = n_tokens;
+  a.basis = c->basis;
+  a.mean = c->mean;
+  a.bits = c->bits;
+  a.packed = packed;
+  a.t_cap = t_capacity;
+  a.W = c->record_words;
+  a.n_streams = (int32_t)c->n_streams;
+  hipError_t e = launch_encode(a, dt == SPECTRA_F32, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "encode launch");
+}
+
+spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, int64_t t_capacity, int64_t t0,
+                              int64_t n_tokens, float* out, void* stream) {
+  spectra_status st = check_codec(c, "decode");
+  if (st != SPECTRA_OK) return st;
+  st = check_slots(t0, n_tokens, t_capacity);
+  if (st != SPECTRA_OK) return st;
+  if (n_tokens == 0) return SPECTRA_OK;
+  if (!out || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "out must be non-null and 4-byte aligned");
+  if (c->record_words > 0 && (!packed || !aligned(packed, 4)))
+    return fail(SPECTRA_EINVAL, "packed must be non-null and 4-byte aligned");
+  DecodeArgs a{};
+  a.packed = packed;
+  a.t_cap = t_capacity;
+  a.t0 = t0;
+  a.n = n_tokens;
+  a.basis = c->basis;
+  a.mean = c->mean;
+  a.bits = c->bits;
+  a.out = out;
+  a.W = c->record_words;
+  a.n_streams = (int32_t)c->n_streams;
+  hipError_t e = launch_decode(a, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "decode launch");
+}
+
+size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, int64_t n_tokens) {
+  if (batch <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_tokens <= 0) return 0;
+  int32_t tpc;
+  const int32_t nch = attention_chunks(batch, n_kv_heads, n_tokens, &tpc);
+  return round256(attention_qprep_floats(batch, n_q_heads, n_kv_heads) * sizeof(float)) +
+         attention_partial_floats(batch, n_q_heads, nch) * sizeof(float);
+}
+
+spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_codec* cv, const uint32_t* packed_k,
+                                        const uint32_t* packed_v, int64_t t_capacity, int64_t n_tokens, const void* q,
+                                        spectra_dtype q_dt, int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        float softmax_scale, float* out, void* workspace, size_t ws_bytes, void* stream) {
+  spectra_status st = check_codec(ck, "decode_attention keys");
+  if (st != SPECTRA_OK) return st;
+  st = check_codec(cv, "decode_attention values");
+  if (st != SPECTRA_OK) return st;
+  if (batch <= 0 || n_kv_heads <= 0 || n_q_heads <= 0 || n_q_heads % n_kv_heads != 0)
+    return fail(SPECTRA_EINVAL, "need batch > 0 and n_q_heads a positive multiple of n_kv_heads");
+  if (n_q_heads / n_kv_heads > 16) return fail(SPECTRA_EUNSUPPORTED, "more than 16 query heads per kv head");
+  if (batch > 65535 || n_kv_heads > 65535) return fail(SPECTRA_EINVAL, "batch or n_kv_heads too large");
+  if ((int64_t)batch * n_kv_heads > ck->n_streams || (int64_t)batch * n_kv_heads > cv->n_streams)
+    return fail(SPECTRA_EINVAL, "batch * n_kv_heads exceeds the codec's streams");
+  if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "attention needs n_tokens >= 1");
+  st = check_slots(0, n_tokens, t_capacity);
+  if (st != SPECTRA_OK) return st;
+  if (q_dt != SPECTRA_F32 && q_dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "q dtype %d not supported", (int)q_dt);
+  if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "q/out must be non-null and aligned");
+  if ((ck->record_words > 0 && (!packed_k || !aligned(packed_k, 4))) ||
+      (cv->record_words > 0 && (!packed_v || !aligned(packed_v, 4))))
+    return fail(SPECTRA_EINVAL, "packed_k / packed_v must be non-null and 4-byte aligned");
+  if (!(softmax_scale == softmax_scale) || std::isinf(softmax_scale)) return fail(SPECTRA_EINVAL, "softmax_scale not finite");
+  const size_t need = spectra_attention_workspace_bytes(batch, n_q_heads, n_kv_heads, n_tokens);
+  if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "attention workspace must be 256-byte aligned");
+  if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "attention workspace %zu < %zu bytes", ws_bytes, need);
+  AttnArgs a{};
+  a.packed_k = packed_k;
+  a.packed_v = packed_v;
+  a.t_cap = t_capacity;
+  a.n_tokens = n_tokens;
+  a.basis_k = ck->basis;
+  a.basis_v = cv->basis;
+  a.mean_v = cv->mean;
+  a.bits_k = ck->bits;
+  a.bits_v = cv->bits;
+  a.q = q;
+  a.q_f32 = q_dt == SPECTRA_F32;
+  a.batch = batch;
+  a.n_q_heads = n_q_heads;
+  a.n_kv_heads = n_kv_heads;
+  a.n_qh = n_q_heads / n_kv_heads;
+  a.Wk = ck->record_words;
+  a.Wv = cv->record_words;
+  const float sc = softmax_scale > 0.0f ? softmax_scale : 1.0f / std::sqrt((float)kD);
+  a.scale_log2 = sc * 1.4426950408889634f;
+  a.n_chunks = attention_chunks(batch, n_kv_heads, n_tokens, &a.tiles_per_chunk);
+  a.qprep = reinterpret_cast<float*>(workspace);
+  a.partial = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                       round256(attention_qprep_floats(batch, n_q_heads, n_kv_heads) * sizeof(float)));
+  a.out = out;
+  hipError_t e = launch_attention(a, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "attention launch");
+}
+
+spectra_status spectra_pack_codes(const spectra_codec* c, const uint8_t* codes, const uint32_t* meta, int64_t n_tokens,
+                                  uint32_t* packed, int64_t t_capacity, void* stream) {
+  spectra_status st = check_codec(c, "pack_codes");
+  if (st != SPECTRA_OK) return st;
+  st = check_slots(0, n_tokens, t_capacity);
+  if (st != SPECTRA_OK) return st;
+  if (n_tokens == 0 || c->record_words == 0) return SPECTRA_OK;
+  if (!codes || !meta || !packed || !aligned(meta, 4) || !aligned(packed, 4))
+    return fail(SPECTRA_EINVAL, "null or misaligned pack buffer");
+  PackArgs a{};
+  a.codes = codes;
+  a.meta = meta;
+  a.packed = packed;
+  a.bits = c->bits;
+  a.n = n_tokens;
+  a.t_cap = t_capacity;
+  a.W = c->record_words;
+  a.n_streams = (int32_t)c->n_streams;
+  hipError_t e = launch_pack_codes(a, false, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "pack launch");
+}
+
+spectra_status spectra_unpack_codes(const spectra_codec* c, const uint32_t* packed, int64_t t_capacity, int64_t n_tokens,
+                                    uint8_t* codes, uint32_t* meta, void* stream) {
+  spectra_status st = check_codec(c, "unpack_codes");
+  if (st != SPECTRA_OK) return st;
+  st = check_slots(0, n_tokens, t_capacity);
+  if (st != SPECTRA_OK) return st;
+  if (n_tokens == 0) return SPECTRA_OK;
+  if (!codes || !meta || !aligned(meta, 4) || (c->record_words > 0 && (!packed || !aligned(packed, 4))))
+    return fail(SPECTRA_EINVAL, "null or misaligned unpack buffer");
+  PackArgs a{};
+  a.packed_in = packed;
+  a.codes_out = codes;
+  a.meta_out = meta;
+  a.bits = c->bits;
+  a.n = n_tokens;
+  a.t_cap = t_capacity;
+  a.W = c->record_words;
+  a.n_streams = (int32_t)c->n_streams;
+  hipError_t e = launch_pack_codes(a, true, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "unpack launch");
+}
+
+}  // extern "C"

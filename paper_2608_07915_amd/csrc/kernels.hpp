@@ -1,0 +1,88 @@
+// Kernel argument blocks and launchers of libspectra (host and device visible).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spectra_dev {
+
+struct EncodeArgs {
+  const void* x;
+  int64_t stream_stride, token_stride;  // elements
+  int64_t t0, n;                        // record slots [t0, t0 + n)
+  const float* basis;
+  const float* mean;
+  const uint8_t* bits;
+  uint32_t* packed;
+  int64_t t_cap;
+  int32_t W;
+  int32_t n_streams;
+};
+
+struct DecodeArgs {
+  const uint32_t* packed;
+  int64_t t_cap, t0, n;
+  const float* basis;
+  const float* mean;
+  const uint8_t* bits;
+  float* out;  // [n_streams][n][128]
+  int32_t W;
+  int32_t n_streams;
+};
+
+struct PackArgs {
+  const uint8_t* codes;  // pack input
+  const uint32_t* meta;
+  uint32_t* packed;      // pack output
+  const uint32_t* packed_in;  // unpack input
+  uint8_t* codes_out;
+  uint32_t* meta_out;
+  const uint8_t* bits;
+  int64_t n, t_cap;
+  int32_t W;
+  int32_t n_streams;
+};
+
+struct GramArgs {
+  const void* x;
+  int64_t stream_stride, token_stride, n;
+  int64_t chunk_tokens;
+  int32_t n_chunks;
+  int32_t n_streams;
+  double* partial;  // [n_streams][n_chunks][128*128 + 128]
+  double* moments;  // [n_streams][128*128 + 128]
+};
+
+struct AttnArgs {
+  const uint32_t* packed_k;
+  const uint32_t* packed_v;
+  int64_t t_cap, n_tokens;
+  const float* basis_k;
+  const float* basis_v;
+  const float* mean_v;
+  const uint8_t* bits_k;
+  const uint8_t* bits_v;
+  const void* q;
+  int32_t q_f32;
+  int32_t batch, n_q_heads, n_kv_heads, n_qh;
+  int32_t Wk, Wv;
+  float scale_log2;      // softmax scale * log2(e)
+  int32_t n_chunks;      // split of the token range per (batch, kv head)
+  int32_t tiles_per_chunk;
+  float* qprep;          // workspace: rotated queries and MFMA operands
+  float* partial;        // workspace: per-chunk softmax partials
+  float* out;            // [batch][n_q_heads][128]
+};
+
+}  // namespace spectra_dev
+
+namespace spectra {
+hipError_t launch_encode(const spectra_dev::EncodeArgs& a, bool f32_input, hipStream_t st);
+hipError_t launch_decode(const spectra_dev::DecodeArgs& a, hipStream_t st);
+hipError_t launch_pack_codes(const spectra_dev::PackArgs& a, bool unpack, hipStream_t st);
+hipError_t launch_gram(const spectra_dev::GramArgs& a, bool f32_input, hipStream_t st);
+hipError_t launch_attention(const spectra_dev::AttnArgs& a, hipStream_t st);
+// Workspace layout of decode_attention (bytes), shared by the host API and launcher.
+size_t attention_qprep_floats(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads);
+size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
+int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
+}  // namespace spectra

@@ -1,0 +1,106 @@
+"""GPU parity of decode-step attention read from the packed caches (App. E,
+Mode B on the GPU) against the oracle's Mode A over reconstructed caches."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2608_07915_amd as S
+import synth
+from gpu_parity import codec_state, fit_and_encode, records_of, rel_l2, sparams, to_device, values_f64
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+
+def _workload_streams(w, T, batch):
+    ks, vs = [], []
+    for b in range(batch):
+        for h in range(w.n_kv_heads):
+            ks.append(synth.numpy_stream(w, b, 0, h, 0, n_tokens=T))
+            vs.append(synth.numpy_stream(w, b, 0, h, 1, n_tokens=T))
+    return np.stack(ks), np.stack(vs)
+
+
+def _queries(w, batch, step=0):
+    return np.stack([synth.numpy_query(w, b, 0, step) for b in range(batch)])
+
+
+def run_and_check(w, T, batch, ratio, scale=0.0, n_tokens=None, check_heads=None):
+    p = O.Params(ratio=ratio)
+    xk, xv = _workload_streams(w, T, batch)
+    t_cap = (T + 63) // 64 * 64
+    ck, pk = fit_and_encode(to_device(xk, w.dtype), p, t_cap)
+    cv, pv = fit_and_encode(to_device(xv, w.dtype), p, t_cap)
+    q = _queries(w, batch)
+    n = T if n_tokens is None else n_tokens
+    out = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, n, to_device(q, w.dtype), w.n_kv_heads,
+                                     softmax_scale=scale).cpu().numpy()
+    assert np.all(np.isfinite(out))
+    W = O.record_words(p)
+    sc = scale if scale > 0 else 0.0
+    worst_own, worst_same = 0.0, 0.0
+    for b in range(batch):
+        kh_same, vh_same, kh_own, vh_own = [], [], [], []
+        for h in range(w.n_kv_heads):
+            s = b * w.n_kv_heads + h
+            for tensor, codec, packed, x, same, own in ((0, ck, pk, xk, kh_same, kh_own), (1, cv, pv, xv, vh_same, vh_own)):
+                basis, mean, bits = codec_state(codec, s)
+                rec = records_of(packed, s, 0, n, t_cap, W)
+                same.append(O.decode(rec, basis, mean, bits, p))
+                rec_o, *_ = O.encode(values_f64(x[s][:n], w.dtype), basis, mean, bits, p)
+                own.append(O.decode(rec_o, basis, mean, bits, p))
+        q64 = values_f64(q[b], w.dtype)
+        ref_same = O.attention_mode_a(q64, np.stack(kh_same), np.stack(vh_same), sc)
+        ref_own = O.attention_mode_a(q64, np.stack(kh_own), np.stack(vh_own), sc)
+        for h in (range(w.n_q_heads) if check_heads is None else check_heads):
+            e_same = rel_l2(out[b, h], ref_same[h])
+            e_own = rel_l2(out[b, h], ref_own[h])
+            worst_same = max(worst_same, e_same)
+            worst_own = max(worst_own, e_own)
+    assert worst_same <= 2e-5, worst_same
+    assert worst_own <= 2e-3, worst_own
+    return worst_same, worst_own
+
+
+def test_attention_tiny_one_head():
+    run_and_check(synth.WORKLOADS["tiny"], 4096, 1, 8.0)
+
+
+def test_attention_llama_gqa4_4x_ragged():
+    run_and_check(synth.WORKLOADS["llama_layer_4x"], 1000, 1, 4.0)
+
+
+def test_attention_qwen_gqa7_8x():
+    run_and_check(synth.WORKLOADS["qwen_layer_8x"], 1300, 1, 8.0)
+
+
+def test_attention_batched_12x():
+    run_and_check(synth.WORKLOADS["llama_batch16_12x"], 700, 3, 12.0)
+
+
+def test_attention_prefix_of_cache_and_explicit_scale():
+    # attend over the first 333 slots only, with an explicit softmax scale
+    run_and_check(synth.WORKLOADS["llama_model_131k_8x"], 640, 1, 8.0, scale=0.05, n_tokens=333)
+
+
+def test_attention_single_token_returns_its_value():
+    w = synth.WORKLOADS["llama_layer_4x"]
+    p = O.Params(ratio=4.0)
+    xk, xv = _workload_streams(w, 200, 1)
+    ck, pk = fit_and_encode(to_device(xk, w.dtype), p, 256)
+    cv, pv = fit_and_encode(to_device(xv, w.dtype), p, 256)
+    q = to_device(_queries(w, 1), w.dtype)
+    out = S.spectra_decode_attention(ck, cv, pk, pv, 256, 1, q, w.n_kv_heads)
+    v0 = S.spectra_decode(cv, pv, 256, 0, 1)[:, 0]          # [n_kv, d]
+    want = v0.repeat_interleave(w.n_qh, dim=0)[None]
+    assert rel_l2(out.cpu().numpy(), want.cpu().numpy()) <= 1e-5
+
+
+def test_attention_long_context_many_chunks():
+    """More tiles than one wavefront's chunk: exercises the split-K combine."""
+    run_and_check(synth.WORKLOADS["llama_layer_4x"], 20000, 1, 8.0, check_heads=[0, 5, 31])
