@@ -1,0 +1,286 @@
+"""Benchmark of the SPECTRA codec hot path on one MI355X.
+
+One step = the whole hot path over one batch of the headline 8x workload
+(Llama-3.1-8B KV geometry, 32 layers x 8 KV heads x head_dim 128, 131072
+prefill tokens in bf16, ~17 GB uncompressed):
+  1. encode the whole cache (keys and values) into packed records;
+  2. 32 decode steps; in each, for every layer: append the new token's key
+     and value to the packed cache (encoded in the fitted bases), then one
+     decode-step attention per layer (32 query heads, GQA 4:1) read straight
+     from the packed records.
+The basis fit (GPU moments + host eigensolve) is calibration, done once before
+the timed region and reported separately as fit_ms.
+
+Prints one JSON line. `value` is the step's algorithmic bytes (inputs read,
+records written and read, queries, outputs, codec state) divided by the step
+time. `roofline` covers the dominant kernel, decode-step attention, timed with
+HIP events around every attention call inside the timed region.
+`cpu_baseline` is the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "KV encode GB/s + compressed decode-attn tokens/s, % of HBM peak, at 8x"
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="llama_model_131k_8x")
+    ap.add_argument("--decode-steps", type=int, default=None, help="decode steps per bench step (default: workload)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(w, Wk, Wv, n_tokens_attended):
+    """Bytes the method itself must move (no dense cache bytes it avoids)."""
+    d = 128
+    in_b = 2 if w.dtype == "bf16" else 4
+    S_layer = w.n_seq * w.n_kv_heads
+    state = S_layer * 2 * (d * d * 4 + d * 4)              # K and V bases + means read once per call
+    enc_per_tok = in_b * d                                   # input read per token per stream
+    att_records = S_layer * n_tokens_attended * (Wk + Wv) * 4
+    att_qo = w.n_seq * w.n_q_heads * d * (in_b + 4)
+    return {"enc_per_token_stream": enc_per_tok, "attn_call": att_records + att_qo + state}
+
+
+def cpu_baseline(w, p, budget_s=20.0):
+    """CPU oracle on a bounded sample: one layer's first KV head (K and V streams),
+    encode of the prefill + one decode-step attention; throughput in the step's
+    bytes/s units."""
+    import numpy as np
+
+    import oracle as O
+    import synth
+    T = w.n_tokens
+    t_start = time.perf_counter()
+    xk = synth.numpy_stream(w, 0, 0, 0, 0, n_tokens=T)
+    xv = synth.numpy_stream(w, 0, 0, 0, 1, n_tokens=T)
+    gen_s = time.perf_counter() - t_start
+    xk64 = synth.bf16_bits_to_f32(xk).astype(np.float64)
+    xv64 = synth.bf16_bits_to_f32(xv).astype(np.float64)
+    q = synth.bf16_bits_to_f32(synth.numpy_query(w, 0, 0, 0)).astype(np.float64)[: w.n_qh]
+    t0 = time.perf_counter()
+    fk, fv = O.fit(xk64, p), O.fit(xv64, p)
+    bk, bv = O.allocate_bits(fk.var, p), O.allocate_bits(fv.var, p)
+    t1 = time.perf_counter()
+    rk, *_ = O.encode(xk64, fk.basis, fk.mean, bk, p)
+    rv, *_ = O.encode(xv64, fv.basis, fv.mean, bv, p)
+    t2 = time.perf_counter()
+    kh = O.decode(rk, fk.basis, fk.mean, bk, p)
+    vh = O.decode(rv, fv.basis, fv.mean, bv, p)
+    O.attention_mode_a(q, kh[None], vh[None])
+    t3 = time.perf_counter()
+    W = O.record_words(p)
+    enc_bytes = 2 * T * (2 * 128 + W * 4)
+    att_bytes = 2 * T * W * 4
+    secs = t3 - t1
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = 1
+    return {
+        "value": (enc_bytes + att_bytes) / secs / 1e9,
+        "unit": "GB/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"1 layer x 1 KV head (K and V streams) of the workload: encode {T} tokens + one "
+                   f"decode-step attention ({w.n_qh} query heads) from the packed records; fit excluded "
+                   f"({t1 - t0:.1f} s); encode {t2 - t1:.2f} s, decode+attention {t3 - t2:.2f} s"),
+        "host_cores_available": len(os.sched_getaffinity(0)),
+    }
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import oracle as O
+    import paper_2608_07915_amd as S
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.WORKLOADS[args.workload]
+    L, H, Hq, d = w.n_layers, w.n_kv_heads, w.n_q_heads, 128
+    n_seq = w.n_seq
+    T = w.n_tokens
+    n_dec = w.n_append if args.decode_steps is None else args.decode_steps
+    T_all = T + max(n_dec, 0)
+    t_cap = (T_all + 63) // 64 * 64
+    Sn = n_seq * L * H                      # streams per codec, index (seq*L + layer)*H + head
+    sp = S.Params(ratio=w.ratio)
+    p = O.Params(ratio=w.ratio)
+
+    # ---- synthetic inputs (resident in HBM before timing) ----
+    t_gen = time.perf_counter()
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    xk = torch.empty((Sn, T_all, d), dtype=dt, device=dev)
+    xv = torch.empty((Sn, T_all, d), dtype=dt, device=dev)
+    for layer in range(L):
+        for tensor, x in ((0, xk), (1, xv)):
+            blk = synth.device_streams(w, tensor, layer, T_all, dev)      # [n_seq*H, T, d]
+            for seq in range(n_seq):
+                dst = (seq * L + layer) * H
+                x[dst:dst + H] = blk[seq * H:(seq + 1) * H]
+            del blk
+    qs = torch.stack([torch.stack([synth.device_queries(w, layer, step, dev) for layer in range(L)])
+                      for step in range(max(n_dec, 1))])  # [steps][L][n_seq][Hq][d]
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t_gen
+
+    # ---- calibration: fit once on the prefill ----
+    ck, cv = S.Codec(sp, Sn), S.Codec(sp, Sn)
+    t_fit = time.perf_counter()
+    S.spectra_fit_basis(ck, xk, n_tokens=T)
+    S.spectra_fit_basis(cv, xv, n_tokens=T)
+    torch.cuda.synchronize()
+    fit_s = time.perf_counter() - t_fit
+    Wk, Wv = ck.record_words, cv.record_words
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    # per-layer views (codec state and packed records)
+    layer_ck = [ck.view(l * H, H) for l in range(L)]
+    layer_cv = [cv.view(l * H, H) for l in range(L)]
+    layer_pk = [pk[l * H * t_cap * Wk:(l + 1) * H * t_cap * Wk] for l in range(L)]
+    layer_pv = [pv[l * H * t_cap * Wv:(l + 1) * H * t_cap * Wv] for l in range(L)]
+    if n_seq != 1:
+        raise SystemExit("the per-layer decode loop here expects one sequence")
+    ws_bytes = S.spectra_attention_workspace_bytes(1, Hq, H, t_cap)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    outs = torch.empty((L, 1, Hq, d), dtype=torch.float32, device=dev)
+
+    n_attn_calls = max(n_dec, 0) * L
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def step(record):
+        e0, e1 = ev(), ev()
+        e0.record()
+        S.spectra_encode(ck, xk, 0, pk, t_cap, n_tokens=T)
+        S.spectra_encode(cv, xv, 0, pv, t_cap, n_tokens=T)
+        e1.record()
+        att = []
+        for s in range(n_dec):
+            t = T + s
+            for l in range(L):
+                S.spectra_encode(layer_ck[l], xk[l * H:(l + 1) * H, t:t + 1], t, layer_pk[l], t_cap)
+                S.spectra_encode(layer_cv[l], xv[l * H:(l + 1) * H, t:t + 1], t, layer_pv[l], t_cap)
+            a0 = ev()
+            a0.record()
+            for l in range(L):
+                S.spectra_decode_attention(layer_ck[l], layer_cv[l], layer_pk[l], layer_pv[l], t_cap, t + 1,
+                                           qs[s, l], H, out=outs[l], workspace=ws)
+            a1 = ev()
+            a1.record()
+            att.append((a0, a1, t + 1))
+        if record is not None:
+            record.append(((e0, e1), att))
+
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    rec = []
+    start, end = ev(), ev()
+    start.record()
+    for _ in range(args.steps):
+        step(rec)
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+
+    # ---- derived throughput ----
+    ab = lambda n: algorithmic_bytes(w, Wk, Wv, n)  # noqa: E731
+    enc_bytes = Sn * T * 2 * d * (2 if w.dtype == "bf16" else 4) + Sn * T * (Wk + Wv) * 4 + Sn * 2 * (d * d * 4 + d * 4)
+    app_bytes = n_dec * Sn * (2 * d * (2 if w.dtype == "bf16" else 4) + (Wk + Wv) * 4)
+    att_bytes_calls = [ab(n)["attn_call"] for s in range(n_dec) for n in [T + s + 1] for _ in range(L)]
+    step_bytes = enc_bytes + app_bytes + sum(att_bytes_calls)
+    enc_ms = float(np.mean([r[0][0].elapsed_time(r[0][1]) for r in rec]))
+    att_ms_blocks = [a0.elapsed_time(a1) for r in rec for (a0, a1, _) in r[1]]
+    att_call_ms = float(np.sum(att_ms_blocks)) / max(len(att_ms_blocks) * L, 1)
+    att_call_bytes = float(np.mean(att_bytes_calls)) if att_bytes_calls else 0.0
+    att_gbps = att_call_bytes / (att_call_ms * 1e-3) / 1e9 if att_call_ms > 0 else 0.0
+    tokens_per_call = n_seq * float(np.mean([T + s + 1 for s in range(n_dec)])) if n_dec else 0.0
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "description": w.description, "n_layers": L, "n_kv_heads": H, "n_q_heads": Hq,
+            "head_dim": d, "batch": n_seq, "prefill_tokens": T, "decode_steps": n_dec,
+            "ratio_nominal": w.ratio, "ratio_actual_k": round(16 * d / (32 * Wk), 3),
+            "ratio_actual_v": round(16 * d / (32 * Wv), 3), "record_words": [Wk, Wv],
+        },
+        "frac_of_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
+        "encode": {"ms": round(enc_ms, 3), "GBps": round(enc_bytes / (enc_ms * 1e-3) / 1e9, 1),
+                   "frac": round(enc_bytes / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
+        "decode_attention": {"ms_per_layer_call": round(att_call_ms, 4), "GBps": round(att_gbps, 1),
+                             "frac": round(att_gbps / HBM_PEAK_GBPS, 4),
+                             "cache_tokens_per_s": round(tokens_per_call / (att_call_ms * 1e-3), 1),
+                             "generated_tokens_per_s": round(1.0 / (att_call_ms * 1e-3 * L), 2)},
+        "roofline": {"bound": "hbm", "achieved": round(att_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "decode_attention (query rotation + split-K scan + combine), per layer call",
+                     "algorithmic_bytes_per_launch": round(att_call_bytes)},
+        "fit_ms": round(fit_s * 1e3, 1),
+        "input_generation_s": round(gen_s, 1),
+        "bits_k_first_layer": ck.bits[:H].cpu().numpy().tolist(),
+        "bits_v_first_layer": cv.bits[:H].cpu().numpy().tolist(),
+    }
+    if args.check:
+        result["check"] = sampled_check(w, p, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, p)
+    print(json.dumps(result))
+
+
+def sampled_check(w, p, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H):
+    """Oracle comparison of the last layer's head 0 after the timed steps."""
+    import numpy as np
+
+    import oracle as O
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from gpu_parity import check_encoded_stream, codec_state, records_of, rel_l2, host_values
+    l = L - 1
+    n = T + n_dec
+    s = l * H
+    res = {}
+    for name, codec, packed, x in (("k", ck, pk, xk), ("v", cv, pv, xv)):
+        basis, mean, bits = codec_state(codec, s)
+        rec = records_of(packed, s, 0, n, t_cap, codec.record_words)
+        r = check_encoded_stream(host_values(x[s, :n]), basis, mean, bits, p, rec)
+        res[name] = {"code_mismatch": r.code_mismatch, "meta_mismatch": r.meta_mismatch}
+    return res
+
+
+if __name__ == "__main__":
+    main()
