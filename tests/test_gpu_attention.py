@@ -104,3 +104,14 @@ def test_attention_single_token_returns_its_value():
 def test_attention_long_context_many_chunks():
     """More tiles than one wavefront's chunk: exercises the split-K combine."""
     run_and_check(synth.WORKLOADS["llama_layer_4x"], 20000, 1, 8.0, check_heads=[0, 5, 31])
+
+
+@pytest.mark.parametrize("n_qh,ratio", [(1, 8.0), (3, 12.0), (8, 4.0), (12, 8.0), (16, 8.0), (4, 16.0 / 9.0),
+                                        (12, 16.0 / 9.0)])
+def test_attention_gqa_widths_and_wide_records(n_qh, ratio):
+    """Every head-quad count (1..4), stacked and separate weight rows, and records
+    wider than 16 words (the path without register prefetch)."""
+    from dataclasses import replace
+    base = synth.WORKLOADS["llama_layer_4x"]
+    w = replace(base, n_kv_heads=2, n_q_heads=2 * n_qh)
+    run_and_check(w, 900, 1, ratio)
