@@ -491,3 +491,20 @@ def test_end_to_end_oracle_attention_error_shrinks_with_rate():
         errs.append(np.linalg.norm(out - ref) / np.linalg.norm(ref))
     assert errs == sorted(errs, reverse=True)
     assert errs[-1] < 1e-2
+
+
+def test_quantize_given_meta_reproduces_quantize_and_hand_case():
+    rng = np.random.default_rng(8)
+    p = O.Params()
+    coef = rng.standard_normal((300, 128)) * 3
+    bits = [5, 0, 2, 8]
+    codes, meta = O.quantize(coef, bits, p)
+    codes2, u = O.quantize_given_meta(coef, meta, bits, p)
+    assert np.array_equal(codes, codes2)
+    assert np.all(np.isnan(u[:, 32:64]))
+    # hand case: s = 0.5, z = -1 -> u = (c + 1) / 0.5; ties round to even
+    p4 = O.Params(head_dim=4, group_size=4)
+    meta = np.array([[int(O.fp16_bits(np.float16(0.5))) | (int(O.fp16_bits(np.float16(-1.0))) << 16)]], np.uint32)
+    c, uu = O.quantize_given_meta(np.array([[-1.0, -0.75, 0.25, 9.0]]), meta, [3], p4)
+    assert uu.tolist() == [[0.0, 0.5, 2.5, 20.0]]
+    assert c.tolist() == [[0, 0, 2, 7]]
