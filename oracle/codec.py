@@ -177,9 +177,9 @@ def allocate_bits(var: Sequence[float], p: Params) -> List[int]:
     App. D minimises sum_j v_j 2^{-2 b_j} at a fixed rate; Sec. 3.2 groups g
     coordinates under one width (from the group mean variance), drops zero-bit
     groups, and charges one fp16 scale + zero-point per kept group per token.
-    The paper rounds the continuous water-filling solution with an unspecified
-    "rate-matching fix-up"; this oracle takes the exact integer optimum of the
-    same objective instead:
+    The paper does not specify how the continuous water-filling widths are
+    rounded to integers and corrected to the rate; this oracle takes the exact
+    integer optimum of the same objective instead:
 
       minimise J(b) = sum_G w_G 4^(8-b_G), then cost C(b), then prefer the
       lexicographically largest b, subject to
@@ -312,8 +312,8 @@ def dequantize(codes: np.ndarray, meta: np.ndarray, bits: Sequence[int], p: Para
 
 
 # ----------------------------------------------------------------------------
-# O-4: record format (the paper only says "payload plus one fp16 scale and
-# zero-point per token" per kept group, Sec. 3.2; the bit layout is ours)
+# O-4: record format (Sec. 3.2 counts a payload plus an fp16 scale and
+# zero-point per kept group and token; the bit layout is ours)
 # ----------------------------------------------------------------------------
 def pack(codes: np.ndarray, meta: np.ndarray, bits: Sequence[int], p: Params) -> np.ndarray:
     """Logical records [T, W] uint32.
