@@ -9,7 +9,10 @@ prefill tokens in bf16, ~17 GB uncompressed):
      decode-step attention per layer (32 query heads, GQA 4:1) read straight
      from the packed records.
 The basis fit (GPU moments + host eigensolve) is calibration, done once before
-the timed region and reported separately as fit_ms.
+the timed region and reported separately as fit_ms. Each decode step is
+replayed from two HIP graphs captured beforehand (the appends, the attention
+calls), as a serving loop would run it; --eager launches every call from
+Python instead.
 
 Prints one JSON line. `value` is the step's algorithmic bytes (inputs read,
 records written and read, queries, outputs, codec state) divided by the step
@@ -42,6 +45,7 @@ def _parse():
     ap.add_argument("--decode-steps", type=int, default=None, help="decode steps per bench step (default: workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
+    ap.add_argument("--eager", action="store_true", help="launch decode steps from Python instead of HIP graphs")
     return ap.parse_args()
 
 
@@ -171,6 +175,22 @@ def main():
     n_attn_calls = max(n_dec, 0) * L
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
 
+    def appends(s):
+        t = T + s
+        for l in range(L):
+            S.spectra_encode(layer_ck[l], xk[l * H:(l + 1) * H, t:t + 1], t, layer_pk[l], t_cap)
+            S.spectra_encode(layer_cv[l], xv[l * H:(l + 1) * H, t:t + 1], t, layer_pv[l], t_cap)
+
+    def attentions(s):
+        for l in range(L):
+            S.spectra_decode_attention(layer_ck[l], layer_cv[l], layer_pk[l], layer_pv[l], t_cap, T + s + 1,
+                                       qs[s, l], H, out=outs[l], workspace=ws)
+
+    # Decode steps run as HIP graphs (one for the 2L appends, one for the L attention
+    # calls of each step), as a serving loop would, so host launch overhead is not
+    # timed; --eager launches every call from Python instead.
+    graphs = None
+
     def step(record):
         e0, e1 = ev(), ev()
         e0.record()
@@ -179,24 +199,37 @@ def main():
         e1.record()
         att = []
         for s in range(n_dec):
-            t = T + s
-            for l in range(L):
-                S.spectra_encode(layer_ck[l], xk[l * H:(l + 1) * H, t:t + 1], t, layer_pk[l], t_cap)
-                S.spectra_encode(layer_cv[l], xv[l * H:(l + 1) * H, t:t + 1], t, layer_pv[l], t_cap)
+            if graphs is None:
+                appends(s)
+            else:
+                graphs[s][0].replay()
             a0 = ev()
             a0.record()
-            for l in range(L):
-                S.spectra_decode_attention(layer_ck[l], layer_cv[l], layer_pk[l], layer_pv[l], t_cap, t + 1,
-                                           qs[s, l], H, out=outs[l], workspace=ws)
+            if graphs is None:
+                attentions(s)
+            else:
+                graphs[s][1].replay()
             a1 = ev()
             a1.record()
-            att.append((a0, a1, t + 1))
+            att.append((a0, a1, T + s + 1))
         if record is not None:
             record.append(((e0, e1), att))
 
     for _ in range(args.warmup):
         step(None)
     torch.cuda.synchronize()
+    if not args.eager:
+        graphs = []
+        for s in range(n_dec):
+            pair = (torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph())
+            with torch.cuda.graph(pair[0]):
+                appends(s)
+            with torch.cuda.graph(pair[1]):
+                attentions(s)
+            graphs.append(pair)
+        torch.cuda.synchronize()
+        step(None)  # one untimed pass through the replays
+        torch.cuda.synchronize()
     rec = []
     start, end = ev(), ev()
     start.record()
@@ -251,6 +284,7 @@ def main():
                      "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
                      "kernel": "decode_attention (query rotation + split-K scan + combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
+        "decode_launch": "eager" if args.eager else "hip_graph",
         "fit_ms": round(fit_s * 1e3, 1),
         "input_generation_s": round(gen_s, 1),
         "bits_k_first_layer": ck.bits[:H].cpu().numpy().tolist(),

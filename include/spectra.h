@@ -84,7 +84,8 @@ typedef struct {
 } spectra_params;
 
 /* Codec state. Device arrays are caller-owned; a view of a subset of streams is
- * made by offsetting the four pointers and lowering n_streams. */
+ * made by offsetting the four pointers and lowering n_streams. basis must be
+ * 16-byte aligned, the other arrays 4-byte aligned (EINVAL otherwise). */
 typedef struct {
   spectra_params p;
   int64_t n_streams;

@@ -38,8 +38,8 @@ spectra_status check_codec(const spectra_codec* c, const char* name) {
   if (c->n_streams <= 0 || c->n_streams > 65535)
     return fail(SPECTRA_EINVAL, "%s: n_streams=%lld out of range [1, 65535]", name, (long long)c->n_streams);
   if (!c->basis || !c->mean || !c->var || !c->bits) return fail(SPECTRA_EINVAL, "%s: null codec array", name);
-  if (!aligned(c->basis, 4) || !aligned(c->mean, 4) || !aligned(c->var, 4) || !aligned(c->bits, 4))
-    return fail(SPECTRA_EINVAL, "%s: codec arrays must be 4-byte aligned", name);
+  if (!aligned(c->basis, 16) || !aligned(c->mean, 4) || !aligned(c->var, 4) || !aligned(c->bits, 4))
+    return fail(SPECTRA_EINVAL, "%s: basis must be 16-byte aligned, the other codec arrays 4-byte aligned", name);
   return SPECTRA_OK;
 }
 

@@ -9,8 +9,15 @@
 // The per-token contractions over the kept latent coefficients are the two
 // matrix products of latent attention; they run on MFMA:
 //   * scores: v_mfma_f32_4x4x4f16 (16 blocks), lane = token, block rows = four
-//     query heads; codes are exact in fp16; q' enters as two fp16 parts (hi+lo)
-//     pre-scaled by a power of two, so the dot products are ~fp32-accurate;
+//     query heads. The B operand is the payload itself, cut by masks into bit
+//     fields that each lie inside one code and inside bits 0..9 of a 16-bit half;
+//     OR-ing in the exponent of 1024 and subtracting 1024 in fp16 (both exact)
+//     turns a field into the normal fp16 integer it spells. A field at bit f0 of
+//     its half holding code bits b0.. equals code-part * 2^(f0-b0), so the
+//     matching A entry is q'_j * 2^(b0-f0). (Fields are not fed as fp16
+//     subnormals: the matrix cores align such products by the subnormal's
+//     nominal exponent and drop low bits.) q' enters as fp16 hi and 2^11-scaled
+//     lo parts in two accumulators, so the dot products are ~fp32-accurate;
 //   * values: v_mfma_f32_16x16x32_bf16, rows = query heads (softmax weights p*s as
 //     bf16 hi and lo parts, stacked in the otherwise unused rows when there are
 //     at most 8 heads), K = 32 tokens, columns = 16 coefficients. Codes of width
@@ -22,11 +29,22 @@
 // states in LDS and write one partial per chunk; combine_kernel merges chunks.
 #include "device_common.hpp"
 #include "kernels.hpp"
+#include "kplan.hpp"
 
 namespace spectra_dev {
 
-constexpr int PART = 136;                    // floats per (chunk, query head): m, l, Z[4], pad[2], acc[128]
-constexpr int QA_QUAD = 4 * 8 * 2 * 4 * 2;   // uint32 of score-MFMA A operands per head quad
+constexpr int PART = 136;  // floats per (chunk, query head): m, l, Z[4], pad[2], acc[128]
+
+constexpr int kplan_mfmas(int B) { return (make_kplan(B).n_ops + 1) / 2; }
+constexpr int KM_MAX = 14;  // score MFMAs per slot, widest plan (B = 7)
+static_assert(make_kplan(7).n_ops == KOPS_MAX && kplan_mfmas(7) == KM_MAX, "plan sizes");
+static_assert(make_kplan(1).n_ops == 16 && make_kplan(5).n_ops == 20 && make_kplan(8).n_ops == 16, "plan sizes");
+__device__ constexpr KPlan KPLANS[8] = {make_kplan(1), make_kplan(2), make_kplan(3), make_kplan(4),
+                                        make_kplan(5), make_kplan(6), make_kplan(7), make_kplan(8)};
+
+// score-MFMA A operands per (head quad, slot): [m][row r][hi k0..k3, lo k0..k3] as fp16
+constexpr int QA_SLOT = KM_MAX * 4 * 4;  // uint32
+constexpr int QA_QUAD = NG * QA_SLOT;
 constexpr int QP = 4 + 16 * 4 + 4 * QA_QUAD;  // floats per (sequence, kv head) of prepared query data
 constexpr int WAVES = 4;
 constexpr int WROW = 72;  // bf16 per weight row (64 tokens + pad: spreads rows over LDS banks)
@@ -36,10 +54,37 @@ __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = __builtin_fmaxf(v, __shfl_xor(v, o));
   return v;
 }
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+
+// DPP lane moves (row = 16 lanes): quad_perm [1,0,3,2] 0xB1 and [2,3,0,1] 0x4E,
+// row_half_mirror 0x141, row_mirror 0x140, row_bcast:15 0x142, row_bcast:31 0x143.
+// Lanes outside ROWMASK, or with no source, receive IDENT.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ float dpp(float v, float ident) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, ident), __builtin_bit_cast(int, v),
+                                                               CTRL, ROWMASK, 0xF, false));
+}
+// Sum over the 64 lanes, valid in lane 63: butterflies within each row of 16,
+// then the row totals are chained through row broadcasts.
+__device__ __forceinline__ float wave_sum_lane63(float v) {
+  v += dpp<0xB1, 0xF>(v, 0.0f);
+  v += dpp<0x4E, 0xF>(v, 0.0f);
+  v += dpp<0x141, 0xF>(v, 0.0f);
+  v += dpp<0x140, 0xF>(v, 0.0f);
+  v += dpp<0x142, 0xA>(v, 0.0f);
+  v += dpp<0x143, 0xC>(v, 0.0f);
   return v;
+}
+// Maximum over the 64 lanes, returned in every lane.
+__device__ __forceinline__ float wave_max_all(float v) {
+  v = __builtin_fmaxf(v, dpp<0xB1, 0xF>(v, v));
+  v = __builtin_fmaxf(v, dpp<0x4E, 0xF>(v, v));
+  v = __builtin_fmaxf(v, dpp<0x141, 0xF>(v, v));
+  v = __builtin_fmaxf(v, dpp<0x140, 0xF>(v, v));
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return __builtin_fmaxf(__builtin_fmaxf(r0, r1), __builtin_fmaxf(r2, r3));
 }
 
 
@@ -48,14 +93,15 @@ __device__ __forceinline__ float wave_sum(float v) {
 // E2 = 2^-E, Qbar[h][g] = sum_{j in g} q'_hj and the score-MFMA A operands
 // [quad][g][k][part][r] = fp16 parts of q'_{4quad+r}[32g + 4k + i] * 2^E.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void qprep_kernel(AttnArgs a) {
+__global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
   __shared__ float qs[16][D];
-  __shared__ float part_s[2][16][D];
-  __shared__ float red_s[4];
+  __shared__ float part_s[4][16][D];
+  __shared__ float red_s[8];
   const int kv = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int s = b * a.n_kv_heads + kv;
   const int nqh = a.n_qh;
-  for (int e = tid; e < 16 * D; e += 256) {
+  const uint32_t bwk = *reinterpret_cast<const uint32_t*>(a.bits_k + (int64_t)s * NG);
+  for (int e = tid; e < 16 * D; e += 512) {
     const int h = e >> 7, c = e & 127;
     float v = 0.0f;
     if (h < nqh) {
@@ -64,77 +110,98 @@ __global__ __launch_bounds__(256) void qprep_kernel(AttnArgs a) {
     }
     qs[h][c] = v;
   }
-  // column j of V_K, rows [64 half, 64 half + 64): all loads issued before use
-  const int j = tid & 127, half = tid >> 7;
-  const float* Vk = a.basis_k + (int64_t)s * D * D + (int64_t)(64 * half) * D + j;
-  float v[64];
+  // column j of V_K, rows [32 qtr, 32 qtr + 32): all loads issued before use
+  const int j = tid & 127, qtr = tid >> 7;
+  const float* Vk = a.basis_k + (int64_t)s * D * D + (int64_t)(32 * qtr) * D + j;
+  float v[32];
 #pragma unroll
-  for (int i = 0; i < 64; ++i) v[i] = Vk[i * D];
+  for (int i = 0; i < 32; ++i) v[i] = Vk[i * D];
   __syncthreads();
   for (int h = 0; h < nqh; ++h) {
     float acc = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 64; ++i) acc = __builtin_fmaf(qs[h][64 * half + i], v[i], acc);
-    part_s[half][h][j] = acc;
+    for (int i = 0; i < 32; ++i) acc = __builtin_fmaf(qs[h][32 * qtr + i], v[i], acc);
+    part_s[qtr][h][j] = acc;
   }
   __syncthreads();
   float amax = 0.0f;
-  for (int e = tid; e < 16 * D; e += 256) {
+  for (int e = tid; e < 16 * D; e += 512) {
     const int h = e >> 7, c = e & 127;
-    const float q = h < nqh ? (part_s[0][h][c] + part_s[1][h][c]) * a.scale_log2 : 0.0f;
+    const float q =
+        h < nqh ? ((part_s[0][h][c] + part_s[1][h][c]) + (part_s[2][h][c] + part_s[3][h][c])) * a.scale_log2 : 0.0f;
     qs[h][c] = q;
     amax = __builtin_fmaxf(amax, __builtin_fabsf(q));
   }
   amax = wave_max(amax);
   if ((tid & 63) == 0) red_s[tid >> 6] = amax;
   __syncthreads();
-  amax = __builtin_fmaxf(__builtin_fmaxf(red_s[0], red_s[1]), __builtin_fmaxf(red_s[2], red_s[3]));
-  // 2^E brings max |q'| into [2^13, 2^14): both fp16 parts stay normal and finite.
+  amax = red_s[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) amax = __builtin_fmaxf(amax, red_s[i]);
+  // 2^E brings max |q'| into [2^8, 2^9), so every A entry x = q' * 2^(E + e) (e <= 6)
+  // stays below 2^15. x is split into hi = fp16(x) and lo = fp16((x - hi) * 2^11):
+  // lo is kept in the normal fp16 range by its 2^11 and accumulates separately.
+  // E2 = 2^-E undoes the scaling.
   int e2 = 0;
   if (amax > 0.0f) (void)__builtin_frexpf(amax, &e2);
-  const int E = amax > 0.0f ? 14 - e2 : 0;
-  const float scl = __builtin_ldexpf(1.0f, E);
+  const int E = amax > 0.0f ? 9 - e2 : 0;
   float* qp = a.qprep + (int64_t)s * QP;
   if (tid == 0) {
     qp[0] = __builtin_ldexpf(1.0f, -E);
     qp[1] = qp[2] = qp[3] = 0.0f;
   }
-  if (tid < 64) {
-    const int h = tid >> 2, g = tid & 3;
+  {
+    // Qbar[h][g]: eight lanes per (head, group), four values each, then a lane reduction
+    const int ent = tid >> 3, part = tid & 7, h = ent >> 2, g = ent & 3;
     float acc = 0.0f;
-    for (int i = 0; i < G; ++i) acc += qs[h][G * g + i];
-    qp[4 + tid] = acc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc += qs[h][G * g + 4 * part + i];
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    if (part == 0) qp[4 + ent] = acc;
   }
-  // K order of the score MFMA: for widths dividing 32 the kernel pairs codes
-  // i and i + 16/b of each payload word (one shift and one mask per pair), so
-  // step k, slot (2u + v) is coefficient word*(32/b) + i + v*(16/b) of pair
-  // 2k + u; other widths keep the natural order 4k + slot.
-  const uint32_t bwk = *reinterpret_cast<const uint32_t*>(a.bits_k + (int64_t)s * NG);
+  // Score-MFMA A operands, entry (quad, slot, m, r): K elements k = 0..3 are the
+  // fields of ops 2m + k/2, half k%2, of the slot's plan; each is q'_{4quad+r}
+  // of the field's coefficient times 2^(E + e) as fp16 hi + lo.
   uint32_t* qa = reinterpret_cast<uint32_t*>(qp + 4 + 64);
-  for (int e = tid; e < 4 * 128; e += 256) {
-    const int r = e & 3, k = (e >> 2) & 7, g = (e >> 5) & 3, quad = e >> 7;
+  const int nquad = (nqh + 3) >> 2;
+  for (int e = tid; e < nquad * NG * KM_MAX * 4; e += 512) {
+    const int r = e & 3, m = (e >> 2) % KM_MAX, slot = (e / (4 * KM_MAX)) & 3, quad = e / (4 * KM_MAX * NG);
+    int g = -1, B = 0, c = 0;
+    for (int gg = 0; gg < NG; ++gg) {
+      const int bb = (int)((bwk >> (8 * gg)) & 0xFFu);
+      if (bb != 0) {
+        if (c == slot) {
+          g = gg;
+          B = bb;
+        }
+        ++c;
+      }
+    }
+    if (g < 0 || B > 8) continue;
+    const KPlan& P = KPLANS[B - 1];
+    if (2 * m >= P.n_ops) continue;
     const int h = 4 * quad + r;
-    const int B = (int)((bwk >> (8 * g)) & 0xFFu);
-    const bool fast = B == 1 || B == 2 || B == 4 || B == 8;
     uint32_t hi[4], lo[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int jj = 4 * k + i;
-      if (fast) {
-        const int half = 16 / B, pair = 2 * k + (i >> 1);
-        jj = (pair / half) * (32 / B) + (pair % half) + (i & 1) * half;
+    for (int k = 0; k < 4; ++k) {
+      const int i = 2 * m + (k >> 1);
+      float x = 0.0f;
+      if (i < P.n_ops) {
+        const KField f = P.op[i].f[k & 1];
+        if (f.code >= 0) x = __builtin_ldexpf(qs[h][G * g + f.code], E + f.e);
       }
-      const float x = qs[h][G * g + jj] * scl;
       const _Float16 xh = (_Float16)x;
-      const _Float16 xl = (_Float16)(x - (float)xh);
-      hi[i] = __builtin_bit_cast(uint16_t, xh);
-      lo[i] = __builtin_bit_cast(uint16_t, xl);
+      const _Float16 xl = (_Float16)((x - (float)xh) * 2048.0f);
+      hi[k] = __builtin_bit_cast(uint16_t, xh);
+      lo[k] = __builtin_bit_cast(uint16_t, xl);
     }
-    const int base = ((((quad * 4 + g) * 8 + k) * 2) * 4 + r) * 2;
-    qa[base + 0] = hi[0] | (hi[1] << 16);
-    qa[base + 1] = hi[2] | (hi[3] << 16);
-    qa[base + 8] = lo[0] | (lo[1] << 16);
-    qa[base + 9] = lo[2] | (lo[3] << 16);
+    uint32_t* dst = qa + ((((quad * NG + slot) * KM_MAX + m) * 4 + r) * 4);
+    dst[0] = hi[0] | (hi[1] << 16);
+    dst[1] = hi[2] | (hi[3] << 16);
+    dst[2] = lo[0] | (lo[1] << 16);
+    dst[3] = lo[2] | (lo[3] << 16);
   }
 }
 
@@ -184,6 +251,46 @@ __device__ __forceinline__ u32x4 value_codes(const uint32_t* __restrict__ vt, in
     }
   }
   return r;
+}
+
+// ---------------------------------------------------------------------------
+// Score contributions of one kept key slot of width B for the lane's token:
+// dh[q][j] += sum over the slot's fields of hi(4q + j, field) * field, and dl
+// likewise with the lo parts (scaled by 2^11); fields are exact fp16 integers.
+// qsl points at the slot's A operands of quad 0; quad q is QA_QUAD further.
+// ---------------------------------------------------------------------------
+template <int B, int NQ>
+__device__ __forceinline__ void score_slot(const uint32_t* __restrict__ kt, int lane, int pay,
+                                           const uint32_t* __restrict__ qsl, int r4, f32x4 (&dh)[NQ],
+                                           f32x4 (&dl)[NQ]) {
+  constexpr KPlan P = make_kplan(B);
+  uint32_t reg0 = 0u;
+  int opi = 0;
+#pragma unroll
+  for (int w = 0; w < B; ++w) {
+    const uint32_t x = kt[(pay + w) * 64 + lane];
+    const uint32_t x6 = x >> 6;
+#pragma unroll
+    for (int i = 0; i < P.word_ops[w]; ++i, ++opi) {
+      // (field | exponent of 1024) - 1024: the field as a normal fp16 integer, both halves
+      const uint32_t v = __builtin_bit_cast(
+          uint32_t, __builtin_bit_cast(f16x2, ((P.op[opi].shifted ? x6 : x) & P.op[opi].mask) | 0x64006400u) -
+                        f16x2{(_Float16)1024.0f, (_Float16)1024.0f});
+      if ((opi & 1) == 0) {
+        reg0 = v;
+        if (opi + 1 < P.n_ops) continue;
+      }
+      // ops opi-1, opi (or opi and an empty register) form the B operand of MFMA m
+      const int m = opi >> 1;
+      const f16x4 bop = as_f16x4(u32x2{(opi & 1) ? reg0 : v, (opi & 1) ? v : 0u});
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const u32x4 A = *reinterpret_cast<const u32x4*>(qsl + q * QA_QUAD + (m * 4 + r4) * 4);
+        dh[q] = __builtin_amdgcn_mfma_f32_4x4x4f16(as_f16x4(u32x2{A[0], A[1]}), bop, dh[q], 0, 0, 0);
+        dl[q] = __builtin_amdgcn_mfma_f32_4x4x4f16(as_f16x4(u32x2{A[2], A[3]}), bop, dl[q], 0, 0, 0);
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -285,10 +392,18 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     const bool valid = t < a.n_tokens;
     // stage this tile's words in LDS (lane = token), then prefetch the next tile
     if constexpr (PW > 0) {
+      if (tt * 64 + 64 <= a.n_tokens) {
 #pragma unroll
-      for (int w = 0; w < PW; ++w) {
-        kt[w * 64 + lane] = valid ? pk[w] : 0u;
-        vt[w * 64 + lane] = valid ? pv[w] : 0u;
+        for (int w = 0; w < PW; ++w) {
+          kt[w * 64 + lane] = pk[w];
+          vt[w * 64 + lane] = pv[w];
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < PW; ++w) {
+          kt[w * 64 + lane] = valid ? pk[w] : 0u;
+          vt[w * 64 + lane] = valid ? pv[w] : 0u;
+        }
       }
       if (tt + WAVES < tile_end) load_tile(tt + WAVES);
     } else {
@@ -306,65 +421,27 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       if (sl >= kk.n) continue;
       const int g = kk.grp[sl];
       const uint32_t meta = kt[sl * 64 + lane];
-      f32x4 d[NQ];
+      f32x4 dh[NQ], dl[NQ];
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) d[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-      {
-        const int B = kk.bits[sl], pay = kk.pay[sl];
-        typedef __attribute__((__vector_size__(2 * sizeof(_Float16)))) _Float16 f16x2;
-        const f16x2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
-        const uint32_t MM = ((1u << B) - 1u) * 0x00010001u;
-        if (B == 1 || B == 2 || B == 4 || B == 8) {
-          // pair (c_i, c_{i+16/B}) of a payload word = (x >> B i) & MM: one shift, one and-or
-          const int lg = B == 1 ? 0 : B == 2 ? 1 : B == 4 ? 2 : 3;  // log2 B
-#pragma unroll 2
-          for (int k = 0; k < 8; ++k) {
-            const int pair = 2 * k, wsel = (pair << lg) >> 4, i0 = pair & ((16 >> lg) - 1);
-            const uint32_t x = kt[(pay + wsel) * 64 + lane];
-            const uint32_t v0 = ((x >> (i0 << lg)) & MM) | 0x64006400u;
-            const uint32_t v1 = ((x >> ((i0 + 1) << lg)) & MM) | 0x64006400u;
-            const f16x2 p01 = __builtin_bit_cast(f16x2, v0) - off;
-            const f16x2 p23 = __builtin_bit_cast(f16x2, v1) - off;
-            const f16x4 bop = {p01[0], p01[1], p23[0], p23[1]};
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-              const int base = ((((q * 4 + g) * 8 + k) * 2) * 4 + r4) * 2;
-              const f16x4 ahi = as_f16x4(*reinterpret_cast<const u32x2*>(qa_s + base));
-              const f16x4 alo = as_f16x4(*reinterpret_cast<const u32x2*>(qa_s + base + 8));
-              d[q] = __builtin_amdgcn_mfma_f32_4x4x4f16(ahi, bop, d[q], 0, 0, 0);
-              d[q] = __builtin_amdgcn_mfma_f32_4x4x4f16(alo, bop, d[q], 0, 0, 0);
-            }
-          }
-        } else {
-#pragma unroll 2
-          for (int k = 0; k < 8; ++k) {
-            // codes 4k..4k+3 of this token: a 4B-bit window starting at bit 4kB
-            const int p0 = 4 * k * B, w0 = pay + (p0 >> 5);
-            const uint32_t lo = kt[w0 * 64 + lane];
-            const uint32_t hi = ((p0 & 31) + 4 * B > 32) ? kt[(w0 + 1) * 64 + lane] : 0u;
-            const uint32_t win = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)(p0 & 31));
-            const uint32_t c0 = __builtin_amdgcn_ubfe(win, 0, B), c1 = __builtin_amdgcn_ubfe(win, B, B);
-            const uint32_t c2 = __builtin_amdgcn_ubfe(win, 2 * B, B), c3 = __builtin_amdgcn_ubfe(win, 3 * B, B);
-            // 1024 + c as fp16 has c in the mantissa; subtracting 1024 is exact
-            const f16x2 p01 = __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(c1, c0, 0x05040100u) | 0x64006400u) - off;
-            const f16x2 p23 = __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(c3, c2, 0x05040100u) | 0x64006400u) - off;
-            const f16x4 bop = {p01[0], p01[1], p23[0], p23[1]};
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-              const int base = ((((q * 4 + g) * 8 + k) * 2) * 4 + r4) * 2;
-              const f16x4 ahi = as_f16x4(*reinterpret_cast<const u32x2*>(qa_s + base));
-              const f16x4 alo = as_f16x4(*reinterpret_cast<const u32x2*>(qa_s + base + 8));
-              d[q] = __builtin_amdgcn_mfma_f32_4x4x4f16(ahi, bop, d[q], 0, 0, 0);
-              d[q] = __builtin_amdgcn_mfma_f32_4x4x4f16(alo, bop, d[q], 0, 0, 0);
-            }
-          }
-        }
+      for (int q = 0; q < NQ; ++q) dh[q] = dl[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const uint32_t* qsl = qa_s + sl * QA_SLOT;
+      const int pay = kk.pay[sl];
+      switch (kk.bits[sl]) {
+        case 1: score_slot<1, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        case 2: score_slot<2, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        case 3: score_slot<3, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        case 4: score_slot<4, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        case 5: score_slot<5, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        case 6: score_slot<6, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        case 7: score_slot<7, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
+        default: score_slot<8, NQ>(kt, lane, pay, qsl, r4, dh, dl); break;
       }
       const float sk = h2f(meta) * E2, zk = h2f(meta >> 16);
 #pragma unroll
       for (int q = 0; q < NQ; ++q)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sc[4 * q + j] += sk * d[q][j] + zk * qbar_s[(4 * q + j) * 4 + g];
+        for (int j = 0; j < 4; ++j)
+          sc[4 * q + j] += sk * __builtin_fmaf(dl[q][j], 1.0f / 2048.0f, dh[q][j]) + zk * qbar_s[(4 * q + j) * 4 + g];
     }
 
     // ---- online softmax (log2 domain); the running max moves only when exceeded ----
@@ -374,7 +451,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       const bool live = valid && h < nqh;
       const float x = live ? sc[h] : -__builtin_inff();
       if (__any(x > m_run[h])) {
-        const float mn = __builtin_fmaxf(m_run[h], wave_max(x));
+        const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x));
         const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
         l_run[h] *= alpha;
 #pragma unroll
@@ -457,15 +534,19 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   // ---- merge the four wavefronts and write this chunk's partial ----
 #pragma unroll
   for (int h = 0; h < NH; ++h) {
-    const float l = wave_sum(l_run[h]);
+    const float l = wave_sum_lane63(l_run[h]);
     float z[NG];
 #pragma unroll
-    for (int g = 0; g < NG; ++g) z[g] = wave_sum(zacc[h][g]);
-    if (lane == 0) {
+    for (int g = 0; g < NG; ++g) z[g] = g < Kv.n ? wave_sum_lane63(zacc[h][g]) : 0.0f;
+    if (lane == 63) {
       mst[wave][h] = ok ? m_run[h] : -__builtin_inff();
       lst[wave][h] = l;
 #pragma unroll
-      for (int g = 0; g < NG; ++g) zst[wave][h][g] = z[g];
+      for (int g = 0; g < NG; ++g) zst[wave][h][g] = 0.0f;
+      // zero-point sums are kept per slot; the partial holds them per group
+#pragma unroll
+      for (int sl = 0; sl < NG; ++sl)
+        if (sl < Kv.n) zst[wave][h][Kv.grp[sl]] = z[sl];
     }
   }
   __syncthreads();  // all waves done with their tile buffers: reuse smem for the value sums
@@ -519,59 +600,95 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 
 // ---------------------------------------------------------------------------
 // Combine chunk partials and inverse-rotate: one workgroup per (query head,
-// sequence); 8 thread groups of 128 split the chunks, then reduce in LDS.
+// sequence). Every global load is issued before the first use: the V_V rows,
+// m_V and bits, then the partials (eight thread groups of 128 take every eighth
+// chunk, merged with a running maximum in batches of CB chunks); the group
+// states are then merged in LDS.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void combine_kernel(AttnArgs a) {
+  constexpr int CB = 8;
   __shared__ float accs[8][D];
   __shared__ float chat[D];
-  __shared__ float red[32];
+  __shared__ float gm[8], gl[8];
   const int hq = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int j = tid & 127, grp = tid >> 7;
   const int kv = hq / a.n_qh;
   const int s = b * a.n_kv_heads + kv;
+  // rotation operands: output row i = tid / 8, coefficients 16 (tid % 8) .. + 15
+  const int ri = tid >> 3, rpart = tid & 7;
+  const f32x4* Vr = reinterpret_cast<const f32x4*>(a.basis_v + (int64_t)s * D * D + (int64_t)ri * D + 16 * rpart);
+  const f32x4 v0 = Vr[0], v1 = Vr[1], v2 = Vr[2], v3 = Vr[3];
+  const float mv = tid < D ? a.mean_v[(int64_t)s * D + tid] : 0.0f;
+  const uint32_t bw = *reinterpret_cast<const uint32_t*>(a.bits_v + (int64_t)s * NG);
+
   const float* ph = a.partial + ((int64_t)b * a.n_q_heads + hq) * a.n_chunks * PART;
   const int nch = a.n_chunks;
-  float mx = -__builtin_inff();
-  for (int c = tid; c < nch; c += 1024) mx = __builtin_fmaxf(mx, ph[(int64_t)c * PART]);
-  mx = wave_max(mx);
-  if ((tid & 63) == 0) red[tid >> 6] = mx;
-  __syncthreads();
-  mx = red[0];
-#pragma unroll
-  for (int i = 1; i < 16; ++i) mx = __builtin_fmaxf(mx, red[i]);
-  const uint32_t bw = *reinterpret_cast<const uint32_t*>(a.bits_v + (int64_t)s * NG);
   const int g = j >> 5;
-  const bool kept = ((bw >> (8 * g)) & 0xFFu) != 0u;
-  float acc = 0.0f, l = 0.0f;
-#pragma unroll 4
-  for (int c = grp; c < nch; c += 8) {
-    const float* pc = ph + (int64_t)c * PART;
-    const float mc = pc[0];
-    const float w = (mc == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(mc - mx);
-    l += w * pc[1];
-    if (kept) acc += w * (pc[2 + g] + pc[8 + j]);
+  float M = -__builtin_inff(), L = 0.0f, A = 0.0f;
+  for (int c0 = grp; c0 < nch; c0 += 8 * CB) {
+    float m[CB], l[CB], z[CB], x[CB];
+#pragma unroll
+    for (int k = 0; k < CB; ++k) {
+      const int c = c0 + 8 * k;
+      const float* pc = ph + (int64_t)(c < nch ? c : grp) * PART;
+      m[k] = c < nch ? pc[0] : -__builtin_inff();
+      l[k] = pc[1];
+      z[k] = pc[2 + g];
+      x[k] = pc[8 + j];
+    }
+    float mb = M;
+#pragma unroll
+    for (int k = 0; k < CB; ++k) mb = __builtin_fmaxf(mb, m[k]);
+    if (mb != -__builtin_inff()) {
+      const float r = (M == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(M - mb);
+      L *= r;
+      A *= r;
+#pragma unroll
+      for (int k = 0; k < CB; ++k) {
+        const float w = (m[k] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m[k] - mb);
+        L = __builtin_fmaf(w, l[k], L);
+        A = __builtin_fmaf(w, z[k] + x[k], A);
+      }
+      M = mb;
+    }
   }
-  accs[grp][j] = acc;
+  if (j == 0) {
+    gm[grp] = M;
+    gl[grp] = L;
+  }
   __syncthreads();
-  if (j == 0) red[16 + grp] = l;
+  float Mx = gm[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) Mx = __builtin_fmaxf(Mx, gm[i]);
+  const float f = (M == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(M - Mx);
+  accs[grp][j] = f * A;
+  if (j == 0) gl[grp] = f * L;  // each group reads only its own entry above
   __syncthreads();
   if (tid < D) {
     float sacc = 0.0f, sl = 0.0f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       sacc += accs[i][tid];
-      sl += red[16 + i];
+      sl += gl[i];
     }
-    chat[tid] = sacc / sl + a.mean_v[(int64_t)s * D + tid];
+    const bool kept = ((bw >> (8 * (tid >> 5))) & 0xFFu) != 0u;
+    chat[tid] = (kept ? sacc / sl : 0.0f) + mv;
   }
   __syncthreads();
-  if (tid < D) {
-    const float* Vv = a.basis_v + (int64_t)s * D * D + (int64_t)tid * D;
-    float o = 0.0f;
-#pragma unroll 16
-    for (int i = 0; i < D; ++i) o = __builtin_fmaf(chat[i], Vv[i], o);
-    a.out[((int64_t)b * a.n_q_heads + hq) * D + tid] = o;
+  // out_i = sum_j chat_j V[i][j]: eight lanes per output row, 16 contiguous j each
+  const float* ch = chat + 16 * rpart;
+  float o = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    o = __builtin_fmaf(ch[k], v0[k], o);
+    o = __builtin_fmaf(ch[4 + k], v1[k], o);
+    o = __builtin_fmaf(ch[8 + k], v2[k], o);
+    o = __builtin_fmaf(ch[12 + k], v3[k], o);
   }
+  o += __shfl_xor(o, 1);
+  o += __shfl_xor(o, 2);
+  o += __shfl_xor(o, 4);
+  if (rpart == 0) a.out[((int64_t)b * a.n_q_heads + hq) * D + ri] = o;
 }
 
 }  // namespace spectra_dev
@@ -617,7 +734,7 @@ static void launch_nq(const AttnArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(qprep_kernel, dim3(a.n_kv_heads, a.batch), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(qprep_kernel, dim3(a.n_kv_heads, a.batch), dim3(512), 0, st, a);
   switch ((a.n_qh + 3) / 4) {
     case 1: launch_nq<1>(a, st); break;
     case 2: launch_nq<2>(a, st); break;

@@ -50,13 +50,54 @@ __device__ __forceinline__ uint32_t quantize16(const float (&c)[16], uint32_t (&
 template <bool F32IN>
 __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
   constexpr int ST = F32IN ? 64 : 128;             // tokens per super-tile
-  constexpr int NB = ST / 32;                      // 32-token MFMA blocks
   constexpr int ROWB = F32IN ? (512 + 16) : (256 + 16);  // padded LDS row (bank spread)
   __shared__ __attribute__((aligned(16))) uint8_t xs[ST * ROWB];
 
   const int s = blockIdx.y;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, col = lane & 31;
+
+  const int64_t first_tile = a.t0 >> 6;
+  const int64_t end = a.t0 + a.n;                       // exclusive slot
+  const int64_t n_tiles = ((end - 1) >> 6) - first_tile + 1;
+  const int64_t n_st = (n_tiles * TILE + ST - 1) / ST;
+  const char* xb = reinterpret_cast<const char*>(a.x);
+  constexpr int ESZ = F32IN ? 4 : 2;
+  constexpr int CPR = (D * ESZ) / 16;  // 16-byte chunks per token row
+  // Super-tile st covers slots [slot0, slot0 + ST); rows [lo, hi) hold the call's
+  // tokens and only the 32-row MFMA blocks [b_lo, b_hi) that meet them are
+  // staged and projected.
+  struct Span {
+    int64_t slot0;
+    int lo, hi, b_lo, b_hi;
+  };
+  auto span = [&](int64_t st) {
+    Span sp;
+    sp.slot0 = (first_tile << 6) + st * ST;
+    sp.lo = (int)(a.t0 > sp.slot0 ? a.t0 - sp.slot0 : 0);
+    sp.hi = (int)(end - sp.slot0 < ST ? end - sp.slot0 : ST);
+    sp.b_lo = sp.lo >> 5;
+    sp.b_hi = (sp.hi + 31) >> 5;
+    return sp;
+  };
+  // Stage the rows of those blocks (16-byte chunks, coalesced) into LDS; rows
+  // outside the call's token range are zero.
+  auto stage = [&](const Span& sp) {
+    for (int c = 32 * sp.b_lo * CPR + tid; c < 32 * sp.b_hi * CPR; c += 256) {
+      const int row = c / CPR, part = c % CPR;
+      const int64_t i = sp.slot0 + row - a.t0;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (i >= 0 && i < a.n)
+        v = *reinterpret_cast<const u32x4*>(xb + ((int64_t)s * a.stream_stride + i * a.token_stride) * ESZ + part * 16);
+      *reinterpret_cast<u32x4*>(xs + row * ROWB + part * 16) = v;
+    }
+  };
+  int64_t st = blockIdx.x;
+  if (st >= n_st) return;
+  // The first rows are loaded before the width table is needed, so their latency
+  // overlaps the basis loads (which depend on it).
+  stage(span(st));
+
   const Kept K = read_kept(a.bits + (int64_t)s * NG);
   const int W = a.W;
   if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
@@ -94,32 +135,14 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
     for (int j = 0; j < 16; ++j) mv[j] = ms[j];
   }
 
-  const int64_t first_tile = a.t0 >> 6;
-  const int64_t end = a.t0 + a.n;                       // exclusive slot
-  const int64_t n_tiles = ((end - 1) >> 6) - first_tile + 1;
-  const int64_t n_st = (n_tiles * TILE + ST - 1) / ST;
-  const char* xb = reinterpret_cast<const char*>(a.x);
-  constexpr int ESZ = F32IN ? 4 : 2;
-
-  for (int64_t st = blockIdx.x; st < n_st; st += gridDim.x) {
-    const int64_t slot0 = (first_tile << 6) + st * ST;
-    __syncthreads();
-    // Stage ST token rows (16-byte chunks, coalesced) into LDS; rows outside the
-    // call's token range are zero.
-    constexpr int CPR = (D * ESZ) / 16;  // chunks per row
-#pragma unroll
-    for (int c = tid; c < ST * CPR; c += 256) {
-      const int row = c / CPR, part = c % CPR;
-      const int64_t i = slot0 + row - a.t0;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (i >= 0 && i < a.n)
-        v = *reinterpret_cast<const u32x4*>(xb + ((int64_t)s * a.stream_stride + i * a.token_stride) * ESZ + part * 16);
-      *reinterpret_cast<u32x4*>(xs + row * ROWB + part * 16) = v;
-    }
-    __syncthreads();
+  for (;;) {
+    const Span sp = span(st);
+    const int64_t slot0 = sp.slot0;
+    const int b_lo = sp.b_lo, b_hi = sp.b_hi, lo = sp.lo, hi = sp.hi;
+    __syncthreads();  // staged rows visible
 
     if (active) {
-      for (int beta = phase; beta < NB; beta += wpg) {
+      for (int beta = b_lo + phase; beta < b_hi; beta += wpg) {
         f32x16 acc = {};
         const int row = 32 * beta + col;
 #pragma unroll
@@ -163,12 +186,15 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
       }
     }
     // Padding words of the record are zero.
-    const int npad = W - K.used;
-    for (int c = tid; c < ST * npad; c += 256) {
-      const int row = c % ST, w = K.used + c / ST;
-      const int64_t t = slot0 + row;
-      if (t >= a.t0 && t < end) a.packed[rec_word(sbase, t, W, w)] = 0u;
+    const int npad = W - K.used, nrow = hi - lo;
+    for (int c = tid; c < nrow * npad; c += 256) {
+      const int row = lo + c % nrow, w = K.used + c / nrow;
+      a.packed[rec_word(sbase, slot0 + row, W, w)] = 0u;
     }
+    st += gridDim.x;
+    if (st >= n_st) break;
+    __syncthreads();  // every wave is done with the staged rows
+    stage(span(st));
   }
 }
 

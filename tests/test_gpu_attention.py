@@ -30,12 +30,22 @@ def _queries(w, batch, step=0):
     return np.stack([synth.numpy_query(w, b, 0, step) for b in range(batch)])
 
 
-def run_and_check(w, T, batch, ratio, scale=0.0, n_tokens=None, check_heads=None):
-    p = O.Params(ratio=ratio)
+def _fit_encode_with_bits(x_dev, p, t_cap, bits):
+    """Fit, then override every stream's width table before encoding."""
+    codec = S.Codec(sparams(p), x_dev.shape[0])
+    S.spectra_fit_basis(codec, x_dev)
+    if bits is not None:
+        codec.bits.copy_(torch.tensor([bits] * x_dev.shape[0], dtype=torch.uint8))
+    return fit_and_encode(x_dev, p, t_cap, fit=False, codec=codec)
+
+
+def run_and_check(w, T, batch, ratio, scale=0.0, n_tokens=None, check_heads=None, p=None, bits_k=None,
+                  bits_v=None):
+    p = O.Params(ratio=ratio) if p is None else p
     xk, xv = _workload_streams(w, T, batch)
     t_cap = (T + 63) // 64 * 64
-    ck, pk = fit_and_encode(to_device(xk, w.dtype), p, t_cap)
-    cv, pv = fit_and_encode(to_device(xv, w.dtype), p, t_cap)
+    ck, pk = _fit_encode_with_bits(to_device(xk, w.dtype), p, t_cap, bits_k)
+    cv, pv = _fit_encode_with_bits(to_device(xv, w.dtype), p, t_cap, bits_v)
     q = _queries(w, batch)
     n = T if n_tokens is None else n_tokens
     out = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, n, to_device(q, w.dtype), w.n_kv_heads,
@@ -115,3 +125,12 @@ def test_attention_gqa_widths_and_wide_records(n_qh, ratio):
     base = synth.WORKLOADS["llama_layer_4x"]
     w = replace(base, n_kv_heads=2, n_q_heads=2 * n_qh)
     run_and_check(w, 900, 1, ratio)
+
+
+@pytest.mark.parametrize("bits_k,bits_v", [([0, 3, 0, 4], [2, 0, 5, 0]), ([1, 1, 1, 0], [0, 0, 0, 7]),
+                                           ([0, 0, 6, 0], [0, 4, 0, 3])])
+def test_attention_non_prefix_kept_groups(bits_k, bits_v):
+    """Width tables that keep non-adjacent groups: slot order differs from group order."""
+    from dataclasses import replace
+    w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=2, n_q_heads=8)
+    run_and_check(w, 700, 1, 0.0, p=O.Params(budget_bits=32 * 9), bits_k=bits_k, bits_v=bits_v)
