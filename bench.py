@@ -4,20 +4,20 @@ One step = the whole hot path over one batch of the headline 8x workload
 (Llama-3.1-8B KV geometry, 32 layers x 8 KV heads x head_dim 128, 131072
 prefill tokens in bf16, ~17 GB uncompressed):
   1. encode the whole cache (keys and values) into packed records;
-  2. 32 decode steps; in each, for every layer: append the new token's key
-     and value to the packed cache (encoded in the fitted bases), then one
-     decode-step attention per layer (32 query heads, GQA 4:1) read straight
-     from the packed records.
+  2. 32 decode steps; in each, one spectra_decode_step call per layer: append
+     the new token's key and value to the packed cache (encoded in the fitted
+     bases), then decode-step attention (32 query heads, GQA 4:1) read
+     straight from the packed records.
 The basis fit (GPU moments + host eigensolve) is calibration, done once before
-the timed region and reported separately as fit_ms. Each decode step is
-replayed from two HIP graphs captured beforehand (the appends, the attention
-calls), as a serving loop would run it; --eager launches every call from
-Python instead.
+the timed region and reported separately as fit_ms. Each decode step (32
+calls) is replayed from a HIP graph captured beforehand, as a serving loop
+would run it; --eager launches every call from Python instead.
 
 Prints one JSON line. `value` is the step's algorithmic bytes (inputs read,
 records written and read, queries, outputs, codec state) divided by the step
-time. `roofline` covers the dominant kernel, decode-step attention, timed with
-HIP events around every attention call inside the timed region.
+time. `roofline` covers the dominant work, the decode-step calls (append,
+query preparation, split-K scan, combine), timed with HIP events around the
+32 calls of every decode step inside the timed region.
 `cpu_baseline` is the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -58,7 +58,9 @@ def algorithmic_bytes(w, Wk, Wv, n_tokens_attended):
     enc_per_tok = in_b * d                                   # input read per token per stream
     att_records = S_layer * n_tokens_attended * (Wk + Wv) * 4
     att_qo = w.n_seq * w.n_q_heads * d * (in_b + 4)
-    return {"enc_per_token_stream": enc_per_tok, "attn_call": att_records + att_qo + state}
+    append = S_layer * 2 * in_b * d + S_layer * (Wk + Wv) * 4   # new key/value rows in, records out
+    return {"enc_per_token_stream": enc_per_tok, "attn_call": att_records + att_qo + state,
+            "step_call": att_records + att_qo + state + append}
 
 
 def cpu_baseline(w, p, budget_s=20.0):
@@ -175,20 +177,18 @@ def main():
     n_attn_calls = max(n_dec, 0) * L
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
 
-    def appends(s):
-        t = T + s
-        for l in range(L):
-            S.spectra_encode(layer_ck[l], xk[l * H:(l + 1) * H, t:t + 1], t, layer_pk[l], t_cap)
-            S.spectra_encode(layer_cv[l], xv[l * H:(l + 1) * H, t:t + 1], t, layer_pv[l], t_cap)
+    # the new key / value rows of every decode step and layer, [1][H][d] contiguous
+    k_new = [[xk[l * H:(l + 1) * H, T + s].contiguous().view(1, H, d) for l in range(L)] for s in range(n_dec)]
+    v_new = [[xv[l * H:(l + 1) * H, T + s].contiguous().view(1, H, d) for l in range(L)] for s in range(n_dec)]
 
-    def attentions(s):
+    def decode_steps(s):
+        # one call per layer: append the new key and value at slot T + s, attend over T + s + 1 slots
         for l in range(L):
-            S.spectra_decode_attention(layer_ck[l], layer_cv[l], layer_pk[l], layer_pv[l], t_cap, T + s + 1,
-                                       qs[s, l], H, out=outs[l], workspace=ws)
+            S.spectra_decode_step(layer_ck[l], layer_cv[l], layer_pk[l], layer_pv[l], t_cap, T + s, k_new[s][l],
+                                  v_new[s][l], qs[s, l], H, out=outs[l], workspace=ws)
 
-    # Decode steps run as HIP graphs (one for the 2L appends, one for the L attention
-    # calls of each step), as a serving loop would, so host launch overhead is not
-    # timed; --eager launches every call from Python instead.
+    # Each decode step (L calls) runs as one HIP graph, as a serving loop would, so
+    # host launch overhead is not timed; --eager launches every call from Python.
     graphs = None
 
     def step(record):
@@ -199,16 +199,12 @@ def main():
         e1.record()
         att = []
         for s in range(n_dec):
-            if graphs is None:
-                appends(s)
-            else:
-                graphs[s][0].replay()
             a0 = ev()
             a0.record()
             if graphs is None:
-                attentions(s)
+                decode_steps(s)
             else:
-                graphs[s][1].replay()
+                graphs[s].replay()
             a1 = ev()
             a1.record()
             att.append((a0, a1, T + s + 1))
@@ -221,12 +217,10 @@ def main():
     if not args.eager:
         graphs = []
         for s in range(n_dec):
-            pair = (torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph())
-            with torch.cuda.graph(pair[0]):
-                appends(s)
-            with torch.cuda.graph(pair[1]):
-                attentions(s)
-            graphs.append(pair)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                decode_steps(s)
+            graphs.append(g)
         torch.cuda.synchronize()
         step(None)  # one untimed pass through the replays
         torch.cuda.synchronize()
@@ -243,9 +237,8 @@ def main():
     # ---- derived throughput ----
     ab = lambda n: algorithmic_bytes(w, Wk, Wv, n)  # noqa: E731
     enc_bytes = Sn * T * 2 * d * (2 if w.dtype == "bf16" else 4) + Sn * T * (Wk + Wv) * 4 + Sn * 2 * (d * d * 4 + d * 4)
-    app_bytes = n_dec * Sn * (2 * d * (2 if w.dtype == "bf16" else 4) + (Wk + Wv) * 4)
-    att_bytes_calls = [ab(n)["attn_call"] for s in range(n_dec) for n in [T + s + 1] for _ in range(L)]
-    step_bytes = enc_bytes + app_bytes + sum(att_bytes_calls)
+    att_bytes_calls = [ab(n)["step_call"] for s in range(n_dec) for n in [T + s + 1] for _ in range(L)]
+    step_bytes = enc_bytes + sum(att_bytes_calls)
     enc_ms = float(np.mean([r[0][0].elapsed_time(r[0][1]) for r in rec]))
     att_ms_blocks = [a0.elapsed_time(a1) for r in rec for (a0, a1, _) in r[1]]
     att_call_ms = float(np.sum(att_ms_blocks)) / max(len(att_ms_blocks) * L, 1)
@@ -276,13 +269,13 @@ def main():
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
         "encode": {"ms": round(enc_ms, 3), "GBps": round(enc_bytes / (enc_ms * 1e-3) / 1e9, 1),
                    "frac": round(enc_bytes / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
-        "decode_attention": {"ms_per_layer_call": round(att_call_ms, 4), "GBps": round(att_gbps, 1),
+        "decode_step": {"ms_per_layer_call": round(att_call_ms, 4), "GBps": round(att_gbps, 1),
                              "frac": round(att_gbps / HBM_PEAK_GBPS, 4),
                              "cache_tokens_per_s": round(tokens_per_call / (att_call_ms * 1e-3), 1),
                              "generated_tokens_per_s": round(1.0 / (att_call_ms * 1e-3 * L), 2)},
         "roofline": {"bound": "hbm", "achieved": round(att_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "decode_attention (query rotation + split-K scan + combine), per layer call",
+                     "kernel": "decode_step (append + query prep, split-K scan, combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
         "decode_launch": "eager" if args.eager else "hip_graph",
         "fit_ms": round(fit_s * 1e3, 1),

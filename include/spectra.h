@@ -169,6 +169,22 @@ spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_c
                                         void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * One decode step (Sec. 3.3: append-only latent cache, then App. E attention):
+ * the new key and value of every stream, k_new[b][kv][c] and v_new[b][kv][c]
+ * (device, dtype kv_dt, contiguous, 16-byte aligned), are encoded into record
+ * slot t of packed_k / packed_v with the fitted state (the records equal those
+ * spectra_encode writes for the same token), then attention runs over slots
+ * [0, t + 1) exactly as spectra_decode_attention with n_tokens = t + 1.
+ * 0 <= t < t_capacity. Workspace: spectra_attention_workspace_bytes(batch,
+ * n_q_heads, n_kv_heads, t + 1) bytes. Asynchronous.
+ * ------------------------------------------------------------------------- */
+spectra_status spectra_decode_step(const spectra_codec* ck, const spectra_codec* cv, uint32_t* packed_k,
+                                   uint32_t* packed_v, int64_t t_capacity, int64_t t, const void* k_new,
+                                   const void* v_new, spectra_dtype kv_dt, const void* q, spectra_dtype q_dt,
+                                   int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, float softmax_scale,
+                                   float* out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Host-side pieces of the fit, exported so they can be checked without a GPU.
  * ------------------------------------------------------------------------- */
 

@@ -158,6 +158,27 @@ def spectra_decode_attention(ck: Codec, cv: Codec, packed_k, packed_v, t_capacit
     return out
 
 
+def spectra_decode_step(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, t: int, k_new, v_new, q,
+                        n_kv_heads: int, softmax_scale: float = 0.0, out=None, workspace=None, stream=None):
+    """Append k_new, v_new [batch, n_kv_heads, d] at record slot t, then attend over slots [0, t]:
+    q [batch, n_q_heads, d] -> float32 [batch, n_q_heads, d]."""
+    import torch
+    batch, n_q_heads, d = q.shape
+    assert q.is_contiguous() and k_new.is_contiguous() and v_new.is_contiguous()
+    assert k_new.dtype == v_new.dtype and tuple(k_new.shape) == tuple(v_new.shape) == (batch, n_kv_heads, d)
+    if out is None:
+        out = torch.empty((batch, n_q_heads, d), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        need = spectra_attention_workspace_bytes(batch, n_q_heads, n_kv_heads, t + 1)
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    check(_lib.get().spectra_decode_step(ctypes.byref(ck.struct), ctypes.byref(cv.struct), packed_k.data_ptr(),
+                                         packed_v.data_ptr(), int(t_capacity), int(t), k_new.data_ptr(),
+                                         v_new.data_ptr(), _dtype_code(k_new), q.data_ptr(), _dtype_code(q), batch,
+                                         n_q_heads, int(n_kv_heads), float(softmax_scale), out.data_ptr(),
+                                         workspace.data_ptr(), workspace.numel(), _stream(stream)))
+    return out
+
+
 def spectra_pack_codes(codec: Codec, codes, meta, packed, t_capacity: int, stream=None) -> None:
     check(_lib.get().spectra_pack_codes(ctypes.byref(codec.struct), codes.data_ptr(), meta.data_ptr(),
                                         codes.shape[1], packed.data_ptr(), int(t_capacity), _stream(stream)))

@@ -215,32 +215,36 @@ size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32
          attention_partial_floats(batch, n_q_heads, nch) * sizeof(float);
 }
 
-spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_codec* cv, const uint32_t* packed_k,
-                                        const uint32_t* packed_v, int64_t t_capacity, int64_t n_tokens, const void* q,
-                                        spectra_dtype q_dt, int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
-                                        float softmax_scale, float* out, void* workspace, size_t ws_bytes, void* stream) {
-  spectra_status st = check_codec(ck, "decode_attention keys");
+// Checks shared by decode_attention and decode_step; fills everything of AttnArgs
+// except the decode-step append fields.
+static spectra_status prepare_attention(const char* name, const spectra_codec* ck, const spectra_codec* cv,
+                                        const uint32_t* packed_k, const uint32_t* packed_v, int64_t t_capacity,
+                                        int64_t n_tokens, const void* q, spectra_dtype q_dt, int32_t batch,
+                                        int32_t n_q_heads, int32_t n_kv_heads, float softmax_scale, float* out,
+                                        void* workspace, size_t ws_bytes, AttnArgs* args) {
+  spectra_status st = check_codec(ck, name);
   if (st != SPECTRA_OK) return st;
-  st = check_codec(cv, "decode_attention values");
+  st = check_codec(cv, name);
   if (st != SPECTRA_OK) return st;
   if (batch <= 0 || n_kv_heads <= 0 || n_q_heads <= 0 || n_q_heads % n_kv_heads != 0)
-    return fail(SPECTRA_EINVAL, "need batch > 0 and n_q_heads a positive multiple of n_kv_heads");
-  if (n_q_heads / n_kv_heads > 16) return fail(SPECTRA_EUNSUPPORTED, "more than 16 query heads per kv head");
-  if (batch > 65535 || n_kv_heads > 65535) return fail(SPECTRA_EINVAL, "batch or n_kv_heads too large");
+    return fail(SPECTRA_EINVAL, "%s: need batch > 0 and n_q_heads a positive multiple of n_kv_heads", name);
+  if (n_q_heads / n_kv_heads > 16) return fail(SPECTRA_EUNSUPPORTED, "%s: more than 16 query heads per kv head", name);
+  if (batch > 65535 || n_kv_heads > 65535) return fail(SPECTRA_EINVAL, "%s: batch or n_kv_heads too large", name);
   if ((int64_t)batch * n_kv_heads > ck->n_streams || (int64_t)batch * n_kv_heads > cv->n_streams)
-    return fail(SPECTRA_EINVAL, "batch * n_kv_heads exceeds the codec's streams");
-  if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "attention needs n_tokens >= 1");
+    return fail(SPECTRA_EINVAL, "%s: batch * n_kv_heads exceeds the codec's streams", name);
+  if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "%s: attention needs n_tokens >= 1", name);
   st = check_slots(0, n_tokens, t_capacity);
   if (st != SPECTRA_OK) return st;
-  if (q_dt != SPECTRA_F32 && q_dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "q dtype %d not supported", (int)q_dt);
-  if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "q/out must be non-null and aligned");
+  if (q_dt != SPECTRA_F32 && q_dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "%s: q dtype %d not supported", name, (int)q_dt);
+  if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "%s: q/out must be non-null and aligned", name);
   if ((ck->record_words > 0 && (!packed_k || !aligned(packed_k, 4))) ||
       (cv->record_words > 0 && (!packed_v || !aligned(packed_v, 4))))
-    return fail(SPECTRA_EINVAL, "packed_k / packed_v must be non-null and 4-byte aligned");
-  if (!(softmax_scale == softmax_scale) || std::isinf(softmax_scale)) return fail(SPECTRA_EINVAL, "softmax_scale not finite");
+    return fail(SPECTRA_EINVAL, "%s: packed_k / packed_v must be non-null and 4-byte aligned", name);
+  if (!(softmax_scale == softmax_scale) || std::isinf(softmax_scale))
+    return fail(SPECTRA_EINVAL, "%s: softmax_scale not finite", name);
   const size_t need = spectra_attention_workspace_bytes(batch, n_q_heads, n_kv_heads, n_tokens);
-  if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "attention workspace must be 256-byte aligned");
-  if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "attention workspace %zu < %zu bytes", ws_bytes, need);
+  if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "%s: workspace must be 256-byte aligned", name);
+  if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "%s: workspace %zu < %zu bytes", name, ws_bytes, need);
   AttnArgs a{};
   a.packed_k = packed_k;
   a.packed_v = packed_v;
@@ -249,6 +253,7 @@ spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_c
   a.basis_k = ck->basis;
   a.basis_v = cv->basis;
   a.mean_v = cv->mean;
+  a.mean_k = ck->mean;
   a.bits_k = ck->bits;
   a.bits_v = cv->bits;
   a.q = q;
@@ -266,8 +271,44 @@ spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_c
   a.partial = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
                                        round256(attention_qprep_floats(batch, n_q_heads, n_kv_heads) * sizeof(float)));
   a.out = out;
+  *args = a;
+  return SPECTRA_OK;
+}
+
+spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_codec* cv, const uint32_t* packed_k,
+                                        const uint32_t* packed_v, int64_t t_capacity, int64_t n_tokens, const void* q,
+                                        spectra_dtype q_dt, int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        float softmax_scale, float* out, void* workspace, size_t ws_bytes, void* stream) {
+  AttnArgs a{};
+  const spectra_status st = prepare_attention("decode_attention", ck, cv, packed_k, packed_v, t_capacity, n_tokens, q,
+                                              q_dt, batch, n_q_heads, n_kv_heads, softmax_scale, out, workspace,
+                                              ws_bytes, &a);
+  if (st != SPECTRA_OK) return st;
   hipError_t e = launch_attention(a, (hipStream_t)stream);
   return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "attention launch");
+}
+
+spectra_status spectra_decode_step(const spectra_codec* ck, const spectra_codec* cv, uint32_t* packed_k,
+                                   uint32_t* packed_v, int64_t t_capacity, int64_t t, const void* k_new,
+                                   const void* v_new, spectra_dtype kv_dt, const void* q, spectra_dtype q_dt,
+                                   int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, float softmax_scale, float* out,
+                                   void* workspace, size_t ws_bytes, void* stream) {
+  if (t < 0 || t >= t_capacity) return fail(SPECTRA_EINVAL, "decode_step: slot t=%lld outside [0, t_capacity)", (long long)t);
+  AttnArgs a{};
+  spectra_status st = prepare_attention("decode_step", ck, cv, packed_k, packed_v, t_capacity, t + 1, q, q_dt, batch,
+                                        n_q_heads, n_kv_heads, softmax_scale, out, workspace, ws_bytes, &a);
+  if (st != SPECTRA_OK) return st;
+  if (kv_dt != SPECTRA_F32 && kv_dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "decode_step: dtype %d not supported", (int)kv_dt);
+  if (!k_new || !v_new || !aligned(k_new, 16) || !aligned(v_new, 16))
+    return fail(SPECTRA_EINVAL, "decode_step: k_new / v_new must be non-null and 16-byte aligned");
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.app_k = packed_k;
+  a.app_v = packed_v;
+  a.t_new = t;
+  a.app_f32 = kv_dt == SPECTRA_F32;
+  hipError_t e = launch_decode_step(a, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "decode_step launch");
 }
 
 spectra_status spectra_pack_codes(const spectra_codec* c, const uint8_t* codes, const uint32_t* meta, int64_t n_tokens,

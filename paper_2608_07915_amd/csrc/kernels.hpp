@@ -68,6 +68,15 @@ struct AttnArgs {
   float scale_log2;      // softmax scale * log2(e)
   int32_t n_chunks;      // split of the token range per (batch, kv head)
   int32_t tiles_per_chunk;
+  // decode step only: the new token of every stream is encoded into slot t_new
+  // of app_k / app_v (the same caches as packed_k / packed_v) before attention
+  const void* k_new;     // [batch][n_kv_heads][128], fp32 if app_f32 else bf16
+  const void* v_new;
+  const float* mean_k;
+  uint32_t* app_k;
+  uint32_t* app_v;
+  int64_t t_new;
+  int32_t app_f32;
   float* qprep;          // workspace: rotated queries and MFMA operands
   float* partial;        // workspace: per-chunk softmax partials
   float* out;            // [batch][n_q_heads][128]
@@ -81,6 +90,8 @@ hipError_t launch_decode(const spectra_dev::DecodeArgs& a, hipStream_t st);
 hipError_t launch_pack_codes(const spectra_dev::PackArgs& a, bool unpack, hipStream_t st);
 hipError_t launch_gram(const spectra_dev::GramArgs& a, bool f32_input, hipStream_t st);
 hipError_t launch_attention(const spectra_dev::AttnArgs& a, hipStream_t st);
+// Same, with the new token of every stream appended first (a.k_new != nullptr).
+hipError_t launch_decode_step(const spectra_dev::AttnArgs& a, hipStream_t st);
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
 size_t attention_qprep_floats(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads);
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);

@@ -28,6 +28,7 @@
 // prefetched into registers; the four wavefronts merge their online-softmax
 // states in LDS and write one partial per chunk; combine_kernel merges chunks.
 #include "device_common.hpp"
+#include "encode_dev.hpp"
 #include "kernels.hpp"
 #include "kplan.hpp"
 
@@ -89,16 +90,69 @@ __device__ __forceinline__ float wave_max_all(float v) {
 
 
 // ---------------------------------------------------------------------------
+// Decode-step append (APP = 1: bf16 rows, 2: fp32 rows): the new key and value
+// of stream s go into slot t_new exactly as the encode kernel would write them
+// (same staging, same MFMA sequence per token). Waves 0..3 take the kept key
+// groups, waves 4..7 the kept value groups; the token sits in LDS row 0 of a
+// 32-row block whose other rows are zero (their columns are discarded).
+// ---------------------------------------------------------------------------
+template <int APP>
+__device__ __forceinline__ void append_token(const AttnArgs& a, int s, int tid) {
+  constexpr bool F32 = APP == 2;
+  constexpr int ESZ = F32 ? 4 : 2;
+  constexpr int ROWB = F32 ? (512 + 16) : (256 + 16);
+  constexpr int CPR = (D * ESZ) / 16;
+  __shared__ __attribute__((aligned(16))) uint8_t xs[2][32 * ROWB];
+  for (int e = tid; e < 2 * 32 * CPR; e += 512) {
+    const int which = e / (32 * CPR), row = (e / CPR) % 32, part = e % CPR;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row == 0) {
+      const char* src = reinterpret_cast<const char*>(which ? a.v_new : a.k_new);
+      v = *reinterpret_cast<const u32x4*>(src + (int64_t)s * D * ESZ + part * 16);
+    }
+    *reinterpret_cast<u32x4*>(&xs[which][row * ROWB + part * 16]) = v;
+  }
+  __syncthreads();
+  const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  const int which = wave >> 2, slot = wave & 3;
+  const Kept K = read_kept((which ? a.bits_v : a.bits_k) + (int64_t)s * NG);
+  const int W = which ? a.Wv : a.Wk;
+  if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
+  uint32_t* packed = which ? a.app_v : a.app_k;
+  const int64_t sbase = (int64_t)s * a.t_cap * W;
+  if (slot < K.n) {
+    bf16x8 Va[3][8];
+    float mv[16];
+    load_group_operands((which ? a.basis_v : a.basis_k) + (int64_t)s * D * D, (which ? a.mean_v : a.mean_k) + (int64_t)s * D,
+                        pick4(K.grp, slot), col, h, Va, mv);
+    encode_block<F32, ROWB>(xs[which], 0, col, h, Va, mv, a.t_new, a.t_new, a.t_new + 1, sbase, W, slot,
+                            pick4(K.bits, slot), pick4(K.pay, slot), packed);
+  }
+  // padding words of the record are zero
+  if (slot == 0 && lane < W - K.used) packed[rec_word(sbase, a.t_new, W, K.used + lane)] = 0u;
+}
+
+// ---------------------------------------------------------------------------
 // Query preparation, once per step: one workgroup per (kv head, sequence) writes
 // E2 = 2^-E, Qbar[h][g] = sum_{j in g} q'_hj and the score-MFMA A operands
-// [quad][g][k][part][r] = fp16 parts of q'_{4quad+r}[32g + 4k + i] * 2^E.
+// [quad][slot][m][row][hi k0..k3, lo k0..k3] (see score_slot). For a decode step
+// (APP != 0) the grid has a second layer, z = 0, whose workgroups append the new
+// token of their stream meanwhile.
 // ---------------------------------------------------------------------------
+template <int APP>
 __global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
   __shared__ float qs[16][D];
   __shared__ float part_s[4][16][D];
   __shared__ float red_s[8];
   const int kv = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int s = b * a.n_kv_heads + kv;
+  if constexpr (APP != 0) {
+    // z = 0: append the new key and value; z = 1: query preparation (independent work)
+    if (blockIdx.z == 0) {
+      append_token<APP>(a, s, tid);
+      return;
+    }
+  }
   const int nqh = a.n_qh;
   const uint32_t bwk = *reinterpret_cast<const uint32_t*>(a.bits_k + (int64_t)s * NG);
   for (int e = tid; e < 16 * D; e += 512) {
@@ -733,8 +787,7 @@ static void launch_nq(const AttnArgs& a, hipStream_t st) {
     launch_nq_pw<NQ, 0>(a, st);
 }
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(qprep_kernel, dim3(a.n_kv_heads, a.batch), dim3(512), 0, st, a);
+static hipError_t launch_scan_combine(const AttnArgs& a, hipStream_t st) {
   switch ((a.n_qh + 3) / 4) {
     case 1: launch_nq<1>(a, st); break;
     case 2: launch_nq<2>(a, st); break;
@@ -745,6 +798,19 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(combine_kernel, dim3(a.n_q_heads, a.batch), dim3(1024), 0, st, a);
   return hipGetLastError();
+}
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(qprep_kernel<0>, dim3(a.n_kv_heads, a.batch), dim3(512), 0, st, a);
+  return launch_scan_combine(a, st);
+}
+
+hipError_t launch_decode_step(const AttnArgs& a, hipStream_t st) {
+  if (a.app_f32)
+    hipLaunchKernelGGL(qprep_kernel<2>, dim3(a.n_kv_heads, a.batch, 2), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL(qprep_kernel<1>, dim3(a.n_kv_heads, a.batch, 2), dim3(512), 0, st, a);
+  return launch_scan_combine(a, st);
 }
 
 }  // namespace spectra

@@ -11,38 +11,10 @@
 // Decode (Sec. 3.3, Mode A): x_hat = sum_G (z_G 1 + s_G q_G) V_G^T + m V^T, with the
 // q_G V_G^T contraction on MFMA (codes are exact small integers in bf16).
 #include "device_common.hpp"
+#include "encode_dev.hpp"
 #include "kernels.hpp"
 
 namespace spectra_dev {
-
-// ---------------------------------------------------------------------------
-// Quantization of 16 centered coefficients of one token (one lane half); the
-// two halves of a group exchange min/max. Returns codes and the metadata word.
-// ---------------------------------------------------------------------------
-template <int B>
-__device__ __forceinline__ uint32_t quantize16(const float (&c)[16], uint32_t (&q)[16]) {
-  float lo = c[0], hi = c[0];
-#pragma unroll
-  for (int j = 1; j < 16; ++j) {
-    lo = __builtin_fminf(lo, c[j]);
-    hi = __builtin_fmaxf(hi, c[j]);
-  }
-  lo = __builtin_fminf(lo, __shfl_xor(lo, 32));
-  hi = __builtin_fmaxf(hi, __shfl_xor(hi, 32));
-  constexpr float LEV = (float)((1 << B) - 1);
-  const uint32_t z16 = f2h_sat(lo);
-  const float z = h2f(z16);
-  const uint32_t s16 = f2h_sat(__builtin_fmaxf(hi - z, 0.0f) / LEV);
-  const float s = h2f(s16);
-  const float rinv = s > 0.0f ? 1.0f / s : 0.0f;
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    float u = __builtin_rintf((c[j] - z) * rinv);
-    u = __builtin_fminf(__builtin_fmaxf(u, 0.0f), LEV);
-    q[j] = (uint32_t)u;
-  }
-  return s16 | (z16 << 16);
-}
 
 // ---------------------------------------------------------------------------
 // Encode
@@ -112,28 +84,9 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
   const int gbits = pick4(K.bits, slot);
   const int gpay = pick4(K.pay, slot);
 
-  // Basis columns of this wave's group as MFMA A operands: row r of the 32x32 tile
-  // is in-group coefficient jj(r) so that lane half h ends up holding 16h..16h+15.
   bf16x8 Va[3][8];
   float mv[16];
-  if (active) {
-    const int r = col;
-    const int jj = 16 * ((r & 7) >> 2) + 4 * (r >> 3) + (r & 3);
-    const float* Vs = a.basis + (int64_t)s * D * D;
-    const int cidx = G * grp + jj;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      uint32_t p0[8], p1[8], p2[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) split3(Vs[(16 * k + 8 * h + i) * D + cidx], p0[i], p1[i], p2[i]);
-      Va[0][k] = as_bf16x8(u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])});
-      Va[1][k] = as_bf16x8(u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])});
-      Va[2][k] = as_bf16x8(u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])});
-    }
-    const float* ms = a.mean + (int64_t)s * D + G * grp + 16 * h;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) mv[j] = ms[j];
-  }
+  if (active) load_group_operands(a.basis + (int64_t)s * D * D, a.mean + (int64_t)s * D, grp, col, h, Va, mv);
 
   for (;;) {
     const Span sp = span(st);
@@ -142,48 +95,8 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
     __syncthreads();  // staged rows visible
 
     if (active) {
-      for (int beta = b_lo + phase; beta < b_hi; beta += wpg) {
-        f32x16 acc = {};
-        const int row = 32 * beta + col;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          if constexpr (!F32IN) {
-            const bf16x8 xb8 = as_bf16x8(*reinterpret_cast<const u32x4*>(xs + row * ROWB + (16 * k + 8 * h) * 2));
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[0][k], xb8, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[1][k], xb8, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[2][k], xb8, acc, 0, 0, 0);
-          } else {
-            const float* xr = reinterpret_cast<const float*>(xs + row * ROWB) + 16 * k + 8 * h;
-            uint32_t q0[8], q1[8], q2[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) split3(xr[i], q0[i], q1[i], q2[i]);
-            const bf16x8 x0 = as_bf16x8(u32x4{pack2(q0[0], q0[1]), pack2(q0[2], q0[3]), pack2(q0[4], q0[5]), pack2(q0[6], q0[7])});
-            const bf16x8 x1 = as_bf16x8(u32x4{pack2(q1[0], q1[1]), pack2(q1[2], q1[3]), pack2(q1[4], q1[5]), pack2(q1[6], q1[7])});
-            const bf16x8 x2 = as_bf16x8(u32x4{pack2(q2[0], q2[1]), pack2(q2[2], q2[3]), pack2(q2[4], q2[5]), pack2(q2[6], q2[7])});
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[0][k], x0, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[0][k], x1, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[1][k], x0, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[0][k], x2, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[1][k], x1, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[2][k], x0, acc, 0, 0, 0);
-          }
-        }
-        // Lane (h, col) now holds coefficients 16h..16h+15 of token slot0 + row.
-        float c[16];
-#pragma unroll
-        for (int j = 0; j < 16; ++j) c[j] = acc[j] - mv[j];
-        const int64_t t = slot0 + row;
-        const bool valid = t >= a.t0 && t < end;
-        const int64_t base = rec_word(sbase, t, W, 0);
-        with_bits(gbits, [&](auto bc) {
-          constexpr int B = decltype(bc)::value;
-          uint32_t q[16], P[4];
-          const uint32_t meta = quantize16<B>(c, q);
-          pack16<B>(q, P);
-          if (h == 0 && valid) a.packed[base + (int64_t)slot * TILE] = meta;
-          store_payload<B>(a.packed, base, gpay, P, h, valid);
-        });
-      }
+      for (int beta = b_lo + phase; beta < b_hi; beta += wpg)
+        encode_block<F32IN, ROWB>(xs, beta, col, h, Va, mv, slot0, a.t0, end, sbase, W, slot, gbits, gpay, a.packed);
     }
     // Padding words of the record are zero.
     const int npad = W - K.used, nrow = hi - lo;

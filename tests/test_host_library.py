@@ -156,6 +156,15 @@ def test_argument_errors_return_before_any_launch(lib):
     assert lib.spectra_decode_attention(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 8, 256, 1, 1, 4, 4, 0.0,
                                         256, 256, 16, None) == -4
     assert lib.spectra_status_string(-4) == b"workspace too small"
+    # decode step: slot outside the capacity, misaligned new rows, too-small workspace
+    ws = lib.spectra_attention_workspace_bytes(1, 4, 4, 9)
+    assert lib.spectra_decode_step(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 64, 256, 256, 1, 256, 1, 1, 4, 4,
+                                   0.0, 256, 256, ws, None) == -1
+    assert lib.spectra_decode_step(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 8, 264, 256, 1, 256, 1, 1, 4, 4,
+                                   0.0, 256, 256, ws, None) == -1
+    assert b"16-byte" in lib.spectra_last_error()
+    assert lib.spectra_decode_step(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 8, 256, 256, 1, 256, 1, 1, 4, 4,
+                                   0.0, 256, 256, 16, None) == -4
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
