@@ -33,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+CALIB_BYTES = 256 << 20
 METRIC = "KV encode GB/s + compressed decode-attn tokens/s, % of HBM peak, at 8x"
 
 
@@ -46,6 +47,8 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
     ap.add_argument("--eager", action="store_true", help="launch decode steps from Python instead of HIP graphs")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 256 MiB device-to-device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -233,6 +236,16 @@ def main():
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
+
+    if args.copy_calibration:
+        # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE counters scale the
+        # counters of the codec kernels to bytes.
+        src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- derived throughput ----
     ab = lambda n: algorithmic_bytes(w, Wk, Wv, n)  # noqa: E731

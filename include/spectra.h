@@ -156,7 +156,8 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
  * computed as q' = scale q V_K once, scores over the kept key coefficients
  * (the constant q' . m_K cancels in the softmax), value accumulation over the
  * kept value coefficients, then one inverse rotation (a + m_V) V_V^T.
- * softmax_scale <= 0 selects 1/sqrt(d). n_q_heads / n_kv_heads <= 16.
+ * softmax_scale <= 0 selects 1/sqrt(d). n_q_heads / n_kv_heads <= 16;
+ * t_capacity * record_words < 2^31 for both codecs.
  * Workspace: device, spectra_attention_workspace_bytes bytes. Asynchronous.
  * ------------------------------------------------------------------------- */
 size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,

@@ -235,6 +235,8 @@ static spectra_status prepare_attention(const char* name, const spectra_codec* c
   if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "%s: attention needs n_tokens >= 1", name);
   st = check_slots(0, n_tokens, t_capacity);
   if (st != SPECTRA_OK) return st;
+  if (t_capacity * (int64_t)std::max(ck->record_words, cv->record_words) >= ((int64_t)1 << 31))
+    return fail(SPECTRA_EINVAL, "%s: t_capacity * record words must stay below 2^31 per stream", name);
   if (q_dt != SPECTRA_F32 && q_dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "%s: q dtype %d not supported", name, (int)q_dt);
   if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "%s: q/out must be non-null and aligned", name);
   if ((ck->record_words > 0 && (!packed_k || !aligned(packed_k, 4))) ||

@@ -49,6 +49,8 @@ constexpr int QA_QUAD = NG * QA_SLOT;
 constexpr int QP = 4 + 16 * 4 + 4 * QA_QUAD;  // floats per (sequence, kv head) of prepared query data
 constexpr int WAVES = 4;
 constexpr int WROW = 72;  // bf16 per weight row (64 tokens + pad: spreads rows over LDS banks)
+constexpr int TROW = 68;  // uint32 per staged record-word row (64 tokens + pad: distinct words of one
+                          // token group fall on distinct LDS banks)
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -264,32 +266,40 @@ __global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
 __host__ __device__ constexpr int attn_wt_bytes(int nq) { return WAVES * NG * (8 * nq) * WROW * 2; }
 
 // ---------------------------------------------------------------------------
-// Value-code operand: 8 codes of in-group coefficient n (bit offset off = n*b in
-// the group payload starting at record word `pay`) for 8 consecutive tokens, as
-// bf16. CLS 0: b in {1,2,4} (a code never crosses a byte); CLS 1: b in {3,5,6,7};
-// both give 128 + c. CLS 2: b = 8, exact c.
+// Value-code operands: the codes of in-group coefficients n and n + 1 (bit
+// offsets off = n*b and off + b in the group payload at record word `pay`) for
+// 8 consecutive tokens, as bf16 pairs. CLS 0: b in {1,2,4} (both codes in one
+// byte: one byte gather per token pair); CLS 1: b in {3,5,6,7} (one 32-bit
+// funnel-shift window per token holds both); both give 128 + c, the OR with the
+// exponent of 128 (`magic`, held in a VGPR) fused into the mask. CLS 2: b = 8,
+// exact c.
 // ---------------------------------------------------------------------------
 template <int CLS>
-__device__ __forceinline__ u32x4 value_codes(const uint32_t* __restrict__ vt, int pay, int used, int b, int off,
-                                             int tok0) {
+__device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, int pay, int used, int b, int off,
+                                             int tok0, uint32_t magic, u32x4& r0, u32x4& r1) {
   const int w = pay + (off >> 5), o = off & 31;
-  const u32x4 a0 = *reinterpret_cast<const u32x4*>(vt + w * 64 + tok0);
-  const u32x4 a1 = *reinterpret_cast<const u32x4*>(vt + w * 64 + tok0 + 4);
+  const u32x4 a0 = *reinterpret_cast<const u32x4*>(vt + w * TROW + tok0);
+  const u32x4 a1 = *reinterpret_cast<const u32x4*>(vt + w * TROW + tok0 + 4);
   const uint32_t M = (1u << b) - 1u;
   const uint32_t MM = M | (M << 16);
-  u32x4 r;
   if constexpr (CLS == 0) {
-    // gather byte k of two tokens' words with one permute, then shift and mask
+    // byte k of two tokens' words in both halves of one register, then shift and mask
     const uint32_t k = (uint32_t)o >> 3, sh = (uint32_t)o & 7u;
     const uint32_t sel = k * 0x00000101u + (4u + k) * 0x01010000u;
-    r[0] = ((__builtin_amdgcn_perm(a0[1], a0[0], sel) >> sh) & MM) | 0x43004300u;
-    r[1] = ((__builtin_amdgcn_perm(a0[3], a0[2], sel) >> sh) & MM) | 0x43004300u;
-    r[2] = ((__builtin_amdgcn_perm(a1[1], a1[0], sel) >> sh) & MM) | 0x43004300u;
-    r[3] = ((__builtin_amdgcn_perm(a1[3], a1[2], sel) >> sh) & MM) | 0x43004300u;
+    uint32_t y[4];
+    y[0] = __builtin_amdgcn_perm(a0[1], a0[0], sel);
+    y[1] = __builtin_amdgcn_perm(a0[3], a0[2], sel);
+    y[2] = __builtin_amdgcn_perm(a1[1], a1[0], sel);
+    y[3] = __builtin_amdgcn_perm(a1[3], a1[2], sel);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r0[i] = ((y[i] >> sh) & MM) | magic;
+      r1[i] = ((y[i] >> (sh + b)) & MM) | magic;
+    }
   } else {
-    const int wn = (w + 1 < used) ? w + 1 : w;  // the next word only matters when the code straddles
-    const u32x4 b0 = *reinterpret_cast<const u32x4*>(vt + wn * 64 + tok0);
-    const u32x4 b1 = *reinterpret_cast<const u32x4*>(vt + wn * 64 + tok0 + 4);
+    const int wn = (w + 1 < used) ? w + 1 : w;  // the next word only matters when a code straddles
+    const u32x4 b0 = *reinterpret_cast<const u32x4*>(vt + wn * TROW + tok0);
+    const u32x4 b1 = *reinterpret_cast<const u32x4*>(vt + wn * TROW + tok0 + 4);
     uint32_t c[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -298,13 +308,19 @@ __device__ __forceinline__ u32x4 value_codes(const uint32_t* __restrict__ vt, in
     }
     if constexpr (CLS == 2) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = int_to_bf16_pair(c[2 * i] & 0xFFu, c[2 * i + 1] & 0xFFu);
+      for (int i = 0; i < 4; ++i) {
+        r0[i] = int_to_bf16_pair(c[2 * i] & 0xFFu, c[2 * i + 1] & 0xFFu);
+        r1[i] = int_to_bf16_pair((c[2 * i] >> 8) & 0xFFu, (c[2 * i + 1] >> 8) & 0xFFu);
+      }
     } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = (__builtin_amdgcn_perm(c[2 * i + 1], c[2 * i], 0x05040100u) & MM) | 0x43004300u;
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t y = __builtin_amdgcn_perm(c[2 * i + 1], c[2 * i], 0x05040100u);
+        r0[i] = (y & MM) | magic;
+        r1[i] = ((y >> b) & MM) | magic;
+      }
     }
   }
-  return r;
 }
 
 // ---------------------------------------------------------------------------
@@ -318,17 +334,21 @@ __device__ __forceinline__ void score_slot(const uint32_t* __restrict__ kt, int 
                                            const uint32_t* __restrict__ qsl, int r4, f32x4 (&dh)[NQ],
                                            f32x4 (&dl)[NQ]) {
   constexpr KPlan P = make_kplan(B);
+  // the exponent of 1024 in both halves, kept in a VGPR so that mask-and-or is one
+  // v_and_or_b32 (its mask then comes from an SGPR)
+  uint32_t magic = 0x64006400u;
+  asm volatile("" : "+v"(magic));
   uint32_t reg0 = 0u;
   int opi = 0;
 #pragma unroll
   for (int w = 0; w < B; ++w) {
-    const uint32_t x = kt[(pay + w) * 64 + lane];
+    const uint32_t x = kt[(pay + w) * TROW + lane];
     const uint32_t x6 = x >> 6;
 #pragma unroll
     for (int i = 0; i < P.word_ops[w]; ++i, ++opi) {
       // (field | exponent of 1024) - 1024: the field as a normal fp16 integer, both halves
       const uint32_t v = __builtin_bit_cast(
-          uint32_t, __builtin_bit_cast(f16x2, ((P.op[opi].shifted ? x6 : x) & P.op[opi].mask) | 0x64006400u) -
+          uint32_t, __builtin_bit_cast(f16x2, ((P.op[opi].shifted ? x6 : x) & P.op[opi].mask) | magic) -
                         f16x2{(_Float16)1024.0f, (_Float16)1024.0f});
       if ((opi & 1) == 0) {
         reg0 = v;
@@ -349,9 +369,9 @@ __device__ __forceinline__ void score_slot(const uint32_t* __restrict__ kt, int 
 
 // ---------------------------------------------------------------------------
 // Split-K partial. NQ = query-head quads (n_qh <= 4 NQ); PW = prefetched record
-// words per tile (>= max(W_k, W_v)).
+// words per tile (>= max(W_k, W_v); 0: no prefetch); EXACT: W_k = W_v = PW.
 // ---------------------------------------------------------------------------
-template <int NQ, int PW>
+template <int NQ, int PW, bool EXACT>
 __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   constexpr int NH = 4 * NQ;
   constexpr bool STACK = NQ <= 2;  // 2*NH <= 16: hi and lo weight rows share one MFMA
@@ -378,9 +398,9 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   // ---- per-wave streaming over this chunk's tiles ----
   const int wk_rows = PW > 0 ? PW : Wk, wv_rows = PW > 0 ? PW : Wv;  // staged words per token
   const int wpw = wk_rows + wv_rows;
-  uint32_t* kt = smem + wave * wpw * 64;
-  uint32_t* vt = kt + wk_rows * 64;
-  uint16_t* wt = reinterpret_cast<uint16_t*>(smem + WAVES * wpw * 64) + wave * (NG * 2 * NH * WROW);
+  uint32_t* kt = smem + wave * wpw * TROW;
+  uint32_t* vt = kt + wk_rows * TROW;
+  uint16_t* wt = reinterpret_cast<uint16_t*>(smem + WAVES * wpw * TROW) + wave * (NG * 2 * NH * WROW);
   const int64_t kbase = (int64_t)s * a.t_cap * Wk;
   const int64_t vbase = (int64_t)s * a.t_cap * Wv;
   const int64_t n_tiles = (a.n_tokens + 63) >> 6;
@@ -407,15 +427,28 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   // register prefetch of one tile's record words (K and V); PW = 0: none
   constexpr int PWR = PW > 0 ? PW : 1;
   uint32_t pk[PWR], pv[PWR];
+  // every lane loads in-bounds words: the word index is clamped to the record (a
+  // uniform offset folded into the per-word base pointer), the token to the tile;
+  // tokens past n_tokens are never weighted (their value metadata is zeroed)
+  const uint32_t* kps = a.packed_k + kbase;
+  const uint32_t* vps = a.packed_v + vbase;
   auto load_tile = [&](int64_t tt) {
-    // every lane loads in-bounds words (word index clamped to the record, token
-    // to the tile); values of tokens past n_tokens are zeroed afterwards
-    const uint32_t* kp = a.packed_k + kbase + tt * (64 * Wk) + lane;  // word w at kp[64 w]
-    const uint32_t* vp = a.packed_v + vbase + tt * (64 * Wv) + lane;
+    const uint32_t ko = (uint32_t)tt * (uint32_t)(64 * Wk) + (uint32_t)lane;
+    const uint32_t vo = (uint32_t)tt * (uint32_t)(64 * Wv) + (uint32_t)lane;
+    if constexpr (EXACT) {  // Wk == Wv == PW: no clamping, word offsets are immediates
+      const uint32_t* kp = kps + ko;
+      const uint32_t* vp = vps + vo;
 #pragma unroll
-    for (int w = 0; w < PW; ++w) {
-      pk[w] = kp[64 * (w < Wk ? w : Wk - 1)];
-      pv[w] = vp[64 * (w < Wv ? w : Wv - 1)];
+      for (int w = 0; w < PW; ++w) {
+        pk[w] = kp[64 * w];
+        pv[w] = vp[64 * w];
+      }
+    } else {
+#pragma unroll
+      for (int w = 0; w < PW; ++w) {
+        pk[w] = (kps + 64 * (w < Wk ? w : Wk - 1))[ko];
+        pv[w] = (vps + 64 * (w < Wv ? w : Wv - 1))[vo];
+      }
     }
   };
   int64_t tt = tile_begin + wave;
@@ -446,23 +479,17 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     const bool valid = t < a.n_tokens;
     // stage this tile's words in LDS (lane = token), then prefetch the next tile
     if constexpr (PW > 0) {
-      if (tt * 64 + 64 <= a.n_tokens) {
 #pragma unroll
-        for (int w = 0; w < PW; ++w) {
-          kt[w * 64 + lane] = pk[w];
-          vt[w * 64 + lane] = pv[w];
-        }
-      } else {
-#pragma unroll
-        for (int w = 0; w < PW; ++w) {
-          kt[w * 64 + lane] = valid ? pk[w] : 0u;
-          vt[w * 64 + lane] = valid ? pv[w] : 0u;
-        }
+      for (int w = 0; w < PW; ++w) {
+        kt[w * TROW + lane] = pk[w];
+        vt[w * TROW + lane] = pv[w];
       }
       if (tt + WAVES < tile_end) load_tile(tt + WAVES);
     } else {
-      for (int w = 0; w < kk.used; ++w) kt[w * 64 + lane] = valid ? a.packed_k[rec_word(kbase, t, Wk, w)] : 0u;
-      for (int w = 0; w < kvv.used; ++w) vt[w * 64 + lane] = valid ? a.packed_v[rec_word(vbase, t, Wv, w)] : 0u;
+      const uint32_t ko = (uint32_t)tt * (uint32_t)(64 * Wk) + (uint32_t)lane;
+      const uint32_t vo = (uint32_t)tt * (uint32_t)(64 * Wv) + (uint32_t)lane;
+      for (int w = 0; w < kk.used; ++w) kt[w * TROW + lane] = (kps + 64 * w)[ko];
+      for (int w = 0; w < kvv.used; ++w) vt[w * TROW + lane] = (vps + 64 * w)[vo];
     }
     __builtin_amdgcn_wave_barrier();
 
@@ -474,7 +501,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     for (int sl = 0; sl < NG; ++sl) {
       if (sl >= kk.n) continue;
       const int g = kk.grp[sl];
-      const uint32_t meta = kt[sl * 64 + lane];
+      const uint32_t meta = kt[sl * TROW + lane];
       f32x4 dh[NQ], dl[NQ];
 #pragma unroll
       for (int q = 0; q < NQ; ++q) dh[q] = dl[q] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -529,23 +556,30 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int sl = 0; sl < NG; ++sl) {
       if (sl >= kvv.n) continue;
-      const uint32_t meta = vt[sl * 64 + lane];
+      // tokens past n_tokens hold whatever the cache holds there: zero their metadata
+      const uint32_t meta = valid ? vt[sl * TROW + lane] : 0u;
       const float sv = h2f(meta), zv = h2f(meta >> 16);
       uint16_t* ws = wt + sl * 2 * NH * WROW;  // rows: hi of heads 0..NH-1, then lo
 #pragma unroll
-      for (int h = 0; h < NH; ++h) {
+      for (int h = 0; h < NH; h += 2) {  // two heads per packed conversion
         zacc[h][sl] = __builtin_fmaf(p[h], zv, zacc[h][sl]);
-        const float w = p[h] * sv;
-        const __bf16 whi = (__bf16)w;
-        const __bf16 wlo = (__bf16)(w - (float)whi);
-        ws[h * WROW + lane] = __builtin_bit_cast(uint16_t, whi);
-        ws[(NH + h) * WROW + lane] = __builtin_bit_cast(uint16_t, wlo);
+        zacc[h + 1][sl] = __builtin_fmaf(p[h + 1], zv, zacc[h + 1][sl]);
+        const float w0 = p[h] * sv, w1 = p[h + 1] * sv;
+        const uint32_t hb = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0, w1}, bf16x2));
+        const float h0 = __builtin_bit_cast(float, hb << 16), h1 = __builtin_bit_cast(float, hb & 0xFFFF0000u);
+        const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0 - h0, w1 - h1}, bf16x2));
+        ws[h * WROW + lane] = (uint16_t)hb;
+        ws[(h + 1) * WROW + lane] = (uint16_t)(hb >> 16);
+        ws[(NH + h) * WROW + lane] = (uint16_t)lb;
+        ws[(NH + h + 1) * WROW + lane] = (uint16_t)(lb >> 16);
       }
     }
     __builtin_amdgcn_wave_barrier();
 
     // ---- value accumulation over the kept value coefficients ----
     const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
+    uint32_t vmagic = 0x43004300u;  // exponent of 128 in both halves, in a VGPR (see value_codes2)
+    asm volatile("" : "+v"(vmagic));
 #pragma unroll
     for (int sl = 0; sl < NG; ++sl) {
       if (sl >= kvv.n) continue;
@@ -561,9 +595,12 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
           if (col < (STACK ? 2 * NH : NH)) aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + col * WROW + tok0));
           bf16x8 awl = bf16x8{};
           if (!STACK && col < NH) awl = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + (NH + col) * WROW + tok0));
+          // MFMA column col of block c2 is in-group coefficient 2 col + c2
+          u32x4 vc[2];
+          value_codes2<CLS>(vt, pay, kvv.used, B, 2 * col * B, tok0, vmagic, vc[0], vc[1]);
 #pragma unroll
           for (int c2 = 0; c2 < 2; ++c2) {
-            const bf16x8 bop = as_bf16x8(value_codes<CLS>(vt, pay, kvv.used, B, (16 * c2 + col) * B, tok0));
+            const bf16x8 bop = as_bf16x8(vc[c2]);
             f32x4 acc = vacc[sl][c2];
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, bop, acc, 0, 0, 0);
             if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
@@ -620,7 +657,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
           const int row = 4 * kq + j;
           const int h = pass == 0 ? row : row - NH;
           if ((pass == 0 && row < NH) || (pass == 1 && row >= NH && row < 2 * NH)) {
-            float* dst = accw + h * D + G * Kv.grp[sl] + 16 * c2 + col;
+            float* dst = accw + h * D + G * Kv.grp[sl] + 2 * col + c2;
             *dst += vacc[sl][c2][j];
           }
         }
@@ -766,25 +803,30 @@ int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, in
   return (int32_t)nch;
 }
 
-template <int NQ, int PW>
+template <int NQ, int PW, bool EXACT>
 static void launch_nq_pw(const AttnArgs& a, hipStream_t st) {
   const int wpw = PW > 0 ? 2 * PW : a.Wk + a.Wv;
-  size_t tiles = (size_t)WAVES * wpw * 64 * 4 + (size_t)attn_wt_bytes(NQ);
+  size_t tiles = (size_t)WAVES * wpw * TROW * 4 + (size_t)attn_wt_bytes(NQ);
   size_t merge = (size_t)WAVES * 4 * NQ * D * 4;       // per-wave value sums
   size_t lds = tiles > merge ? tiles : merge;
   const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
-  hipLaunchKernelGGL((attn_kernel<NQ, PW>), grid, dim3(256), lds, st, a);
+  hipLaunchKernelGGL((attn_kernel<NQ, PW, EXACT>), grid, dim3(256), lds, st, a);
 }
 
 template <int NQ>
 static void launch_nq(const AttnArgs& a, hipStream_t st) {
   const int w = a.Wk > a.Wv ? a.Wk : a.Wv;
-  if (w <= 8)
-    launch_nq_pw<NQ, 8>(a, st);
+  const bool same = a.Wk == a.Wv;
+  if (w == 8 && same)
+    launch_nq_pw<NQ, 8, true>(a, st);
+  else if (w <= 8)
+    launch_nq_pw<NQ, 8, false>(a, st);
+  else if (w == 16 && same)
+    launch_nq_pw<NQ, 16, true>(a, st);
   else if (w <= 16)
-    launch_nq_pw<NQ, 16>(a, st);
+    launch_nq_pw<NQ, 16, false>(a, st);
   else
-    launch_nq_pw<NQ, 0>(a, st);
+    launch_nq_pw<NQ, 0, false>(a, st);
 }
 
 static hipError_t launch_scan_combine(const AttnArgs& a, hipStream_t st) {
