@@ -146,6 +146,7 @@ __global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
   __shared__ float qs[16][D];
   __shared__ float part_s[4][16][D];
   __shared__ float red_s[8];
+  __shared__ __attribute__((aligned(16))) KPlan plans_s[8];  // field plans of widths 1..8
   const int kv = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int s = b * a.n_kv_heads + kv;
   if constexpr (APP != 0) {
@@ -157,6 +158,9 @@ __global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
   }
   const int nqh = a.n_qh;
   const uint32_t bwk = *reinterpret_cast<const uint32_t*>(a.bits_k + (int64_t)s * NG);
+  static_assert(sizeof(KPlan) % 4 == 0, "plan copy");
+  for (int i = tid; i < (int)(sizeof(KPLANS) / 4); i += 512)
+    reinterpret_cast<uint32_t*>(plans_s)[i] = reinterpret_cast<const uint32_t*>(KPLANS)[i];
   for (int e = tid; e < 16 * D; e += 512) {
     const int h = e >> 7, c = e & 127;
     float v = 0.0f;
@@ -236,7 +240,7 @@ __global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
       }
     }
     if (g < 0 || B > 8) continue;
-    const KPlan& P = KPLANS[B - 1];
+    const KPlan& P = plans_s[B - 1];
     if (2 * m >= P.n_ops) continue;
     const int h = 4 * quad + r;
     uint32_t hi[4], lo[4];
@@ -384,17 +388,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int s = b * a.n_kv_heads + kv;
   const int nqh = a.n_qh;
-  const Kept Kk = read_kept(a.bits_k + (int64_t)s * NG);
-  const Kept Kv = read_kept(a.bits_v + (int64_t)s * NG);
   const int Wk = a.Wk, Wv = a.Wv;
-  const bool ok = Kk.ok && Kv.ok && Kk.used <= Wk && Kv.used <= Wv;
-
-  // ---- prologue: prepared query data of this (sequence, kv head) ----
-  const float* qp = a.qprep + (int64_t)s * QP;
-  for (int i = tid; i < NQ * QA_QUAD; i += 256) qa_s[i] = reinterpret_cast<const uint32_t*>(qp + 4 + 64)[i];
-  if (tid < 64) qbar_s[tid] = qp[4 + tid];
-  const float E2 = qp[0];
-
   // ---- per-wave streaming over this chunk's tiles ----
   const int wk_rows = PW > 0 ? PW : Wk, wv_rows = PW > 0 ? PW : Wv;  // staged words per token
   const int wpw = wk_rows + wv_rows;
@@ -451,8 +445,20 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       }
     }
   };
+  // the first tile's loads go out before anything that waits on the width tables
+  // (they stay in bounds whatever the tables hold)
   int64_t tt = tile_begin + wave;
-  if (ok && tt < tile_end) load_tile(tt);
+  if (tt < tile_end) load_tile(tt);
+  const Kept Kk = read_kept(a.bits_k + (int64_t)s * NG);
+  const Kept Kv = read_kept(a.bits_v + (int64_t)s * NG);
+  const bool ok = Kk.ok && Kv.ok && Kk.used <= Wk && Kv.used <= Wv;
+
+  // ---- prologue: prepared query data of this (sequence, kv head) ----
+  const float* qp = a.qprep + (int64_t)s * QP;
+  for (int i = tid; i < NQ * QA_QUAD; i += 256) qa_s[i] = reinterpret_cast<const uint32_t*>(qp + 4 + 64)[i];
+  if (tid < 64) qbar_s[tid] = qp[4 + tid];
+  const float E2 = qp[0];
+
   __syncthreads();  // prepared query data in LDS
 
   Kept kk = Kk, kvv = Kv;
