@@ -34,6 +34,30 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 CALIB_BYTES = 256 << 20
+
+# HBM bytes per decode-step call from rocprofv3 counters (FETCH_SIZE and WRITE_SIZE
+# passes over `bench.py --steps 1 --warmup 0 --decode-steps 2 --no-cpu-baseline
+# --eager --copy-calibration`), scaled by the counters' reading of the 256 MiB
+# copy (FETCH_SIZE reads 131089 KiB for 256 MiB read: x2.0; WRITE_SIZE reads
+# 262148 KiB for 256 MiB written: x1.0). Valid only for the kernel sources they
+# were taken on (sha256 over DECODE_STEP_SOURCES); otherwise `traffic` is null.
+DECODE_STEP_SOURCES = ("kernels_attn.hip", "kplan.hpp", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
+# sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
+MEASURED_TRAFFIC = {
+    "0ee7091a1ca6b11d9d5b1f6e87f628ba9568deed8d9bfed1fe0a062f5d86c9e6": {
+        "fetch_bytes": 72906752, "write_bytes": 1668403,
+        "per_kernel": {"qprep_kernel<1>": [1195213, 15667], "attn_kernel<1,8,true>": [67897139, 1636352],
+                       "combine_kernel": [3814400, 16384]}},
+}
+
+
+def decode_step_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in DECODE_STEP_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_07915_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 METRIC = "KV encode GB/s + compressed decode-attn tokens/s, % of HBM peak, at 8x"
 
 
@@ -259,6 +283,8 @@ def main():
     att_gbps = att_call_bytes / (att_call_ms * 1e-3) / 1e9 if att_call_ms > 0 else 0.0
     tokens_per_call = n_seq * float(np.mean([T + s + 1 for s in range(n_dec)])) if n_dec else 0.0
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    measured = MEASURED_TRAFFIC.get(decode_step_sources_sha256())
+    traffic = (measured["fetch_bytes"] + measured["write_bytes"]) if measured else None
 
     result = {
         "metric": METRIC,
@@ -287,9 +313,10 @@ def main():
                              "cache_tokens_per_s": round(tokens_per_call / (att_call_ms * 1e-3), 1),
                              "generated_tokens_per_s": round(1.0 / (att_call_ms * 1e-3 * L), 2)},
         "roofline": {"bound": "hbm", "achieved": round(att_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "kernel": "decode_step (append + query prep, split-K scan, combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
+        "traffic_detail": measured,
         "decode_launch": "eager" if args.eager else "hip_graph",
         "fit_ms": round(fit_s * 1e3, 1),
         "input_generation_s": round(gen_s, 1),
