@@ -39,25 +39,41 @@ __device__ __forceinline__ uint32_t quantize16(const float (&c)[16], uint32_t (&
 // Basis columns of kept group grp as MFMA A operands: row r of the 32x32 tile is
 // in-group coefficient jj(r), so that after the product lane half h holds
 // coefficients 16h..16h+15. The fp32 basis is split into three bf16 parts.
-// Also loads the 16 coefficient means of the lane half.
+// Also loads the 16 coefficient means of the lane half. Split in two steps
+// (raw loads, then the split) so that a caller can put other loads in flight
+// between them.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void load_group_operands(const float* __restrict__ Vs, const float* __restrict__ ms, int grp,
-                                                    int col, int h, bf16x8 (&Va)[3][8], float (&mv)[16]) {
+__device__ __forceinline__ void load_group_raw(const float* __restrict__ Vs, const float* __restrict__ ms, int grp,
+                                               int col, int h, float (&raw)[64], float (&mv)[16]) {
   const int r = col;
   const int jj = 16 * ((r & 7) >> 2) + 4 * (r >> 3) + (r & 3);
   const int cidx = G * grp + jj;
 #pragma unroll
+  for (int k = 0; k < 8; ++k)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) raw[8 * k + i] = Vs[(16 * k + 8 * h + i) * D + cidx];
+  const float* m = ms + G * grp + 16 * h;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) mv[j] = m[j];
+}
+
+__device__ __forceinline__ void split_group_operands(const float (&raw)[64], bf16x8 (&Va)[3][8]) {
+#pragma unroll
   for (int k = 0; k < 8; ++k) {
     uint32_t p0[8], p1[8], p2[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) split3(Vs[(16 * k + 8 * h + i) * D + cidx], p0[i], p1[i], p2[i]);
+    for (int i = 0; i < 8; ++i) split3(raw[8 * k + i], p0[i], p1[i], p2[i]);
     Va[0][k] = as_bf16x8(u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])});
     Va[1][k] = as_bf16x8(u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])});
     Va[2][k] = as_bf16x8(u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])});
   }
-  const float* m = ms + G * grp + 16 * h;
-#pragma unroll
-  for (int j = 0; j < 16; ++j) mv[j] = m[j];
+}
+
+__device__ __forceinline__ void load_group_operands(const float* __restrict__ Vs, const float* __restrict__ ms, int grp,
+                                                    int col, int h, bf16x8 (&Va)[3][8], float (&mv)[16]) {
+  float raw[64];
+  load_group_raw(Vs, ms, grp, col, h, raw, mv);
+  split_group_operands(raw, Va);
 }
 
 // ---------------------------------------------------------------------------

@@ -49,6 +49,7 @@ constexpr int QA_QUAD = NG * QA_SLOT;
 constexpr int QP = 4 + 16 * 4 + 4 * QA_QUAD;  // floats per (sequence, kv head) of prepared query data
 constexpr int WAVES = 4;
 constexpr int WROW = 72;  // bf16 per weight row (64 tokens + pad: spreads rows over LDS banks)
+constexpr int AROW = D + 4;  // floats per row of merged value sums (rows of one wave spread over banks)
 constexpr int TROW = 68;  // uint32 per staged record-word row (64 tokens + pad: distinct words of one
                           // token group fall on distinct LDS banks)
 
@@ -104,29 +105,46 @@ __device__ __forceinline__ void append_token(const AttnArgs& a, int s, int tid) 
   constexpr int ESZ = F32 ? 4 : 2;
   constexpr int ROWB = F32 ? (512 + 16) : (256 + 16);
   constexpr int CPR = (D * ESZ) / 16;
+  constexpr int PER = (2 * 32 * CPR) / 512;  // staged 16-byte pieces per thread
+  static_assert(PER * 512 == 2 * 32 * CPR, "staging split");
   __shared__ __attribute__((aligned(16))) uint8_t xs[2][32 * ROWB];
-  for (int e = tid; e < 2 * 32 * CPR; e += 512) {
-    const int which = e / (32 * CPR), row = (e / CPR) % 32, part = e % CPR;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (row == 0) {
-      const char* src = reinterpret_cast<const char*>(which ? a.v_new : a.k_new);
-      v = *reinterpret_cast<const u32x4*>(src + (int64_t)s * D * ESZ + part * 16);
-    }
-    *reinterpret_cast<u32x4*>(&xs[which][row * ROWB + part * 16]) = v;
-  }
-  __syncthreads();
   const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
   const int which = wave >> 2, slot = wave & 3;
+  // every global read of this wave is issued before the first use: the new rows,
+  // the width table, and the basis columns and means of group `slot` (kept groups
+  // are a prefix in the common case; another group is loaded once the table is known)
+  u32x4 stg[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = tid + 512 * i;
+    const int wh = e / (32 * CPR), row = (e / CPR) % 32, part = e % CPR;
+    stg[i] = u32x4{0u, 0u, 0u, 0u};
+    if (row == 0) {
+      const char* src = reinterpret_cast<const char*>(wh ? a.v_new : a.k_new);
+      stg[i] = *reinterpret_cast<const u32x4*>(src + (int64_t)s * D * ESZ + part * 16);
+    }
+  }
   const Kept K = read_kept((which ? a.bits_v : a.bits_k) + (int64_t)s * NG);
+  const float* Vs = (which ? a.basis_v : a.basis_k) + (int64_t)s * D * D;
+  const float* ms = (which ? a.mean_v : a.mean_k) + (int64_t)s * D;
+  float raw[64], mv[16];
+  load_group_raw(Vs, ms, slot, col, h, raw, mv);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = tid + 512 * i;
+    const int wh = e / (32 * CPR), row = (e / CPR) % 32, part = e % CPR;
+    *reinterpret_cast<u32x4*>(&xs[wh][row * ROWB + part * 16]) = stg[i];
+  }
+  __syncthreads();
   const int W = which ? a.Wv : a.Wk;
   if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
   uint32_t* packed = which ? a.app_v : a.app_k;
   const int64_t sbase = (int64_t)s * a.t_cap * W;
   if (slot < K.n) {
+    const int grp = pick4(K.grp, slot);
+    if (grp != slot) load_group_raw(Vs, ms, grp, col, h, raw, mv);
     bf16x8 Va[3][8];
-    float mv[16];
-    load_group_operands((which ? a.basis_v : a.basis_k) + (int64_t)s * D * D, (which ? a.mean_v : a.mean_k) + (int64_t)s * D,
-                        pick4(K.grp, slot), col, h, Va, mv);
+    split_group_operands(raw, Va);
     encode_block<F32, ROWB>(xs[which], 0, col, h, Va, mv, a.t_new, a.t_new, a.t_new + 1, sbase, W, slot,
                             pick4(K.bits, slot), pick4(K.pay, slot), packed);
   }
@@ -647,33 +665,31 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     }
   }
   __syncthreads();  // all waves done with their tile buffers: reuse smem for the value sums
-  float* accw = reinterpret_cast<float*>(smem) + wave * NH * D;  // [NH][128] per wave
-  for (int i = lane; i < NH * D; i += 64) accw[i] = 0.0f;
-  __builtin_amdgcn_wave_barrier();
-  // rows 4*kq + j: heads (hi rows) then, when stacked, the lo rows of the same heads
+  // per wave, MFMA row r of the value accumulators lands in row r of [ACC_ROWS][AROW]
+  // (stacked: rows NH.. hold the lo-weight sums of the same heads); every kept
+  // column of a row is written exactly once, so no read-modify-write is needed
+  constexpr int ACC_ROWS = STACK ? 2 * NH : NH;
+  float* accw = reinterpret_cast<float*>(smem) + wave * ACC_ROWS * AROW;
 #pragma unroll
-  for (int pass = 0; pass < (STACK ? 2 : 1); ++pass) {
+  for (int sl = 0; sl < NG; ++sl) {
+    if (sl >= Kv.n) continue;
 #pragma unroll
-    for (int sl = 0; sl < NG; ++sl) {
-      if (sl >= Kv.n) continue;
+    for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int row = 4 * kq + j;
-          const int h = pass == 0 ? row : row - NH;
-          if ((pass == 0 && row < NH) || (pass == 1 && row >= NH && row < 2 * NH)) {
-            float* dst = accw + h * D + G * Kv.grp[sl] + 2 * col + c2;
-            *dst += vacc[sl][c2][j];
-          }
-        }
-    }
-    __builtin_amdgcn_wave_barrier();
+      for (int j = 0; j < 4; ++j) {
+        const int row = 4 * kq + j;
+        if (row < ACC_ROWS) accw[row * AROW + G * Kv.grp[sl] + 2 * col + c2] = vacc[sl][c2][j];
+      }
   }
+  uint32_t kept_groups = 0u;  // groups with no kept value coefficients have no sums
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl)
+    if (sl < Kv.n) kept_groups |= 1u << Kv.grp[sl];
   __syncthreads();
   float* part = a.partial + ((int64_t)b * a.n_q_heads + kv * nqh) * a.n_chunks * PART + (int64_t)chunk * PART;
   for (int e = tid; e < nqh * D; e += 256) {
     const int h = e >> 7, j = e & 127;
+    const bool kept = (kept_groups >> (j >> 5)) & 1u;
     float M = -__builtin_inff();
 #pragma unroll
     for (int w = 0; w < WAVES; ++w) M = __builtin_fmaxf(M, mst[w][h]);
@@ -681,7 +697,10 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int w = 0; w < WAVES; ++w) {
       const float f = (mst[w][h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(mst[w][h] - M);
-      acc += f * (reinterpret_cast<float*>(smem) + w * NH * D)[h * D + j];
+      const float* aw = reinterpret_cast<const float*>(smem) + w * ACC_ROWS * AROW;
+      float v = kept ? aw[h * AROW + j] : 0.0f;
+      if constexpr (STACK) v += kept ? aw[(NH + h) * AROW + j] : 0.0f;
+      acc += f * v;
       l += f * lst[w][h];
       if (j < NG) z += f * zst[w][h][j];
     }
@@ -703,7 +722,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 // states are then merged in LDS.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void combine_kernel(AttnArgs a) {
-  constexpr int CB = 8;
+  constexpr int CB = 12;  // 8 x 12 = 96 chunks per round: one round of loads for ~768 scan workgroups over 8 heads
   __shared__ float accs[8][D];
   __shared__ float chat[D];
   __shared__ float gm[8], gl[8];
@@ -813,7 +832,7 @@ template <int NQ, int PW, bool EXACT>
 static void launch_nq_pw(const AttnArgs& a, hipStream_t st) {
   const int wpw = PW > 0 ? 2 * PW : a.Wk + a.Wv;
   size_t tiles = (size_t)WAVES * wpw * TROW * 4 + (size_t)attn_wt_bytes(NQ);
-  size_t merge = (size_t)WAVES * 4 * NQ * D * 4;       // per-wave value sums
+  size_t merge = (size_t)WAVES * (NQ <= 2 ? 8 * NQ : 4 * NQ) * AROW * 4;  // per-wave value sums
   size_t lds = tiles > merge ? tiles : merge;
   const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
   hipLaunchKernelGGL((attn_kernel<NQ, PW, EXACT>), grid, dim3(256), lds, st, a);

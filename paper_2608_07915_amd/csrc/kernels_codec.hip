@@ -20,7 +20,7 @@ namespace spectra_dev {
 // Encode
 // ---------------------------------------------------------------------------
 template <bool F32IN>
-__global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
+__global__ __launch_bounds__(256, 2) void encode_kernel(EncodeArgs a) {
   constexpr int ST = F32IN ? 64 : 128;             // tokens per super-tile
   constexpr int ROWB = F32IN ? (512 + 16) : (256 + 16);  // padded LDS row (bank spread)
   __shared__ __attribute__((aligned(16))) uint8_t xs[ST * ROWB];
@@ -52,23 +52,37 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
     sp.b_hi = (sp.hi + 31) >> 5;
     return sp;
   };
-  // Stage the rows of those blocks (16-byte chunks, coalesced) into LDS; rows
-  // outside the call's token range are zero.
-  auto stage = [&](const Span& sp) {
-    for (int c = 32 * sp.b_lo * CPR + tid; c < 32 * sp.b_hi * CPR; c += 256) {
+  // The rows of those blocks are staged in LDS in 16-byte chunks (coalesced); rows
+  // outside the call's token range are zero. A super-tile is PRE chunks per thread;
+  // the next super-tile's chunks are loaded into registers while this one is
+  // projected and quantized, then written to LDS.
+  constexpr int PRE = (ST * CPR) / 256;
+  static_assert(PRE * 256 == ST * CPR, "staging split");
+  auto load_stage = [&](const Span& sp, u32x4 (&r)[PRE]) {
+#pragma unroll
+    for (int i = 0; i < PRE; ++i) {
+      const int c = tid + 256 * i;
       const int row = c / CPR, part = c % CPR;
-      const int64_t i = sp.slot0 + row - a.t0;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (i >= 0 && i < a.n)
-        v = *reinterpret_cast<const u32x4*>(xb + ((int64_t)s * a.stream_stride + i * a.token_stride) * ESZ + part * 16);
-      *reinterpret_cast<u32x4*>(xs + row * ROWB + part * 16) = v;
+      const int64_t t = sp.slot0 + row - a.t0;
+      r[i] = u32x4{0u, 0u, 0u, 0u};
+      if (row >= 32 * sp.b_lo && row < 32 * sp.b_hi && t >= 0 && t < a.n)
+        r[i] = *reinterpret_cast<const u32x4*>(xb + ((int64_t)s * a.stream_stride + t * a.token_stride) * ESZ + part * 16);
+    }
+  };
+  auto store_stage = [&](const Span& sp, const u32x4 (&r)[PRE]) {
+#pragma unroll
+    for (int i = 0; i < PRE; ++i) {
+      const int c = tid + 256 * i;
+      const int row = c / CPR, part = c % CPR;
+      if (row >= 32 * sp.b_lo && row < 32 * sp.b_hi) *reinterpret_cast<u32x4*>(xs + row * ROWB + part * 16) = r[i];
     }
   };
   int64_t st = blockIdx.x;
   if (st >= n_st) return;
-  // The first rows are loaded before the width table is needed, so their latency
+  // The first rows are requested before the width table is needed, so their latency
   // overlaps the basis loads (which depend on it).
-  stage(span(st));
+  u32x4 pre[PRE];
+  load_stage(span(st), pre);
 
   const Kept K = read_kept(a.bits + (int64_t)s * NG);
   const int W = a.W;
@@ -92,7 +106,10 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
     const Span sp = span(st);
     const int64_t slot0 = sp.slot0;
     const int b_lo = sp.b_lo, b_hi = sp.b_hi, lo = sp.lo, hi = sp.hi;
+    store_stage(sp, pre);
     __syncthreads();  // staged rows visible
+    const int64_t st_next = st + gridDim.x;
+    if (st_next < n_st) load_stage(span(st_next), pre);
 
     if (active) {
       for (int beta = b_lo + phase; beta < b_hi; beta += wpg)
@@ -104,10 +121,9 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
       const int row = lo + c % nrow, w = K.used + c / nrow;
       a.packed[rec_word(sbase, slot0 + row, W, w)] = 0u;
     }
-    st += gridDim.x;
+    st = st_next;
     if (st >= n_st) break;
     __syncthreads();  // every wave is done with the staged rows
-    stage(span(st));
   }
 }
 
