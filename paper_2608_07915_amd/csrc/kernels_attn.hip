@@ -49,6 +49,7 @@ constexpr int QA_QUAD = NG * QA_SLOT;
 constexpr int QP = 4 + 16 * 4 + 4 * QA_QUAD;  // floats per (sequence, kv head) of prepared query data
 constexpr int WAVES = 4;
 constexpr int WROW = 72;  // bf16 per weight row (64 tokens + pad: spreads rows over LDS banks)
+constexpr float RESCALE_SLACK = 4.0f;  // log2 units: weights exp2(score - m) stay <= 16
 constexpr int AROW = D + 4;  // floats per row of merged value sums (rows of one wave spread over banks)
 constexpr int TROW = 68;  // uint32 per staged record-word row (64 tokens + pad: distinct words of one
                           // token group fall on distinct LDS banks)
@@ -549,13 +550,15 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
           sc[4 * q + j] += sk * __builtin_fmaf(dl[q][j], 1.0f / 2048.0f, dh[q][j]) + zk * qbar_s[(4 * q + j) * 4 + g];
     }
 
-    // ---- online softmax (log2 domain); the running max moves only when exceeded ----
+    // ---- online softmax (log2 domain) against a reference m that moves only when
+    // a score exceeds it by more than RESCALE_SLACK: weights stay <= 2^RESCALE_SLACK,
+    // and the rescale of the running sums is rare after the first tile ----
     float p[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
       const bool live = valid && h < nqh;
       const float x = live ? sc[h] : -__builtin_inff();
-      if (__any(x > m_run[h])) {
+      if (__any(x > m_run[h] + RESCALE_SLACK)) {
         const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x));
         const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
         l_run[h] *= alpha;
