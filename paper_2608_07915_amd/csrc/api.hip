@@ -211,8 +211,7 @@ size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32
   if (batch <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_tokens <= 0) return 0;
   int32_t tpc;
   const int32_t nch = attention_chunks(batch, n_kv_heads, n_tokens, &tpc);
-  return round256(attention_qprep_floats(batch, n_q_heads, n_kv_heads) * sizeof(float)) +
-         attention_partial_floats(batch, n_q_heads, nch) * sizeof(float);
+  return attention_partial_floats(batch, n_q_heads, nch) * sizeof(float);
 }
 
 // Checks shared by decode_attention and decode_step; fills everything of AttnArgs
@@ -269,9 +268,7 @@ static spectra_status prepare_attention(const char* name, const spectra_codec* c
   const float sc = softmax_scale > 0.0f ? softmax_scale : 1.0f / std::sqrt((float)kD);
   a.scale_log2 = sc * 1.4426950408889634f;
   a.n_chunks = attention_chunks(batch, n_kv_heads, n_tokens, &a.tiles_per_chunk);
-  a.qprep = reinterpret_cast<float*>(workspace);
-  a.partial = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
-                                       round256(attention_qprep_floats(batch, n_q_heads, n_kv_heads) * sizeof(float)));
+  a.partial = reinterpret_cast<float*>(workspace);
   a.out = out;
   *args = a;
   return SPECTRA_OK;
@@ -309,7 +306,7 @@ spectra_status spectra_decode_step(const spectra_codec* ck, const spectra_codec*
   a.app_v = packed_v;
   a.t_new = t;
   a.app_f32 = kv_dt == SPECTRA_F32;
-  hipError_t e = launch_decode_step(a, (hipStream_t)stream);
+  hipError_t e = launch_attention(a, (hipStream_t)stream);
   return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "decode_step launch");
 }
 

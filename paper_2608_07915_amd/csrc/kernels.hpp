@@ -77,7 +77,6 @@ struct AttnArgs {
   uint32_t* app_v;
   int64_t t_new;
   int32_t app_f32;
-  float* qprep;          // workspace: rotated queries and MFMA operands
   float* partial;        // workspace: per-chunk softmax partials
   float* out;            // [batch][n_q_heads][128]
 };
@@ -89,11 +88,10 @@ hipError_t launch_encode(const spectra_dev::EncodeArgs& a, bool f32_input, hipSt
 hipError_t launch_decode(const spectra_dev::DecodeArgs& a, hipStream_t st);
 hipError_t launch_pack_codes(const spectra_dev::PackArgs& a, bool unpack, hipStream_t st);
 hipError_t launch_gram(const spectra_dev::GramArgs& a, bool f32_input, hipStream_t st);
+// Decode-step attention; with a.app_k != nullptr the new token of every stream is
+// appended first (the decode step).
 hipError_t launch_attention(const spectra_dev::AttnArgs& a, hipStream_t st);
-// Same, with the new token of every stream appended first (a.k_new != nullptr).
-hipError_t launch_decode_step(const spectra_dev::AttnArgs& a, hipStream_t st);
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
-size_t attention_qprep_floats(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads);
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
 }  // namespace spectra

@@ -40,13 +40,12 @@ constexpr int kplan_mfmas(int B) { return (make_kplan(B).n_ops + 1) / 2; }
 constexpr int KM_MAX = 14;  // score MFMAs per slot, widest plan (B = 7)
 static_assert(make_kplan(7).n_ops == KOPS_MAX && kplan_mfmas(7) == KM_MAX, "plan sizes");
 static_assert(make_kplan(1).n_ops == 16 && make_kplan(5).n_ops == 20 && make_kplan(8).n_ops == 16, "plan sizes");
-__device__ constexpr KPlan KPLANS[8] = {make_kplan(1), make_kplan(2), make_kplan(3), make_kplan(4),
-                                        make_kplan(5), make_kplan(6), make_kplan(7), make_kplan(8)};
+__device__ constexpr KGather KGATHER = make_kgather();
+static_assert(KMFMA_MAX == KM_MAX, "plan sizes");
 
 // score-MFMA A operands per (head quad, slot): [m][row r][hi k0..k3, lo k0..k3] as fp16
 constexpr int QA_SLOT = KM_MAX * 4 * 4;  // uint32
 constexpr int QA_QUAD = NG * QA_SLOT;
-constexpr int QP = 4 + 16 * 4 + 4 * QA_QUAD;  // floats per (sequence, kv head) of prepared query data
 constexpr int WAVES = 4;
 constexpr int WROW = 72;  // bf16 per weight row (64 tokens + pad: spreads rows over LDS banks)
 constexpr float RESCALE_SLACK = 4.0f;  // log2 units: weights exp2(score - m) stay <= 16
@@ -94,129 +93,131 @@ __device__ __forceinline__ float wave_max_all(float v) {
 
 
 // ---------------------------------------------------------------------------
-// Decode-step append (APP = 1: bf16 rows, 2: fp32 rows): the new key and value
-// of stream s go into slot t_new exactly as the encode kernel would write them
-// (same staging, same MFMA sequence per token). Waves 0..3 take the kept key
-// groups, waves 4..7 the kept value groups; the token sits in LDS row 0 of a
-// 32-row block whose other rows are zero (their columns are discarded).
+// Decode-step append, done by the workgroup whose chunk holds the last tile:
+// the new key and value of stream s go into slot t_new exactly as the encode
+// kernel would write them (same staging, same MFMA sequence per token). Wave w
+// takes kept key slot w, then kept value slot w; the token sits in LDS row 0 of
+// a 32-row block whose other rows are zero (their columns are discarded).
+// `xs` is scratch LDS of at least append_stage_bytes(F32) bytes.
 // ---------------------------------------------------------------------------
-template <int APP>
-__device__ __forceinline__ void append_token(const AttnArgs& a, int s, int tid) {
-  constexpr bool F32 = APP == 2;
+__host__ __device__ constexpr int append_rowb(bool f32) { return f32 ? (512 + 16) : (256 + 16); }
+__host__ __device__ constexpr int append_stage_bytes(bool f32) { return 2 * 32 * append_rowb(f32); }
+
+template <bool F32>
+__device__ __forceinline__ void append_token(const AttnArgs& a, int s, int tid, uint8_t* xs) {
   constexpr int ESZ = F32 ? 4 : 2;
-  constexpr int ROWB = F32 ? (512 + 16) : (256 + 16);
+  constexpr int ROWB = append_rowb(F32);
   constexpr int CPR = (D * ESZ) / 16;
-  constexpr int PER = (2 * 32 * CPR) / 512;  // staged 16-byte pieces per thread
-  static_assert(PER * 512 == 2 * 32 * CPR, "staging split");
-  __shared__ __attribute__((aligned(16))) uint8_t xs[2][32 * ROWB];
+  constexpr int PER = (2 * 32 * CPR) / 256;  // staged 16-byte pieces per thread
+  static_assert(PER * 256 == 2 * 32 * CPR, "staging split");
   const int wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
-  const int which = wave >> 2, slot = wave & 3;
-  // every global read of this wave is issued before the first use: the new rows,
-  // the width table, and the basis columns and means of group `slot` (kept groups
-  // are a prefix in the common case; another group is loaded once the table is known)
-  u32x4 stg[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    const int e = tid + 512 * i;
+    const int e = tid + 256 * i;
     const int wh = e / (32 * CPR), row = (e / CPR) % 32, part = e % CPR;
-    stg[i] = u32x4{0u, 0u, 0u, 0u};
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (row == 0) {
       const char* src = reinterpret_cast<const char*>(wh ? a.v_new : a.k_new);
-      stg[i] = *reinterpret_cast<const u32x4*>(src + (int64_t)s * D * ESZ + part * 16);
+      v = *reinterpret_cast<const u32x4*>(src + (int64_t)s * D * ESZ + part * 16);
     }
-  }
-  const Kept K = read_kept((which ? a.bits_v : a.bits_k) + (int64_t)s * NG);
-  const float* Vs = (which ? a.basis_v : a.basis_k) + (int64_t)s * D * D;
-  const float* ms = (which ? a.mean_v : a.mean_k) + (int64_t)s * D;
-  float raw[64], mv[16];
-  load_group_raw(Vs, ms, slot, col, h, raw, mv);
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int e = tid + 512 * i;
-    const int wh = e / (32 * CPR), row = (e / CPR) % 32, part = e % CPR;
-    *reinterpret_cast<u32x4*>(&xs[wh][row * ROWB + part * 16]) = stg[i];
+    *reinterpret_cast<u32x4*>(xs + wh * 32 * ROWB + row * ROWB + part * 16) = v;
   }
   __syncthreads();
-  const int W = which ? a.Wv : a.Wk;
-  if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
-  uint32_t* packed = which ? a.app_v : a.app_k;
-  const int64_t sbase = (int64_t)s * a.t_cap * W;
-  if (slot < K.n) {
-    const int grp = pick4(K.grp, slot);
-    if (grp != slot) load_group_raw(Vs, ms, grp, col, h, raw, mv);
-    bf16x8 Va[3][8];
-    split_group_operands(raw, Va);
-    encode_block<F32, ROWB>(xs[which], 0, col, h, Va, mv, a.t_new, a.t_new, a.t_new + 1, sbase, W, slot,
-                            pick4(K.bits, slot), pick4(K.pay, slot), packed);
+#pragma unroll 1
+  for (int which = 0; which < 2; ++which) {
+    const Kept K = read_kept((which ? a.bits_v : a.bits_k) + (int64_t)s * NG);
+    const int W = which ? a.Wv : a.Wk;
+    if (!K.ok || K.used > W) continue;  // width table inconsistent with the record: write nothing
+    uint32_t* packed = which ? a.app_v : a.app_k;
+    const int64_t sbase = (int64_t)s * a.t_cap * W;
+    const int slot = wave;
+    if (slot < K.n) {
+      const int grp = pick4(K.grp, slot);
+      float mv[16];
+      const float* m = (which ? a.mean_v : a.mean_k) + (int64_t)s * D + G * grp + 16 * h;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mv[j] = m[j];
+      encode_block_streamed<F32, ROWB>(xs + which * 32 * ROWB, 0, col, h, (which ? a.basis_v : a.basis_k) + (int64_t)s * D * D,
+                                       grp, mv, a.t_new, a.t_new, a.t_new + 1, sbase, W, slot, pick4(K.bits, slot),
+                                       pick4(K.pay, slot), packed);
+    }
+    // padding words of the record are zero
+    if (wave == 0 && lane < W - K.used) packed[rec_word(sbase, a.t_new, W, K.used + lane)] = 0u;
   }
-  // padding words of the record are zero
-  if (slot == 0 && lane < W - K.used) packed[rec_word(sbase, a.t_new, W, K.used + lane)] = 0u;
 }
 
 // ---------------------------------------------------------------------------
-// Query preparation, once per step: one workgroup per (kv head, sequence) writes
-// E2 = 2^-E, Qbar[h][g] = sum_{j in g} q'_hj and the score-MFMA A operands
-// [quad][slot][m][row][hi k0..k3, lo k0..k3] (see score_slot). For a decode step
-// (APP != 0) the grid has a second layer, z = 0, whose workgroups append the new
-// token of their stream meanwhile.
+// Query preparation of one (sequence, kv head), done by every scan workgroup in
+// its prologue (the result is identical in all of them): q' = scale * log2(e) *
+// q V_K for the n_qh heads, Qbar[h][g] = sum_{j in g} q'_hj, and the score-MFMA
+// A operands [quad][slot][m][row][hi k0..k3, lo k0..k3] (see score_slot) in
+// qa_s. Returns E2 = 2^-E. `scratch` is LDS of at least qprep_scratch_bytes(NQ).
 // ---------------------------------------------------------------------------
-template <int APP>
-__global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
-  __shared__ float qs[16][D];
-  __shared__ float part_s[4][16][D];
-  __shared__ float red_s[8];
-  __shared__ __attribute__((aligned(16))) KPlan plans_s[8];  // field plans of widths 1..8
-  const int kv = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-  const int s = b * a.n_kv_heads + kv;
-  if constexpr (APP != 0) {
-    // z = 0: append the new key and value; z = 1: query preparation (independent work)
-    if (blockIdx.z == 0) {
-      append_token<APP>(a, s, tid);
-      return;
-    }
-  }
+__host__ __device__ constexpr int qprep_scratch_bytes(int nq) {
+  return (3 * 4 * nq * D) * 4 + (int)sizeof(KGather);
+}
+
+// `issue_more` is called once the loads this step needs are in flight (the caller
+// puts its own, later-needed loads behind them).
+template <int NQ, typename F>
+__device__ __forceinline__ float prepare_query(const AttnArgs& a, int s, int b, int kv, int tid, uint8_t* scratch,
+                                               uint32_t* __restrict__ qa_s, float* __restrict__ qbar_s, float* red_s,
+                                               F&& issue_more) {
+  constexpr int NH = 4 * NQ;
+  constexpr int QPT = (NH * D) / 256;  // q values per thread
+  float(*qs)[D] = reinterpret_cast<float(*)[D]>(scratch);                          // [NH][D]: q, then q'
+  float(*part)[NH][D] = reinterpret_cast<float(*)[NH][D]>(scratch + NH * D * 4);  // [2][NH][D]
+  KField(*gat)[KM_MAX][4] = reinterpret_cast<KField(*)[KM_MAX][4]>(scratch + 3 * NH * D * 4);  // [8][m][k]
   const int nqh = a.n_qh;
   const uint32_t bwk = *reinterpret_cast<const uint32_t*>(a.bits_k + (int64_t)s * NG);
-  static_assert(sizeof(KPlan) % 4 == 0, "plan copy");
-  for (int i = tid; i < (int)(sizeof(KPLANS) / 4); i += 512)
-    reinterpret_cast<uint32_t*>(plans_s)[i] = reinterpret_cast<const uint32_t*>(KPLANS)[i];
-  for (int e = tid; e < 16 * D; e += 512) {
-    const int h = e >> 7, c = e & 127;
-    float v = 0.0f;
+  // column j of V_K, rows [64 half, 64 half + 64)
+  const int j = tid & 127, half = tid >> 7;
+  const float* Vk = a.basis_k + (int64_t)s * D * D + (int64_t)(64 * half) * D + j;
+  float v[64];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) v[i] = Vk[i * D];
+  float qv[QPT];
+#pragma unroll
+  for (int i = 0; i < QPT; ++i) {
+    const int e = tid + 256 * i, h = e >> 7, c = e & 127;
+    qv[i] = 0.0f;
     if (h < nqh) {
       const int64_t qi = ((int64_t)b * a.n_q_heads + kv * nqh + h) * D + c;
-      v = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi]);
+      qv[i] = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi]);
     }
-    qs[h][c] = v;
   }
-  // column j of V_K, rows [32 qtr, 32 qtr + 32): all loads issued before use
-  const int j = tid & 127, qtr = tid >> 7;
-  const float* Vk = a.basis_k + (int64_t)s * D * D + (int64_t)(32 * qtr) * D + j;
-  float v[32];
+  constexpr int GW = (int)(sizeof(KGather) / 4);
+  static_assert(sizeof(KGather) % 4 == 0 && GW <= 256, "gather table copy");
+  const uint32_t gw = tid < GW ? reinterpret_cast<const uint32_t*>(&KGATHER)[tid] : 0u;
+  issue_more();
 #pragma unroll
-  for (int i = 0; i < 32; ++i) v[i] = Vk[i * D];
+  for (int i = 0; i < QPT; ++i) {
+    const int e = tid + 256 * i;
+    qs[e >> 7][e & 127] = qv[i];
+  }
+  if (tid < GW) reinterpret_cast<uint32_t*>(gat)[tid] = gw;
   __syncthreads();
-  for (int h = 0; h < nqh; ++h) {
-    float acc = 0.0f;
+  float acc[NH];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) acc = __builtin_fmaf(qs[h][32 * qtr + i], v[i], acc);
-    part_s[qtr][h][j] = acc;
-  }
+  for (int h = 0; h < NH; ++h) acc[h] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 64; ++i)
+#pragma unroll
+    for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][64 * half + i], v[i], acc[h]);
+#pragma unroll
+  for (int h = 0; h < NH; ++h) part[half][h][j] = acc[h];
   __syncthreads();
   float amax = 0.0f;
-  for (int e = tid; e < 16 * D; e += 512) {
+  for (int e = tid; e < NH * D; e += 256) {
     const int h = e >> 7, c = e & 127;
-    const float q =
-        h < nqh ? ((part_s[0][h][c] + part_s[1][h][c]) + (part_s[2][h][c] + part_s[3][h][c])) * a.scale_log2 : 0.0f;
+    const float q = h < nqh ? (part[0][h][c] + part[1][h][c]) * a.scale_log2 : 0.0f;
     qs[h][c] = q;
     amax = __builtin_fmaxf(amax, __builtin_fabsf(q));
   }
   amax = wave_max(amax);
   if ((tid & 63) == 0) red_s[tid >> 6] = amax;
   __syncthreads();
-  amax = red_s[0];
-#pragma unroll
-  for (int i = 1; i < 8; ++i) amax = __builtin_fmaxf(amax, red_s[i]);
+  amax = __builtin_fmaxf(__builtin_fmaxf(red_s[0], red_s[1]), __builtin_fmaxf(red_s[2], red_s[3]));
   // 2^E brings max |q'| into [2^8, 2^9), so every A entry x = q' * 2^(E + e) (e <= 6)
   // stays below 2^15. x is split into hi = fp16(x) and lo = fp16((x - hi) * 2^11):
   // lo is kept in the normal fp16 range by its 2^11 and accumulates separately.
@@ -224,64 +225,52 @@ __global__ __launch_bounds__(512) void qprep_kernel(AttnArgs a) {
   int e2 = 0;
   if (amax > 0.0f) (void)__builtin_frexpf(amax, &e2);
   const int E = amax > 0.0f ? 9 - e2 : 0;
-  float* qp = a.qprep + (int64_t)s * QP;
-  if (tid == 0) {
-    qp[0] = __builtin_ldexpf(1.0f, -E);
-    qp[1] = qp[2] = qp[3] = 0.0f;
-  }
   {
-    // Qbar[h][g]: eight lanes per (head, group), four values each, then a lane reduction
-    const int ent = tid >> 3, part = tid & 7, h = ent >> 2, g = ent & 3;
-    float acc = 0.0f;
+    // Qbar[h][g]: four lanes per (head, group), eight values each, then a lane reduction
+    const int ent = tid >> 2, pt = tid & 3, h = ent >> 2, g = ent & 3;
+    if (ent < NH * NG) {
+      float sum = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc += qs[h][G * g + 4 * part + i];
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 4);
-    if (part == 0) qp[4 + ent] = acc;
+      for (int i = 0; i < 8; ++i) sum += qs[h][G * g + 8 * pt + i];
+      sum += __shfl_xor(sum, 1);
+      sum += __shfl_xor(sum, 2);
+      if (pt == 0) qbar_s[ent] = sum;
+    }
   }
-  // Score-MFMA A operands, entry (quad, slot, m, r): K elements k = 0..3 are the
-  // fields of ops 2m + k/2, half k%2, of the slot's plan; each is q'_{4quad+r}
-  // of the field's coefficient times 2^(E + e) as fp16 hi + lo.
-  uint32_t* qa = reinterpret_cast<uint32_t*>(qp + 4 + 64);
-  const int nquad = (nqh + 3) >> 2;
-  for (int e = tid; e < nquad * NG * KM_MAX * 4; e += 512) {
+  // Score-MFMA A operands, entry (quad, slot, m, r): K element k is field
+  // (op 2m + k/2, half k%2) of the slot's plan, i.e. q'_{4quad+r} of the field's
+  // coefficient times 2^(E + e), as fp16 hi + lo.
+  for (int e = tid; e < NQ * NG * KM_MAX * 4; e += 256) {
     const int r = e & 3, m = (e >> 2) % KM_MAX, slot = (e / (4 * KM_MAX)) & 3, quad = e / (4 * KM_MAX * NG);
     int g = -1, B = 0, c = 0;
+#pragma unroll
     for (int gg = 0; gg < NG; ++gg) {
       const int bb = (int)((bwk >> (8 * gg)) & 0xFFu);
-      if (bb != 0) {
-        if (c == slot) {
-          g = gg;
-          B = bb;
-        }
-        ++c;
-      }
+      const bool here = bb != 0 && c == slot;
+      g = here ? gg : g;
+      B = here ? bb : B;
+      c += bb != 0 ? 1 : 0;
     }
-    if (g < 0 || B > 8) continue;
-    const KPlan& P = plans_s[B - 1];
-    if (2 * m >= P.n_ops) continue;
-    const int h = 4 * quad + r;
-    uint32_t hi[4], lo[4];
+    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+    if (g >= 0 && B <= 8) {
+      const int h = 4 * quad + r;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = 2 * m + (k >> 1);
-      float x = 0.0f;
-      if (i < P.n_ops) {
-        const KField f = P.op[i].f[k & 1];
-        if (f.code >= 0) x = __builtin_ldexpf(qs[h][G * g + f.code], E + f.e);
+      for (int k = 0; k < 4; ++k) {
+        const KField f = gat[B - 1][m][k];
+        const float x = f.code >= 0 ? __builtin_ldexpf(qs[h][G * g + f.code], E + f.e) : 0.0f;
+        const _Float16 xh = (_Float16)x;
+        const _Float16 xl = (_Float16)((x - (float)xh) * 2048.0f);
+        hi[k] = __builtin_bit_cast(uint16_t, xh);
+        lo[k] = __builtin_bit_cast(uint16_t, xl);
       }
-      const _Float16 xh = (_Float16)x;
-      const _Float16 xl = (_Float16)((x - (float)xh) * 2048.0f);
-      hi[k] = __builtin_bit_cast(uint16_t, xh);
-      lo[k] = __builtin_bit_cast(uint16_t, xl);
     }
-    uint32_t* dst = qa + ((((quad * NG + slot) * KM_MAX + m) * 4 + r) * 4);
+    uint32_t* dst = qa_s + ((((quad * NG + slot) * KM_MAX + m) * 4 + r) * 4);
     dst[0] = hi[0] | (hi[1] << 16);
     dst[1] = hi[2] | (hi[3] << 16);
     dst[2] = lo[0] | (lo[1] << 16);
     dst[3] = lo[2] | (lo[3] << 16);
   }
+  return __builtin_ldexpf(1.0f, -E);
 }
 
 // Bytes of LDS holding the softmax-weight rows of all wavefronts: per wave and kept
@@ -416,10 +405,13 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   uint16_t* wt = reinterpret_cast<uint16_t*>(smem + WAVES * wpw * TROW) + wave * (NG * 2 * NH * WROW);
   const int64_t kbase = (int64_t)s * a.t_cap * Wk;
   const int64_t vbase = (int64_t)s * a.t_cap * Wv;
+  // chunk c < n_chunks - 1 holds tiles [c * tpc, (c + 1) * tpc) of all but the last
+  // tile; the last chunk holds the last tile alone
   const int64_t n_tiles = (a.n_tokens + 63) >> 6;
-  const int64_t tile_begin = (int64_t)chunk * a.tiles_per_chunk;
-  int64_t tile_end = tile_begin + a.tiles_per_chunk;
-  if (tile_end > n_tiles) tile_end = n_tiles;
+  const bool last_chunk = chunk == a.n_chunks - 1;
+  const int64_t tile_begin = last_chunk ? n_tiles - 1 : (int64_t)chunk * a.tiles_per_chunk;
+  int64_t tile_end = last_chunk ? n_tiles : tile_begin + a.tiles_per_chunk;
+  if (!last_chunk && tile_end > n_tiles - 1) tile_end = n_tiles - 1;
 
   float m_run[NH], l_run[NH], zacc[NH][NG];
 #pragma unroll
@@ -464,21 +456,32 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       }
     }
   };
-  // the first tile's loads go out before anything that waits on the width tables
-  // (they stay in bounds whatever the tables hold)
+  // In a decode step the workgroup of the last chunk (the last tile) first appends
+  // the new token of its stream (and makes the records visible to its own loads).
   int64_t tt = tile_begin + wave;
-  if (tt < tile_end) load_tile(tt);
+  if (a.app_k != nullptr && last_chunk) {
+    if (a.app_f32)
+      append_token<true>(a, s, tid, reinterpret_cast<uint8_t*>(smem));
+    else
+      append_token<false>(a, s, tid, reinterpret_cast<uint8_t*>(smem));
+    __threadfence();
+    __syncthreads();
+  }
+
+  // ---- prologue: query preparation of this (sequence, kv head) into LDS; the
+  // first tile's loads (in bounds whatever the width tables hold) queue behind
+  // its loads ----
+  __shared__ float red_s[WAVES];
+  __shared__ float e2_s;
+  const float E2q = prepare_query<NQ>(a, s, b, kv, tid, reinterpret_cast<uint8_t*>(smem), qa_s, qbar_s, red_s, [&] {
+    if (tt < tile_end) load_tile(tt);
+  });
   const Kept Kk = read_kept(a.bits_k + (int64_t)s * NG);
   const Kept Kv = read_kept(a.bits_v + (int64_t)s * NG);
   const bool ok = Kk.ok && Kv.ok && Kk.used <= Wk && Kv.used <= Wv;
-
-  // ---- prologue: prepared query data of this (sequence, kv head) ----
-  const float* qp = a.qprep + (int64_t)s * QP;
-  for (int i = tid; i < NQ * QA_QUAD; i += 256) qa_s[i] = reinterpret_cast<const uint32_t*>(qp + 4 + 64)[i];
-  if (tid < 64) qbar_s[tid] = qp[4 + tid];
-  const float E2 = qp[0];
-
-  __syncthreads();  // prepared query data in LDS
+  if (tid == 0) e2_s = E2q;
+  __syncthreads();  // prepared query data in LDS; the scratch may now hold tiles
+  const float E2 = e2_s;
 
   Kept kk = Kk, kvv = Kv;
   for (; ok && tt < tile_end; tt += WAVES) {
@@ -815,18 +818,22 @@ __global__ __launch_bounds__(1024) void combine_kernel(AttnArgs a) {
 namespace spectra {
 using namespace spectra_dev;
 
-size_t attention_qprep_floats(int32_t batch, int32_t, int32_t n_kv_heads) { return (size_t)batch * n_kv_heads * QP; }
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks) {
   return (size_t)batch * n_q_heads * n_chunks * PART;
 }
+// Split of each (sequence, kv head) token range into chunks of whole tiles: about
+// 768 workgroups of four wavefronts, >= 4 tiles per wavefront, over all tiles but
+// the last; the last tile is a chunk of its own (in a decode step its workgroup
+// also appends the new token).
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk) {
   const int64_t n_tiles = (n_tokens + 63) / 64;
+  const int64_t body = n_tiles > 0 ? n_tiles - 1 : 0;
   const int64_t groups = (int64_t)batch * n_kv_heads;
-  const int64_t want = (768 + groups - 1) / groups;   // ~768 workgroups of 4 wavefronts
-  int64_t tpc = (n_tiles + want - 1) / want;
-  if (tpc < 16) tpc = 16;                              // >= 4 tiles per wavefront
-  if (tpc > n_tiles) tpc = n_tiles > 0 ? n_tiles : 1;
-  const int64_t nch = n_tiles > 0 ? (n_tiles + tpc - 1) / tpc : 1;
+  const int64_t want = (768 + groups - 1) / groups;
+  int64_t tpc = (body + want - 1) / want;
+  if (tpc < 16) tpc = 16;
+  if (tpc > body) tpc = body > 0 ? body : 1;
+  const int64_t nch = (body + tpc - 1) / tpc + 1;
   *tiles_per_chunk = (int32_t)tpc;
   return (int32_t)nch;
 }
@@ -837,6 +844,8 @@ static void launch_nq_pw(const AttnArgs& a, hipStream_t st) {
   size_t tiles = (size_t)WAVES * wpw * TROW * 4 + (size_t)attn_wt_bytes(NQ);
   size_t merge = (size_t)WAVES * (NQ <= 2 ? 8 * NQ : 4 * NQ) * AROW * 4;  // per-wave value sums
   size_t lds = tiles > merge ? tiles : merge;
+  if ((size_t)qprep_scratch_bytes(NQ) > lds) lds = qprep_scratch_bytes(NQ);
+  if (a.app_k && (size_t)append_stage_bytes(a.app_f32 != 0) > lds) lds = append_stage_bytes(a.app_f32 != 0);
   const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
   hipLaunchKernelGGL((attn_kernel<NQ, PW, EXACT>), grid, dim3(256), lds, st, a);
 }
@@ -870,17 +879,8 @@ static hipError_t launch_scan_combine(const AttnArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(qprep_kernel<0>, dim3(a.n_kv_heads, a.batch), dim3(512), 0, st, a);
-  return launch_scan_combine(a, st);
-}
-
-hipError_t launch_decode_step(const AttnArgs& a, hipStream_t st) {
-  if (a.app_f32)
-    hipLaunchKernelGGL(qprep_kernel<2>, dim3(a.n_kv_heads, a.batch, 2), dim3(512), 0, st, a);
-  else
-    hipLaunchKernelGGL(qprep_kernel<1>, dim3(a.n_kv_heads, a.batch, 2), dim3(512), 0, st, a);
-  return launch_scan_combine(a, st);
-}
+// Decode-step attention; with a.app_k set, the decode step (append first): the
+// scan kernel, then the chunk combine.
+hipError_t launch_attention(const AttnArgs& a, hipStream_t st) { return launch_scan_combine(a, st); }
 
 }  // namespace spectra

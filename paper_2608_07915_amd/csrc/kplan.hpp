@@ -87,4 +87,28 @@ constexpr KPlan make_kplan(int B) {
   return P;
 }
 
+// The same plans as MFMA operand gathers: score MFMA m of a width-B slot takes the
+// fields of ops 2m and 2m + 1 (low half, high half of each) as its four K elements;
+// entry [B - 1][m][k] is field (op 2m + k / 2, half k % 2), code -1 where empty.
+constexpr int KMFMA_MAX = (KOPS_MAX + 1) / 2;
+struct alignas(4) KGather {
+  KField f[8][KMFMA_MAX][4];
+};
+constexpr KGather make_kgather() {
+  KGather T{};
+  for (int B = 1; B <= 8; ++B) {
+    const KPlan P = make_kplan(B);
+    for (int m = 0; m < KMFMA_MAX; ++m)
+      for (int k = 0; k < 4; ++k) {
+        const int i = 2 * m + k / 2;
+        KField f{};
+        f.code = -1;
+        f.e = 0;
+        if (i < P.n_ops) f = P.op[i].f[k % 2];
+        T.f[B - 1][m][k] = f;
+      }
+  }
+  return T;
+}
+
 }  // namespace spectra_dev
