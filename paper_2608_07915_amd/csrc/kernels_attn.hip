@@ -154,7 +154,7 @@ __device__ __forceinline__ void append_token(const AttnArgs& a, int s, int tid, 
 // qa_s. Returns E2 = 2^-E. `scratch` is LDS of at least qprep_scratch_bytes(NQ).
 // ---------------------------------------------------------------------------
 __host__ __device__ constexpr int qprep_scratch_bytes(int nq) {
-  return (3 * 4 * nq * D) * 4 + (int)sizeof(KGather);
+  return (5 * 4 * nq * D) * 4 + (int)sizeof(KGather);
 }
 
 // `issue_more` is called once the loads this step needs are in flight (the caller
@@ -166,16 +166,19 @@ __device__ __forceinline__ float prepare_query(const AttnArgs& a, int s, int b, 
   constexpr int NH = 4 * NQ;
   constexpr int QPT = (NH * D) / 256;  // q values per thread
   float(*qs)[D] = reinterpret_cast<float(*)[D]>(scratch);                          // [NH][D]: q, then q'
-  float(*part)[NH][D] = reinterpret_cast<float(*)[NH][D]>(scratch + NH * D * 4);  // [2][NH][D]
-  KField(*gat)[KM_MAX][4] = reinterpret_cast<KField(*)[KM_MAX][4]>(scratch + 3 * NH * D * 4);  // [8][m][k]
+  float(*part)[NH][D] = reinterpret_cast<float(*)[NH][D]>(scratch + NH * D * 4);  // [4][NH][D]
+  KField(*gat)[KM_MAX][4] = reinterpret_cast<KField(*)[KM_MAX][4]>(scratch + 5 * NH * D * 4);  // [8][m][k]
   const int nqh = a.n_qh;
   const uint32_t bwk = *reinterpret_cast<const uint32_t*>(a.bits_k + (int64_t)s * NG);
-  // column j of V_K, rows [64 half, 64 half + 64)
-  const int j = tid & 127, half = tid >> 7;
-  const float* Vk = a.basis_k + (int64_t)s * D * D + (int64_t)(64 * half) * D + j;
-  float v[64];
+  // Only the kept groups' q' are needed. Columns 0..63 (groups 0 and 1, kept in the
+  // common case: widths fall with the variance) are requested before the width
+  // table arrives; columns 64..127 only when groups 2 or 3 are kept. Thread
+  // (quarter qt, column jj) takes rows [32 qt, 32 qt + 32).
+  const int jj = tid & 63, qt = tid >> 6;
+  const float* Vk = a.basis_k + (int64_t)s * D * D + (int64_t)(32 * qt) * D + jj;
+  float v[32];
 #pragma unroll
-  for (int i = 0; i < 64; ++i) v[i] = Vk[i * D];
+  for (int i = 0; i < 32; ++i) v[i] = Vk[i * D];
   float qv[QPT];
 #pragma unroll
   for (int i = 0; i < QPT; ++i) {
@@ -197,20 +200,30 @@ __device__ __forceinline__ float prepare_query(const AttnArgs& a, int s, int b, 
   }
   if (tid < GW) reinterpret_cast<uint32_t*>(gat)[tid] = gw;
   __syncthreads();
-  float acc[NH];
+  const int npass = (bwk >> 16) != 0u ? 2 : 1;  // groups 2 or 3 kept: columns 64..127 too
+#pragma unroll 1
+  for (int pass = 0; pass < npass; ++pass) {
+    if (pass > 0) {
 #pragma unroll
-  for (int h = 0; h < NH; ++h) acc[h] = 0.0f;
+      for (int i = 0; i < 32; ++i) v[i] = Vk[i * D + 64];
+    }
+    float acc[NH];
 #pragma unroll
-  for (int i = 0; i < 64; ++i)
+    for (int h = 0; h < NH; ++h) acc[h] = 0.0f;
 #pragma unroll
-    for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][64 * half + i], v[i], acc[h]);
+    for (int i = 0; i < 32; ++i)
 #pragma unroll
-  for (int h = 0; h < NH; ++h) part[half][h][j] = acc[h];
+      for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][32 * qt + i], v[i], acc[h]);
+#pragma unroll
+    for (int h = 0; h < NH; ++h) part[qt][h][64 * pass + jj] = acc[h];
+  }
   __syncthreads();
   float amax = 0.0f;
   for (int e = tid; e < NH * D; e += 256) {
     const int h = e >> 7, c = e & 127;
-    const float q = h < nqh ? (part[0][h][c] + part[1][h][c]) * a.scale_log2 : 0.0f;
+    const bool kept = ((bwk >> (8 * (c >> 5))) & 0xFFu) != 0u;
+    const float q =
+        (h < nqh && kept) ? ((part[0][h][c] + part[1][h][c]) + (part[2][h][c] + part[3][h][c])) * a.scale_log2 : 0.0f;
     qs[h][c] = q;
     amax = __builtin_fmaxf(amax, __builtin_fabsf(q));
   }
@@ -556,30 +569,39 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     // ---- online softmax (log2 domain) against a reference m that moves only when
     // a score exceeds it by more than RESCALE_SLACK: weights stay <= 2^RESCALE_SLACK,
     // and the rescale of the running sums is rare after the first tile ----
-    float p[NH];
+    float p[NH], x[NH];
+    bool over = false;
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
-      const bool live = valid && h < nqh;
-      const float x = live ? sc[h] : -__builtin_inff();
-      if (__any(x > m_run[h] + RESCALE_SLACK)) {
-        const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x));
-        const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
-        l_run[h] *= alpha;
+      x[h] = (valid && h < nqh) ? sc[h] : -__builtin_inff();
+      over = over || x[h] > m_run[h] + RESCALE_SLACK;
+    }
+    if (__any(over)) {  // rare after the first tile: one branch for all heads
 #pragma unroll
-        for (int g = 0; g < NG; ++g) zacc[h][g] *= alpha;
+      for (int h = 0; h < NH; ++h) {
+        if (__any(x[h] > m_run[h] + RESCALE_SLACK)) {
+          const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x[h]));
+          const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
+          l_run[h] *= alpha;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int row = 4 * kq + j;
-          const float f = (row == h || (STACK && row == NH + h)) ? alpha : 1.0f;
+          for (int g = 0; g < NG; ++g) zacc[h][g] *= alpha;
 #pragma unroll
-          for (int g = 0; g < NG; ++g) {
-            vacc[g][0][j] *= f;
-            vacc[g][1][j] *= f;
+          for (int j = 0; j < 4; ++j) {
+            const int row = 4 * kq + j;
+            const float f = (row == h || (STACK && row == NH + h)) ? alpha : 1.0f;
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+              vacc[g][0][j] *= f;
+              vacc[g][1][j] *= f;
+            }
           }
+          m_run[h] = mn;
         }
-        m_run[h] = mn;
       }
-      p[h] = live ? __builtin_amdgcn_exp2f(x - m_run[h]) : 0.0f;
+    }
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      p[h] = x[h] != -__builtin_inff() ? __builtin_amdgcn_exp2f(x[h] - m_run[h]) : 0.0f;
       l_run[h] += p[h];
     }
     // softmax weight times value scale, as bf16 hi/lo rows; zero-point terms per lane
@@ -617,7 +639,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       const int B = kvv.bits[sl], pay = kvv.pay[sl];
       auto body = [&](auto cls) {
         constexpr int CLS = decltype(cls)::value;
-#pragma unroll 1
+#pragma unroll
         for (int th = 0; th < 2; ++th) {
           const int tok0 = 32 * th + 8 * kq;
           // stacked: rows 0..2NH-1 = hi then lo; otherwise hi rows and lo rows separately
