@@ -44,10 +44,9 @@ CALIB_BYTES = 256 << 20
 DECODE_STEP_SOURCES = ("kernels_attn.hip", "kplan.hpp", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "0ee7091a1ca6b11d9d5b1f6e87f628ba9568deed8d9bfed1fe0a062f5d86c9e6": {
-        "fetch_bytes": 72906752, "write_bytes": 1668403,
-        "per_kernel": {"qprep_kernel<1>": [1195213, 15667], "attn_kernel<1,8,true>": [67897139, 1636352],
-                       "combine_kernel": [3814400, 16384]}},
+    "9c25c89e4410da24064f9c110cc6e904e50cafd79382d5dde23cdb2192380ddf": {
+        "fetch_bytes": 74618675, "write_bytes": 1674240,
+        "per_kernel": {"attn_kernel<1,8,true>": [70776627, 1657856], "combine_kernel": [3842048, 16384]}},
 }
 
 
@@ -314,7 +313,7 @@ def main():
                              "generated_tokens_per_s": round(1.0 / (att_call_ms * 1e-3 * L), 2)},
         "roofline": {"bound": "hbm", "achieved": round(att_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": "decode_step (append + query prep, split-K scan, combine), per layer call",
+                     "kernel": "decode_step (split-K scan with in-kernel query prep and append, then combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
         "traffic_detail": measured,
         "decode_launch": "eager" if args.eager else "hip_graph",
