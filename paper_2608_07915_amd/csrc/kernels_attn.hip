@@ -302,15 +302,18 @@ __host__ __device__ constexpr int attn_wt_bytes(int nq) { return WAVES * NG * (8
 template <int CLS>
 __device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, int pay, int used, int b, int off,
                                              int tok0, uint32_t magic, u32x4& r0, u32x4& r1) {
+  // offsets fit in 24 bits: full-rate 24-bit multiplies instead of 32-bit ones
   const int w = pay + (off >> 5), o = off & 31;
-  const u32x4 a0 = *reinterpret_cast<const u32x4*>(vt + w * TROW + tok0);
-  const u32x4 a1 = *reinterpret_cast<const u32x4*>(vt + w * TROW + tok0 + 4);
+  const uint32_t* row = vt + __umul24(w, TROW) + tok0;
+  const u32x4 a0 = *reinterpret_cast<const u32x4*>(row);
+  const u32x4 a1 = *reinterpret_cast<const u32x4*>(row + 4);
   const uint32_t M = (1u << b) - 1u;
   const uint32_t MM = M | (M << 16);
   if constexpr (CLS == 0) {
     // byte k of two tokens' words in both halves of one register, then shift and mask
     const uint32_t k = (uint32_t)o >> 3, sh = (uint32_t)o & 7u;
-    const uint32_t sel = k * 0x00000101u + (4u + k) * 0x01010000u;
+    // bytes k, k, 4 + k, 4 + k (a byte broadcast, not a 32-bit multiply)
+    const uint32_t sel = __builtin_amdgcn_perm(k, k, 0u) | 0x04040000u;
     uint32_t y[4];
     y[0] = __builtin_amdgcn_perm(a0[1], a0[0], sel);
     y[1] = __builtin_amdgcn_perm(a0[3], a0[2], sel);
@@ -323,8 +326,9 @@ __device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, in
     }
   } else {
     const int wn = (w + 1 < used) ? w + 1 : w;  // the next word only matters when a code straddles
-    const u32x4 b0 = *reinterpret_cast<const u32x4*>(vt + wn * TROW + tok0);
-    const u32x4 b1 = *reinterpret_cast<const u32x4*>(vt + wn * TROW + tok0 + 4);
+    const uint32_t* rown = vt + __umul24(wn, TROW) + tok0;
+    const u32x4 b0 = *reinterpret_cast<const u32x4*>(rown);
+    const u32x4 b1 = *reinterpret_cast<const u32x4*>(rown + 4);
     uint32_t c[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -497,7 +501,12 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const float E2 = e2_s;
 
   Kept kk = Kk, kvv = Kv;
+  // bit offset 2 col b (< 256) of the lane's first value code in each kept slot, one byte per slot
+  uint32_t voffs = 0u;
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl) voffs |= (uint32_t)(2 * col * Kv.bits[sl]) << (8 * sl);
   for (; ok && tt < tile_end; tt += WAVES) {
+    asm volatile("" : "+v"(voffs));
     // keep per-tile LDS reads (operand tables) inside the loop instead of in registers,
     // and make the slot tables opaque so their derived scalars are not hoisted out of it
     asm volatile("" ::: "memory");
@@ -630,6 +639,8 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 
     // ---- value accumulation over the kept value coefficients ----
     const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
+    constexpr int AR = STACK ? 2 * NH : NH;  // weight rows of one MFMA (8, 12 or 16)
+    static_assert(AR >= 8 && AR <= 16, "rows past AR re-read row col - AR");
     uint32_t vmagic = 0x43004300u;  // exponent of 128 in both halves, in a VGPR (see value_codes2)
     asm volatile("" : "+v"(vmagic));
 #pragma unroll
@@ -642,14 +653,16 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int th = 0; th < 2; ++th) {
           const int tok0 = 32 * th + 8 * kq;
-          // stacked: rows 0..2NH-1 = hi then lo; otherwise hi rows and lo rows separately
-          bf16x8 aw = bf16x8{};
-          if (col < (STACK ? 2 * NH : NH)) aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + col * WROW + tok0));
+          // stacked: rows 0..2NH-1 = hi then lo; otherwise hi rows and lo rows separately.
+          // Lanes of MFMA rows past the weight rows read a weight row again (no masked
+          // load): those accumulator rows are never read.
+          const int arow = col < AR ? col : col - AR;
+          const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * WROW + tok0));
           bf16x8 awl = bf16x8{};
-          if (!STACK && col < NH) awl = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + (NH + col) * WROW + tok0));
+          if constexpr (!STACK) awl = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + (NH + arow) * WROW + tok0));
           // MFMA column col of block c2 is in-group coefficient 2 col + c2
           u32x4 vc[2];
-          value_codes2<CLS>(vt, pay, kvv.used, B, 2 * col * B, tok0, vmagic, vc[0], vc[1]);
+          value_codes2<CLS>(vt, pay, kvv.used, B, (int)((voffs >> (8 * sl)) & 0xFFu), tok0, vmagic, vc[0], vc[1]);
 #pragma unroll
           for (int c2 = 0; c2 < 2; ++c2) {
             const bf16x8 bop = as_bf16x8(vc[c2]);
