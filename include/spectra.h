@@ -105,6 +105,16 @@ spectra_status spectra_codec_init(spectra_codec* c, const spectra_params* p, int
 int32_t spectra_record_budget_bits(const spectra_params* p);
 int32_t spectra_record_words(const spectra_params* p);
 
+/* Asymmetric key/value split (Sec. 3.1: ranks r_k = kappa B and r_v = (1 - kappa) B;
+ * kappa = 1/2 and 1/4 in App. F). The allocation turns a bit budget into a kept
+ * rank, so the split is applied to the two records' combined budget 2R (R from p):
+ * keys get R_k = 32 * floor(kappa * 2R / 32 + 1/2) bits, values R_v = 2R - R_k.
+ * Writes copies of *p with budget_bits = R_k into *p_k and R_v into *p_v (key and
+ * value codecs then have different record widths). SPECTRA_EINVAL unless
+ * 0 < kappa < 1 and both budgets hold at least one group (g + meta_bits). Host only. */
+spectra_status spectra_split_budget(const spectra_params* p, double kappa, spectra_params* p_k,
+                                    spectra_params* p_v);
+
 /* Number of uint32 words of a packed cache holding t_capacity tokens per stream
  * (n_streams * t_capacity * W); t_capacity must be a multiple of 64. */
 int64_t spectra_packed_words(const spectra_codec* c, int64_t t_capacity);

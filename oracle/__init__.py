@@ -10,7 +10,7 @@ Every function is pinned by ``tests/test_oracle_pins.py`` against values the
 mathematics fixes (closed forms, identities, brute force, hand-built records).
 """
 from .codec import (  # noqa: F401
-    Params, FitResult, record_budget_bits, record_words,
+    Params, FitResult, record_budget_bits, record_words, split_budget,
     fit, allocate_bits, allocate_bits_bruteforce,
     quantize, quantize_given_meta, dequantize, pack, unpack, physical_index, encode, decode,
     attention_mode_a, attention_mode_b, softmax_f64, fp16_rne_sat, fp16_bits,

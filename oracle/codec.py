@@ -21,7 +21,7 @@ orthonormal coefficients, exact integer allocation, record format).
 from __future__ import annotations
 
 import math
-from dataclasses import dataclass
+from dataclasses import dataclass, replace
 from itertools import product
 from typing import List, Sequence, Tuple
 
@@ -60,6 +60,31 @@ def record_budget_bits(p: Params) -> int:
 def record_words(p: Params) -> int:
     """Record width W in 32-bit words: floor(R / 32)."""
     return record_budget_bits(p) // 32
+
+
+def split_budget(p: Params, kappa: float) -> Tuple[Params, Params]:
+    """Asymmetric key/value split of the per-token budget (Sec. 3.1: r_k = kappa B,
+    r_v = (1 - kappa) B; App. F: rates count payload and metadata).
+
+    Reading: the allocation turns a bit budget into a kept rank (zero-bit groups
+    are dropped, Sec. 3.2), so the paper's split of the rank budget between the
+    key and value paths is realised as a split of the two records' combined
+    per-token budget 2R. Keys get R_k = 32 * floor(kappa * 2R / 32 + 1/2) bits
+    (whole words, nearest, halves up) and values R_v = 2R - R_k; each tensor is
+    then allocated on its own budget. kappa = 1/2 gives the symmetric setting
+    (App. F: 1/2 for the water-filling variant, 1/4 for the low-rank one). Both
+    budgets must pay for at least one group (g + meta_bits bits).
+    Returns (params_k, params_v) with budget_bits set.
+    """
+    if not (0.0 < kappa < 1.0):
+        raise ValueError("kappa must lie in (0, 1)")
+    total = 2 * record_budget_bits(p)
+    rk = 32 * int(math.floor(kappa * total / 32 + 0.5))
+    rv = total - rk
+    one = p.group_size + p.meta_bits
+    if rk < one or rv < one:
+        raise ValueError("split leaves a tensor without a whole group")
+    return replace(p, budget_bits=rk), replace(p, budget_bits=rv)
 
 
 # ----------------------------------------------------------------------------

@@ -42,6 +42,7 @@ _SIGNATURES = {
     "spectra_codec_init": (_I32, [_PC, _PP, _I64]),
     "spectra_record_budget_bits": (_I32, [_PP]),
     "spectra_record_words": (_I32, [_PP]),
+    "spectra_split_budget": (_I32, [_PP, ctypes.c_double, _PP, _PP]),
     "spectra_packed_words": (_I64, [_PC, _I64]),
     "spectra_fit_workspace_bytes": (_SZ, [_PC, _I64]),
     "spectra_fit_basis": (_I32, [_PC, _P, _I32, _I64, _I64, _I64, _P, _SZ, _P]),

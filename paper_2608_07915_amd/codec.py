@@ -7,8 +7,9 @@ codec runs in the HIP library. Function names match the C ABI in
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 from dataclasses import dataclass
-from typing import Optional
+from typing import Optional, Tuple
 
 import numpy as np
 
@@ -98,6 +99,15 @@ def spectra_record_words(params: Params) -> int:
 
 def spectra_record_budget_bits(params: Params) -> int:
     return int(_lib.get().spectra_record_budget_bits(ctypes.byref(params.c())))
+
+
+def spectra_split_budget(params: Params, kappa: float) -> Tuple[Params, Params]:
+    """Key and value params for the asymmetric split kappa of the combined budget."""
+    pk, pv = spectra_params(), spectra_params()
+    check(_lib.get().spectra_split_budget(ctypes.byref(params.c()), ctypes.c_double(kappa), ctypes.byref(pk),
+                                          ctypes.byref(pv)))
+    return dataclasses.replace(params, budget_bits=int(pk.budget_bits)), \
+        dataclasses.replace(params, budget_bits=int(pv.budget_bits))
 
 
 def spectra_fit_workspace_bytes(codec: Codec, n_tokens: int) -> int:

@@ -120,6 +120,26 @@ spectra_status spectra_codec_init(spectra_codec* c, const spectra_params* p, int
 int32_t spectra_record_budget_bits(const spectra_params* p) { return p ? budget_bits(*p) : -1; }
 int32_t spectra_record_words(const spectra_params* p) { return p ? record_words(*p) : -1; }
 
+spectra_status spectra_split_budget(const spectra_params* p, double kappa, spectra_params* p_k, spectra_params* p_v) {
+  if (!p || !p_k || !p_v) return fail(SPECTRA_EINVAL, "null argument");
+  spectra_status st = check_params(*p);
+  if (st != SPECTRA_OK) return st;
+  if (!(kappa > 0.0 && kappa < 1.0)) return fail(SPECTRA_EINVAL, "kappa must lie in (0, 1)");
+  // the two records' combined budget, keys' share rounded to whole words
+  const int64_t total = 2 * (int64_t)budget_bits(*p);
+  const int64_t rk = 32 * (int64_t)std::floor(kappa * (double)total / 32.0 + 0.5);
+  const int64_t rv = total - rk;
+  const int64_t one = (int64_t)p->group_size + p->meta_bits;
+  if (rk < one || rv < one)
+    return fail(SPECTRA_EINVAL, "kappa=%g leaves a tensor without a whole group (%lld + %lld bits)", kappa,
+                (long long)rk, (long long)rv);
+  *p_k = *p;
+  *p_v = *p;
+  p_k->budget_bits = (int32_t)rk;
+  p_v->budget_bits = (int32_t)rv;
+  return SPECTRA_OK;
+}
+
 int64_t spectra_packed_words(const spectra_codec* c, int64_t t_capacity) {
   if (!c || t_capacity < 0 || t_capacity % 64 != 0) return -1;
   return c->n_streams * t_capacity * (int64_t)c->record_words;

@@ -40,30 +40,31 @@ def _fit_encode_with_bits(x_dev, p, t_cap, bits):
 
 
 def run_and_check(w, T, batch, ratio, scale=0.0, n_tokens=None, check_heads=None, p=None, bits_k=None,
-                  bits_v=None):
+                  bits_v=None, p_v=None):
+    """p: key params (and value params unless p_v is given)."""
     p = O.Params(ratio=ratio) if p is None else p
+    p_v = p if p_v is None else p_v
     xk, xv = _workload_streams(w, T, batch)
     t_cap = (T + 63) // 64 * 64
     ck, pk = _fit_encode_with_bits(to_device(xk, w.dtype), p, t_cap, bits_k)
-    cv, pv = _fit_encode_with_bits(to_device(xv, w.dtype), p, t_cap, bits_v)
+    cv, pv = _fit_encode_with_bits(to_device(xv, w.dtype), p_v, t_cap, bits_v)
     q = _queries(w, batch)
     n = T if n_tokens is None else n_tokens
     out = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, n, to_device(q, w.dtype), w.n_kv_heads,
                                      softmax_scale=scale).cpu().numpy()
     assert np.all(np.isfinite(out))
-    W = O.record_words(p)
     sc = scale if scale > 0 else 0.0
     worst_own, worst_same = 0.0, 0.0
     for b in range(batch):
         kh_same, vh_same, kh_own, vh_own = [], [], [], []
         for h in range(w.n_kv_heads):
             s = b * w.n_kv_heads + h
-            for tensor, codec, packed, x, same, own in ((0, ck, pk, xk, kh_same, kh_own), (1, cv, pv, xv, vh_same, vh_own)):
+            for par, codec, packed, x, same, own in ((p, ck, pk, xk, kh_same, kh_own), (p_v, cv, pv, xv, vh_same, vh_own)):
                 basis, mean, bits = codec_state(codec, s)
-                rec = records_of(packed, s, 0, n, t_cap, W)
-                same.append(O.decode(rec, basis, mean, bits, p))
-                rec_o, *_ = O.encode(values_f64(x[s][:n], w.dtype), basis, mean, bits, p)
-                own.append(O.decode(rec_o, basis, mean, bits, p))
+                rec = records_of(packed, s, 0, n, t_cap, O.record_words(par))
+                same.append(O.decode(rec, basis, mean, bits, par))
+                rec_o, *_ = O.encode(values_f64(x[s][:n], w.dtype), basis, mean, bits, par)
+                own.append(O.decode(rec_o, basis, mean, bits, par))
         q64 = values_f64(q[b], w.dtype)
         ref_same = O.attention_mode_a(q64, np.stack(kh_same), np.stack(vh_same), sc)
         ref_own = O.attention_mode_a(q64, np.stack(kh_own), np.stack(vh_own), sc)
@@ -134,3 +135,14 @@ def test_attention_non_prefix_kept_groups(bits_k, bits_v):
     from dataclasses import replace
     w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=2, n_q_heads=8)
     run_and_check(w, 700, 1, 0.0, p=O.Params(budget_bits=32 * 9), bits_k=bits_k, bits_v=bits_v)
+
+
+@pytest.mark.parametrize("kappa", [0.25, 0.75])
+def test_attention_asymmetric_budget_split(kappa):
+    """Key and value records of different widths from the kappa split of the 8x
+    budget (Sec. 3.1, App. F): kappa = 1/4 gives 4-word keys and 12-word values."""
+    from dataclasses import replace
+    w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=2, n_q_heads=8)
+    pk, pv = O.split_budget(O.Params(ratio=8.0), kappa)
+    assert {O.record_words(pk), O.record_words(pv)} == {4, 12}
+    run_and_check(w, 1500, 1, 0.0, p=pk, p_v=pv)

@@ -23,18 +23,24 @@ def _streams(w, T, batch, tensor):
                      for h in range(w.n_kv_heads)])
 
 
-@pytest.mark.parametrize("name,T0,batch,ratio", [("llama_layer_4x", 61, 2, 8.0), ("tiny", 127, 1, 8.0),
-                                                 ("qwen_layer_8x", 700, 1, 12.0), ("llama_layer_4x", 500, 1, 16 / 9)])
-def test_decode_step_equals_encode_then_attention(name, T0, batch, ratio):
+@pytest.mark.parametrize("name,T0,batch,ratio,kappa", [("llama_layer_4x", 61, 2, 8.0, 0.5), ("tiny", 127, 1, 8.0, 0.5),
+                                                       ("qwen_layer_8x", 700, 1, 12.0, 0.5),
+                                                       ("llama_layer_4x", 500, 1, 16 / 9, 0.5),
+                                                       ("llama_layer_4x", 61, 1, 8.0, 0.25),
+                                                       ("qwen_layer_8x", 190, 1, 4.0, 0.7)])
+def test_decode_step_equals_encode_then_attention(name, T0, batch, ratio, kappa):
+    """kappa != 1/2: key and value records of different widths (asymmetric split)."""
     w = synth.WORKLOADS[name]
     n_steps = 5                                   # crosses a 64-token tile boundary for T0 = 61 / 127
     T = T0 + n_steps
     t_cap = (T + 63) // 64 * 64
     xk, xv = _streams(w, T, batch, 0), _streams(w, T, batch, 1)
     dk, dv = to_device(xk, w.dtype), to_device(xv, w.dtype)
-    p = O.Params(ratio=ratio)
-    ck, pk = fit_and_encode(dk[:, :T0].contiguous(), p, t_cap)
-    cv, pv = fit_and_encode(dv[:, :T0].contiguous(), p, t_cap)
+    p_k = p_v = O.Params(ratio=ratio)
+    if kappa != 0.5:
+        p_k, p_v = O.split_budget(p_k, kappa)
+    ck, pk = fit_and_encode(dk[:, :T0].contiguous(), p_k, t_cap)
+    cv, pv = fit_and_encode(dv[:, :T0].contiguous(), p_v, t_cap)
     pk2, pv2 = pk.clone(), pv.clone()
     H, Hq = w.n_kv_heads, w.n_q_heads
     for i in range(n_steps):
