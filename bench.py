@@ -68,6 +68,8 @@ def _parse():
     ap.add_argument("--workload", default="llama_model_131k_8x")
     ap.add_argument("--decode-steps", type=int, default=None, help="decode steps per bench step (default: workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kappa", type=float, default=0.5,
+                    help="key share of the combined K+V budget (asymmetric split; 0.5 = symmetric records)")
     ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
     ap.add_argument("--eager", action="store_true", help="launch decode steps from Python instead of HIP graphs")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -89,7 +91,7 @@ def algorithmic_bytes(w, Wk, Wv, n_tokens_attended):
             "step_call": att_records + att_qo + state + append}
 
 
-def cpu_baseline(w, p, budget_s=20.0):
+def cpu_baseline(w, p, budget_s=20.0, p_v=None):
     """CPU oracle on a bounded sample: one layer's first KV head (K and V streams),
     encode of the prefill + one decode-step attention; throughput in the step's
     bytes/s units."""
@@ -97,6 +99,7 @@ def cpu_baseline(w, p, budget_s=20.0):
 
     import oracle as O
     import synth
+    p_v = p if p_v is None else p_v
     T = w.n_tokens
     t_start = time.perf_counter()
     xk = synth.numpy_stream(w, 0, 0, 0, 0, n_tokens=T)
@@ -106,19 +109,19 @@ def cpu_baseline(w, p, budget_s=20.0):
     xv64 = synth.bf16_bits_to_f32(xv).astype(np.float64)
     q = synth.bf16_bits_to_f32(synth.numpy_query(w, 0, 0, 0)).astype(np.float64)[: w.n_qh]
     t0 = time.perf_counter()
-    fk, fv = O.fit(xk64, p), O.fit(xv64, p)
-    bk, bv = O.allocate_bits(fk.var, p), O.allocate_bits(fv.var, p)
+    fk, fv = O.fit(xk64, p), O.fit(xv64, p_v)
+    bk, bv = O.allocate_bits(fk.var, p), O.allocate_bits(fv.var, p_v)
     t1 = time.perf_counter()
     rk, *_ = O.encode(xk64, fk.basis, fk.mean, bk, p)
-    rv, *_ = O.encode(xv64, fv.basis, fv.mean, bv, p)
+    rv, *_ = O.encode(xv64, fv.basis, fv.mean, bv, p_v)
     t2 = time.perf_counter()
     kh = O.decode(rk, fk.basis, fk.mean, bk, p)
-    vh = O.decode(rv, fv.basis, fv.mean, bv, p)
+    vh = O.decode(rv, fv.basis, fv.mean, bv, p_v)
     O.attention_mode_a(q, kh[None], vh[None])
     t3 = time.perf_counter()
-    W = O.record_words(p)
-    enc_bytes = 2 * T * (2 * 128 + W * 4)
-    att_bytes = 2 * T * W * 4
+    Wk, Wv = O.record_words(p), O.record_words(p_v)
+    enc_bytes = T * (2 * 2 * 128 + (Wk + Wv) * 4)
+    att_bytes = T * (Wk + Wv) * 4
     secs = t3 - t1
     try:
         from threadpoolctl import threadpool_info
@@ -160,8 +163,11 @@ def main():
     T_all = T + max(n_dec, 0)
     t_cap = (T_all + 63) // 64 * 64
     Sn = n_seq * L * H                      # streams per codec, index (seq*L + layer)*H + head
-    sp = S.Params(ratio=w.ratio)
-    p = O.Params(ratio=w.ratio)
+    sp = sp_v = S.Params(ratio=w.ratio)
+    p = p_v = O.Params(ratio=w.ratio)
+    if args.kappa != 0.5:
+        sp, sp_v = S.spectra_split_budget(sp, args.kappa)
+        p, p_v = O.split_budget(p, args.kappa)
 
     # ---- synthetic inputs (resident in HBM before timing) ----
     t_gen = time.perf_counter()
@@ -181,7 +187,7 @@ def main():
     gen_s = time.perf_counter() - t_gen
 
     # ---- calibration: fit once on the prefill ----
-    ck, cv = S.Codec(sp, Sn), S.Codec(sp, Sn)
+    ck, cv = S.Codec(sp, Sn), S.Codec(sp_v, Sn)
     t_fit = time.perf_counter()
     S.spectra_fit_basis(ck, xk, n_tokens=T)
     S.spectra_fit_basis(cv, xv, n_tokens=T)
@@ -282,7 +288,9 @@ def main():
     att_gbps = att_call_bytes / (att_call_ms * 1e-3) / 1e9 if att_call_ms > 0 else 0.0
     tokens_per_call = n_seq * float(np.mean([T + s + 1 for s in range(n_dec)])) if n_dec else 0.0
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    measured = MEASURED_TRAFFIC.get(decode_step_sources_sha256())
+    # counters were taken on the default workload with symmetric records
+    measured = (MEASURED_TRAFFIC.get(decode_step_sources_sha256())
+                if (w.name, args.kappa) == ("llama_model_131k_8x", 0.5) else None)
     traffic = (measured["fetch_bytes"] + measured["write_bytes"]) if measured else None
 
     result = {
@@ -303,6 +311,7 @@ def main():
             "head_dim": d, "batch": n_seq, "prefill_tokens": T, "decode_steps": n_dec,
             "ratio_nominal": w.ratio, "ratio_actual_k": round(16 * d / (32 * Wk), 3),
             "ratio_actual_v": round(16 * d / (32 * Wv), 3), "record_words": [Wk, Wv],
+            "kappa": args.kappa,
         },
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
         "encode": {"ms": round(enc_ms, 3), "GBps": round(enc_bytes / (enc_ms * 1e-3) / 1e9, 1),
@@ -323,13 +332,13 @@ def main():
         "bits_v_first_layer": cv.bits[:H].cpu().numpy().tolist(),
     }
     if args.check:
-        result["check"] = sampled_check(w, p, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H)
+        result["check"] = sampled_check(w, p, p_v, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, p)
+        result["cpu_baseline"] = cpu_baseline(w, p, p_v=p_v)
     print(json.dumps(result))
 
 
-def sampled_check(w, p, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H):
+def sampled_check(w, p, p_v, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H):
     """Oracle comparison of the last layer's head 0 after the timed steps."""
     import numpy as np
 
@@ -340,10 +349,10 @@ def sampled_check(w, p, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H)
     n = T + n_dec
     s = l * H
     res = {}
-    for name, codec, packed, x in (("k", ck, pk, xk), ("v", cv, pv, xv)):
+    for name, par, codec, packed, x in (("k", p, ck, pk, xk), ("v", p_v, cv, pv, xv)):
         basis, mean, bits = codec_state(codec, s)
         rec = records_of(packed, s, 0, n, t_cap, codec.record_words)
-        r = check_encoded_stream(host_values(x[s, :n]), basis, mean, bits, p, rec)
+        r = check_encoded_stream(host_values(x[s, :n]), basis, mean, bits, par, rec)
         res[name] = {"code_mismatch": r.code_mismatch, "meta_mismatch": r.meta_mismatch}
     return res
 

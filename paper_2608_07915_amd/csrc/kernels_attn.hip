@@ -397,10 +397,11 @@ __device__ __forceinline__ void score_slot(const uint32_t* __restrict__ kt, int 
 }
 
 // ---------------------------------------------------------------------------
-// Split-K partial. NQ = query-head quads (n_qh <= 4 NQ); PW = prefetched record
-// words per tile (>= max(W_k, W_v); 0: no prefetch); EXACT: W_k = W_v = PW.
+// Split-K partial. NQ = query-head quads (n_qh <= 4 NQ); PK, PV = prefetched key
+// and value record words per tile (>= W_k, W_v; both 0: no prefetch); EXACT:
+// W_k = PK and W_v = PV.
 // ---------------------------------------------------------------------------
-template <int NQ, int PW, bool EXACT>
+template <int NQ, int PK, int PV, bool EXACT>
 __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   constexpr int NH = 4 * NQ;
   constexpr bool STACK = NQ <= 2;  // 2*NH <= 16: hi and lo weight rows share one MFMA
@@ -415,7 +416,8 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int nqh = a.n_qh;
   const int Wk = a.Wk, Wv = a.Wv;
   // ---- per-wave streaming over this chunk's tiles ----
-  const int wk_rows = PW > 0 ? PW : Wk, wv_rows = PW > 0 ? PW : Wv;  // staged words per token
+  static_assert((PK > 0) == (PV > 0), "prefetch both tensors or neither");
+  const int wk_rows = PK > 0 ? PK : Wk, wv_rows = PV > 0 ? PV : Wv;  // staged words per token
   const int wpw = wk_rows + wv_rows;
   uint32_t* kt = smem + wave * wpw * TROW;
   uint32_t* vt = kt + wk_rows * TROW;
@@ -446,9 +448,9 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int col = lane & 15;  // value MFMA: coefficient column / A row
   const int kq = lane >> 4;   // value MFMA: 8-token group of K
 
-  // register prefetch of one tile's record words (K and V); PW = 0: none
-  constexpr int PWR = PW > 0 ? PW : 1;
-  uint32_t pk[PWR], pv[PWR];
+  // register prefetch of one tile's record words (K and V); PK = PV = 0: none
+  constexpr int PKR = PK > 0 ? PK : 1, PVR = PV > 0 ? PV : 1;
+  uint32_t pk[PKR], pv[PVR];
   // every lane loads in-bounds words: the word index is clamped to the record (a
   // uniform offset folded into the per-word base pointer), the token to the tile;
   // tokens past n_tokens are never weighted (their value metadata is zeroed)
@@ -457,19 +459,19 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   auto load_tile = [&](int64_t tt) {
     const uint32_t ko = (uint32_t)tt * (uint32_t)(64 * Wk) + (uint32_t)lane;
     const uint32_t vo = (uint32_t)tt * (uint32_t)(64 * Wv) + (uint32_t)lane;
-    if constexpr (EXACT) {  // Wk == Wv == PW: no clamping, word offsets are immediates
+    if constexpr (EXACT) {  // Wk == PK, Wv == PV: no clamping, word offsets are immediates
       const uint32_t* kp = kps + ko;
       const uint32_t* vp = vps + vo;
 #pragma unroll
-      for (int w = 0; w < PW; ++w) {
-        pk[w] = kp[64 * w];
-        pv[w] = vp[64 * w];
+      for (int w = 0; w < (PK > PV ? PK : PV); ++w) {
+        if (w < PK) pk[w] = kp[64 * w];
+        if (w < PV) pv[w] = vp[64 * w];
       }
     } else {
 #pragma unroll
-      for (int w = 0; w < PW; ++w) {
-        pk[w] = (kps + 64 * (w < Wk ? w : Wk - 1))[ko];
-        pv[w] = (vps + 64 * (w < Wv ? w : Wv - 1))[vo];
+      for (int w = 0; w < (PK > PV ? PK : PV); ++w) {
+        if (w < PK) pk[w] = (kps + 64 * (w < Wk ? w : Wk - 1))[ko];
+        if (w < PV) pv[w] = (vps + 64 * (w < Wv ? w : Wv - 1))[vo];
       }
     }
   };
@@ -528,11 +530,11 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     const int64_t t = tt * 64 + lane;
     const bool valid = t < a.n_tokens;
     // stage this tile's words in LDS (lane = token), then prefetch the next tile
-    if constexpr (PW > 0) {
+    if constexpr (PK > 0) {
 #pragma unroll
-      for (int w = 0; w < PW; ++w) {
-        kt[w * TROW + lane] = pk[w];
-        vt[w * TROW + lane] = pv[w];
+      for (int w = 0; w < (PK > PV ? PK : PV); ++w) {
+        if (w < PK) kt[w * TROW + lane] = pk[w];
+        if (w < PV) vt[w * TROW + lane] = pv[w];
       }
       if (tt + WAVES < tile_end) load_tile(tt + WAVES);
     } else {
@@ -873,32 +875,41 @@ int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, in
   return (int32_t)nch;
 }
 
-template <int NQ, int PW, bool EXACT>
+template <int NQ, int PK, int PV, bool EXACT>
 static void launch_nq_pw(const AttnArgs& a, hipStream_t st) {
-  const int wpw = PW > 0 ? 2 * PW : a.Wk + a.Wv;
+  const int wpw = PK > 0 ? PK + PV : a.Wk + a.Wv;
   size_t tiles = (size_t)WAVES * wpw * TROW * 4 + (size_t)attn_wt_bytes(NQ);
   size_t merge = (size_t)WAVES * (NQ <= 2 ? 8 * NQ : 4 * NQ) * AROW * 4;  // per-wave value sums
   size_t lds = tiles > merge ? tiles : merge;
   if ((size_t)qprep_scratch_bytes(NQ) > lds) lds = qprep_scratch_bytes(NQ);
   if (a.app_k && (size_t)append_stage_bytes(a.app_f32 != 0) > lds) lds = append_stage_bytes(a.app_f32 != 0);
   const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
-  hipLaunchKernelGGL((attn_kernel<NQ, PW, EXACT>), grid, dim3(256), lds, st, a);
+  hipLaunchKernelGGL((attn_kernel<NQ, PK, PV, EXACT>), grid, dim3(256), lds, st, a);
 }
 
+// Prefetch shapes. Up to eight query heads per KV head, records of unequal width
+// get their own shapes: exact (4, 12) and (12, 4) (the 8x budget split a quarter
+// or three quarters to the keys), otherwise (8, 16) or (16, 8); at most 24
+// prefetch registers keep three wavefronts per SIMD.
 template <int NQ>
 static void launch_nq(const AttnArgs& a, hipStream_t st) {
-  const int w = a.Wk > a.Wv ? a.Wk : a.Wv;
-  const bool same = a.Wk == a.Wv;
-  if (w == 8 && same)
-    launch_nq_pw<NQ, 8, true>(a, st);
-  else if (w <= 8)
-    launch_nq_pw<NQ, 8, false>(a, st);
-  else if (w == 16 && same)
-    launch_nq_pw<NQ, 16, true>(a, st);
-  else if (w <= 16)
-    launch_nq_pw<NQ, 16, false>(a, st);
+  const int wk = a.Wk, wv = a.Wv;
+  if constexpr (NQ <= 2) {
+    if (wk == 4 && wv == 12) return launch_nq_pw<NQ, 4, 12, true>(a, st);
+    if (wk == 12 && wv == 4) return launch_nq_pw<NQ, 12, 4, true>(a, st);
+    if (wk <= 8 && wv > 8 && wv <= 16) return launch_nq_pw<NQ, 8, 16, false>(a, st);
+    if (wv <= 8 && wk > 8 && wk <= 16) return launch_nq_pw<NQ, 16, 8, false>(a, st);
+  }
+  if (wk == 8 && wv == 8)
+    launch_nq_pw<NQ, 8, 8, true>(a, st);
+  else if (wk <= 8 && wv <= 8)
+    launch_nq_pw<NQ, 8, 8, false>(a, st);
+  else if (wk == 16 && wv == 16)
+    launch_nq_pw<NQ, 16, 16, true>(a, st);
+  else if (wk <= 16 && wv <= 16)
+    launch_nq_pw<NQ, 16, 16, false>(a, st);
   else
-    launch_nq_pw<NQ, 0, false>(a, st);
+    launch_nq_pw<NQ, 0, 0, false>(a, st);
 }
 
 static hipError_t launch_scan_combine(const AttnArgs& a, hipStream_t st) {

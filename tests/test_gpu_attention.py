@@ -137,12 +137,13 @@ def test_attention_non_prefix_kept_groups(bits_k, bits_v):
     run_and_check(w, 700, 1, 0.0, p=O.Params(budget_bits=32 * 9), bits_k=bits_k, bits_v=bits_v)
 
 
-@pytest.mark.parametrize("kappa", [0.25, 0.75])
-def test_attention_asymmetric_budget_split(kappa):
+@pytest.mark.parametrize("kappa,n_qh", [(0.25, 4), (0.75, 4), (0.3, 4), (0.7, 4), (0.25, 8), (0.7, 7)])
+def test_attention_asymmetric_budget_split(kappa, n_qh):
     """Key and value records of different widths from the kappa split of the 8x
-    budget (Sec. 3.1, App. F): kappa = 1/4 gives 4-word keys and 12-word values."""
+    budget (Sec. 3.1, App. F): kappa = 1/4 gives 4-word keys and 12-word values,
+    0.3 gives 5 and 11 words (each prefetch shape of unequal widths)."""
     from dataclasses import replace
-    w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=2, n_q_heads=8)
+    w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=2, n_q_heads=2 * n_qh)
     pk, pv = O.split_budget(O.Params(ratio=8.0), kappa)
-    assert {O.record_words(pk), O.record_words(pv)} == {4, 12}
+    assert O.record_words(pk) + O.record_words(pv) == 16
     run_and_check(w, 1500, 1, 0.0, p=pk, p_v=pv)
