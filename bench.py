@@ -44,9 +44,9 @@ CALIB_BYTES = 256 << 20
 DECODE_STEP_SOURCES = ("kernels_attn.hip", "kplan.hpp", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "9c25c89e4410da24064f9c110cc6e904e50cafd79382d5dde23cdb2192380ddf": {
-        "fetch_bytes": 74618675, "write_bytes": 1674240,
-        "per_kernel": {"attn_kernel<1,8,true>": [70776627, 1657856], "combine_kernel": [3842048, 16384]}},
+    "8020b6d0b9e3e7a3d1a819633499676ace6e96557e9881df35c9c3dab624f152": {
+        "fetch_bytes": 74546790, "write_bytes": 1674240,
+        "per_kernel": {"attn_kernel<1,8,8,true>": [70706790, 1657856], "combine_kernel": [3840000, 16384]}},
 }
 
 
