@@ -134,6 +134,25 @@ spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype 
                                  int64_t stream_stride, int64_t token_stride, void* workspace,
                                  size_t ws_bytes, void* stream);
 
+/* Calibrate-once fit from weights (Sec. 3.1, Eqs. gweighted and gsvd; App. B). The
+ * paper whitens a head's projection, M = G^{1/2} W = U S V^T, and keeps the top right
+ * singular directions; for k = h W these are the eigenvectors of E[k^T k] = W^T G W,
+ * so the basis, coefficient means, centered variances and widths are those of a
+ * stream whose second moment is W^T G W and whose mean is hbar W (no data pass).
+ *   W     device fp32 [n_streams][d_model][d]: stream s's projection (k = h W);
+ *   G     device fp64 [n_streams / streams_per_layer][d_model][d_model]: E[h^T h] of
+ *         the input of stream s's layer, layer = s / streams_per_layer;
+ *   hbar  device fp64 [layers][d_model]: E[h]; NULL means zero mean.
+ * d_model: a multiple of 64 in [64, 16384]. The products run in fp64 on the GPU
+ * (P_s = G W_s in the workspace, then W_s^T P_s); the eigensolve as in
+ * spectra_fit_basis. Synchronises `stream`. Workspace: device,
+ * spectra_fit_weights_workspace_bytes bytes, 256-B aligned (n_streams * (d^2 + d +
+ * d_model * d) doubles). Errors as spectra_fit_basis. */
+size_t spectra_fit_weights_workspace_bytes(const spectra_codec* c, int32_t d_model);
+spectra_status spectra_fit_weights(spectra_codec* c, const float* W, int32_t d_model, const double* G,
+                                   const double* hbar, int32_t streams_per_layer, void* workspace,
+                                   size_t ws_bytes, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Encode (Sec. 3.2-3.3: every new token is projected, quantized and appended).
  * Token i < n_tokens of stream s is read from x[s*stream_stride + i*token_stride + c]

@@ -143,6 +143,31 @@ def fit(x: np.ndarray, p: Params) -> FitResult:
     assert d == p.head_dim and T > 0
     mu = x.sum(axis=0) / T
     S = (x.T @ x) / T
+    return _fit_from_moments(S, mu, p)
+
+
+def fit_from_weights(W: np.ndarray, G: np.ndarray, hbar, p: Params) -> FitResult:
+    """Calibrate-once basis from a head's projection and its layer's input statistics
+    (Sec. 3.1, Eqs. gweighted and gsvd; App. B).
+
+    The paper whitens the weight, M = G^{1/2} W = U S V^T with G = E[h^T h], and keeps
+    the top right singular directions. The keys the head produces, k = h W, have
+    E[k^T k] = W^T G W = M^T M = V S^2 V^T and E[k] = hbar W (hbar = E[h]; None for
+    zero), so the basis, coefficient mean, centered variances and widths are those
+    of ``fit`` for a stream with exactly these moments: no pass over cached data.
+    W [d_model, d], G [d_model, d_model], hbar [d_model]; all read as fp64.
+    """
+    W = np.asarray(W, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    assert W.shape[1] == p.head_dim and G.shape == (W.shape[0], W.shape[0])
+    S = W.T @ G @ W
+    mu = np.zeros(p.head_dim) if hbar is None else np.asarray(hbar, dtype=np.float64) @ W
+    return _fit_from_moments(S, mu, p)
+
+
+def _fit_from_moments(S: np.ndarray, mu: np.ndarray, p: Params) -> FitResult:
+    """Steps of ``fit`` after the moments: second moment S and mean mu, fp64."""
+    d = p.head_dim
     C = S - np.outer(mu, mu)
     M = C if p.centered else S
     M = 0.5 * (M + M.T)

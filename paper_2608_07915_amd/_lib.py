@@ -46,6 +46,8 @@ _SIGNATURES = {
     "spectra_packed_words": (_I64, [_PC, _I64]),
     "spectra_fit_workspace_bytes": (_SZ, [_PC, _I64]),
     "spectra_fit_basis": (_I32, [_PC, _P, _I32, _I64, _I64, _I64, _P, _SZ, _P]),
+    "spectra_fit_weights_workspace_bytes": (_SZ, [_PC, _I32]),
+    "spectra_fit_weights": (_I32, [_PC, _P, _I32, _P, _P, _I32, _P, _SZ, _P]),
     "spectra_encode": (_I32, [_PC, _P, _I32, _I64, _I64, _I64, _I64, _P, _I64, _P]),
     "spectra_decode": (_I32, [_PC, _P, _I64, _I64, _I64, _P, _P]),
     "spectra_attention_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I64]),

@@ -125,6 +125,27 @@ def spectra_fit_basis(codec: Codec, x, n_tokens: Optional[int] = None, workspace
                                        x.stride(1), workspace.data_ptr(), workspace.numel(), _stream(stream)))
 
 
+def spectra_fit_weights_workspace_bytes(codec: Codec, d_model: int) -> int:
+    return int(_lib.get().spectra_fit_weights_workspace_bytes(ctypes.byref(codec.struct), int(d_model)))
+
+
+def spectra_fit_weights(codec: Codec, W, G, hbar=None, streams_per_layer: int = 1, workspace=None,
+                        stream=None) -> None:
+    """Fit every stream from weights: W [n_streams, d_model, d] fp32, G [layers, d_model, d_model]
+    fp64, hbar [layers, d_model] fp64 or None (device tensors, contiguous)."""
+    import torch
+    d_model = int(W.shape[1])
+    for t, dt in ((W, torch.float32), (G, torch.float64)) + (((hbar, torch.float64),) if hbar is not None else ()):
+        if t.dtype != dt or not t.is_contiguous():
+            raise ValueError("W must be contiguous float32, G and hbar contiguous float64")
+    if workspace is None:
+        workspace = torch.empty(spectra_fit_weights_workspace_bytes(codec, d_model), dtype=torch.uint8,
+                                device=W.device)
+    check(_lib.get().spectra_fit_weights(ctypes.byref(codec.struct), W.data_ptr(), d_model, G.data_ptr(),
+                                         hbar.data_ptr() if hbar is not None else None, int(streams_per_layer),
+                                         workspace.data_ptr(), workspace.numel(), _stream(stream)))
+
+
 def spectra_encode(codec: Codec, x, t0: int, packed, t_capacity: int, n_tokens: Optional[int] = None,
                    stream=None) -> None:
     """Encode tokens x[:, i] of every stream into record slots t0 + i of ``packed``."""

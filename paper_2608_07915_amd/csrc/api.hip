@@ -82,6 +82,43 @@ size_t fit_ws_bytes(int64_t n_streams, int64_t n_tokens) {
 
 size_t round256(size_t b) { return (b + 255) / 256 * 256; }
 
+// Host half of a fit: eigenbasis, mean, variances and widths of every stream from
+// its moments (gram, column sums over n_tokens), in parallel, then copied into the
+// codec arrays. Synchronises hs.
+spectra_status finish_fit(spectra_codec* c, const std::vector<double>& mom, int64_t n_tokens, hipStream_t hs) {
+  const int64_t S = c->n_streams;
+  hipError_t e = hipSuccess;
+  std::vector<float> basis((size_t)S * kD * kD), mean((size_t)S * kD), var32((size_t)S * kD);
+  std::vector<double> var((size_t)S * kD);
+  const int nG = kD / c->p.group_size;
+  std::vector<uint8_t> bits((size_t)S * nG);
+  std::vector<spectra_status> res((size_t)S, SPECTRA_OK);
+  std::vector<std::string> msgs((size_t)S);
+  const int nthreads = (int)std::max<int64_t>(1, std::min<int64_t>(S, std::min(16u, std::max(1u, std::thread::hardware_concurrency()))));
+  std::vector<std::thread> pool;
+  for (int w = 0; w < nthreads; ++w) {
+    pool.emplace_back([&, w]() {
+      for (int64_t s = w; s < S; s += nthreads) {
+        const double* m = &mom[(size_t)(s * kMoments)];
+        res[(size_t)s] = fit_from_moments(c->p, n_tokens, m, m + kD * kD, &basis[(size_t)s * kD * kD], &mean[(size_t)s * kD],
+                                          &var[(size_t)s * kD], &bits[(size_t)s * nG]);
+        if (res[(size_t)s] != SPECTRA_OK) msgs[(size_t)s] = spectra_last_error();
+      }
+    });
+  }
+  for (auto& t : pool) t.join();
+  for (int64_t s = 0; s < S; ++s)
+    if (res[(size_t)s] != SPECTRA_OK) return fail(res[(size_t)s], "fit stream %lld: %s", (long long)s, msgs[(size_t)s].c_str());
+  for (size_t i = 0; i < var.size(); ++i) var32[i] = (float)var[i];
+  e = hipMemcpyAsync(c->basis, basis.data(), basis.size() * sizeof(float), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->mean, mean.data(), mean.size() * sizeof(float), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->var, var32.data(), var32.size() * sizeof(float), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->bits, bits.data(), bits.size(), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "fit result copy");
+  return SPECTRA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -121,36 +158,43 @@ spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype 
   e = hipStreamSynchronize(hs);
   if (e != hipSuccess) return hip_fail(e, "fit moments sync");
 
-  // Host: eigenbasis, mean, variances and allocation per stream, in parallel.
-  std::vector<float> basis((size_t)S * kD * kD), mean((size_t)S * kD), var32((size_t)S * kD);
-  std::vector<double> var((size_t)S * kD);
-  const int nG = kD / c->p.group_size;
-  std::vector<uint8_t> bits((size_t)S * nG);
-  std::vector<spectra_status> res((size_t)S, SPECTRA_OK);
-  std::vector<std::string> msgs((size_t)S);
-  const int nthreads = (int)std::max<int64_t>(1, std::min<int64_t>(S, std::min(16u, std::max(1u, std::thread::hardware_concurrency()))));
-  std::vector<std::thread> pool;
-  for (int w = 0; w < nthreads; ++w) {
-    pool.emplace_back([&, w]() {
-      for (int64_t s = w; s < S; s += nthreads) {
-        const double* m = &mom[(size_t)(s * kMoments)];
-        res[(size_t)s] = fit_from_moments(c->p, n_tokens, m, m + kD * kD, &basis[(size_t)s * kD * kD], &mean[(size_t)s * kD],
-                                          &var[(size_t)s * kD], &bits[(size_t)s * nG]);
-        if (res[(size_t)s] != SPECTRA_OK) msgs[(size_t)s] = spectra_last_error();
-      }
-    });
-  }
-  for (auto& t : pool) t.join();
-  for (int64_t s = 0; s < S; ++s)
-    if (res[(size_t)s] != SPECTRA_OK) return fail(res[(size_t)s], "fit stream %lld: %s", (long long)s, msgs[(size_t)s].c_str());
-  for (size_t i = 0; i < var.size(); ++i) var32[i] = (float)var[i];
-  e = hipMemcpyAsync(c->basis, basis.data(), basis.size() * sizeof(float), hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess) e = hipMemcpyAsync(c->mean, mean.data(), mean.size() * sizeof(float), hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess) e = hipMemcpyAsync(c->var, var32.data(), var32.size() * sizeof(float), hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess) e = hipMemcpyAsync(c->bits, bits.data(), bits.size(), hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess) e = hipStreamSynchronize(hs);
-  if (e != hipSuccess) return hip_fail(e, "fit result copy");
-  return SPECTRA_OK;
+  return finish_fit(c, mom, n_tokens, hs);
+}
+
+size_t spectra_fit_weights_workspace_bytes(const spectra_codec* c, int32_t d_model) {
+  if (!c || c->n_streams <= 0 || d_model <= 0) return 0;
+  return round256((size_t)c->n_streams * (size_t)kMoments * sizeof(double)) +
+         (size_t)c->n_streams * (size_t)d_model * kD * sizeof(double);
+}
+
+spectra_status spectra_fit_weights(spectra_codec* c, const float* W, int32_t d_model, const double* G,
+                                   const double* hbar, int32_t streams_per_layer, void* workspace, size_t ws_bytes,
+                                   void* stream) {
+  spectra_status st = check_codec(c, "fit_weights");
+  if (st != SPECTRA_OK) return st;
+  if (!W || !G || !aligned(W, 4) || !aligned(G, 8) || (hbar && !aligned(hbar, 8)))
+    return fail(SPECTRA_EINVAL, "fit_weights: W and G must be non-null and aligned (4 / 8 bytes)");
+  if (d_model < 64 || d_model > 16384 || d_model % 64 != 0)
+    return fail(SPECTRA_EINVAL, "fit_weights: d_model=%d must be a multiple of 64 in [64, 16384]", d_model);
+  const int64_t S = c->n_streams;
+  if (streams_per_layer < 1 || S % streams_per_layer != 0)
+    return fail(SPECTRA_EINVAL, "fit_weights: streams_per_layer=%d must divide n_streams=%lld", streams_per_layer,
+                (long long)S);
+  if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "fit_weights workspace must be 256-byte aligned");
+  const size_t need = spectra_fit_weights_workspace_bytes(c, d_model);
+  if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "fit_weights workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t hs = (hipStream_t)stream;
+  double* moments = reinterpret_cast<double*>(workspace);
+  double* scratch = reinterpret_cast<double*>(static_cast<char*>(workspace) +
+                                              round256((size_t)S * (size_t)kMoments * sizeof(double)));
+  hipError_t e = launch_weights_moments(W, G, hbar, d_model, (int32_t)S, streams_per_layer, scratch, moments, kMoments, hs);
+  if (e != hipSuccess) return hip_fail(e, "fit_weights launch");
+  std::vector<double> mom((size_t)(S * kMoments));
+  e = hipMemcpyAsync(mom.data(), moments, mom.size() * sizeof(double), hipMemcpyDeviceToHost, hs);
+  if (e != hipSuccess) return hip_fail(e, "fit_weights moments copy");
+  e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "fit_weights moments sync");
+  return finish_fit(c, mom, 1, hs);  // moments are already expectations
 }
 
 spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dtype dt, int64_t stream_stride,

@@ -81,6 +81,19 @@ struct AttnArgs {
   float* out;            // [batch][n_q_heads][128]
 };
 
+// Batched fp64 product C_b = A_{b / a_div} B_b, element strides; M, N multiples
+// of 64, K of 16 (calibration from weights).
+struct WgemmArgs {
+  const void* A;
+  const void* B;
+  double* C;
+  int32_t M, N, K;
+  int64_t a_rs, a_cs, a_bs;
+  int32_t a_div;
+  int64_t b_rs, b_cs, b_bs;
+  int64_t c_rs, c_bs;
+};
+
 }  // namespace spectra_dev
 
 namespace spectra {
@@ -94,4 +107,10 @@ hipError_t launch_attention(const spectra_dev::AttnArgs& a, hipStream_t st);
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
+// moments[s] = [W_s^T G W_s, hbar W_s] for W [n_streams][d_model][128] fp32 and per-layer
+// G [layers][d_model][d_model], hbar [layers][d_model] fp64 (layer = s / streams_per_layer);
+// scratch: n_streams * d_model * 128 doubles.
+hipError_t launch_weights_moments(const float* W, const double* G, const double* hbar, int32_t d_model,
+                                  int32_t n_streams, int32_t streams_per_layer, double* scratch, double* moments,
+                                  int64_t mom_stride, hipStream_t st);
 }  // namespace spectra

@@ -165,6 +165,16 @@ def test_argument_errors_return_before_any_launch(lib):
     assert b"16-byte" in lib.spectra_last_error()
     assert lib.spectra_decode_step(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 8, 256, 256, 1, 256, 1, 1, 4, 4,
                                    0.0, 256, 256, 16, None) == -4
+    # fit from weights: d_model, layer grouping, alignment, workspace (c holds 4 streams)
+    need = lib.spectra_fit_weights_workspace_bytes(ctypes.byref(c), 256)
+    assert need == 4 * (128 * 128 + 128) * 8 + 4 * 256 * 128 * 8
+    assert lib.spectra_fit_weights(ctypes.byref(c), 256, 200, 256, None, 1, 256, need, None) == -1
+    assert b"multiple of 64" in lib.spectra_last_error()
+    assert lib.spectra_fit_weights(ctypes.byref(c), 256, 256, 256, None, 3, 256, need, None) == -1
+    assert b"streams_per_layer" in lib.spectra_last_error()
+    assert lib.spectra_fit_weights(ctypes.byref(c), None, 256, 256, None, 1, 256, need, None) == -1
+    assert lib.spectra_fit_weights(ctypes.byref(c), 256, 256, 260, None, 1, 256, need, None) == -1
+    assert lib.spectra_fit_weights(ctypes.byref(c), 256, 256, 256, None, 2, 256, need - 8, None) == -4
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
