@@ -68,6 +68,9 @@ def _parse():
     ap.add_argument("--workload", default="llama_model_131k_8x")
     ap.add_argument("--decode-steps", type=int, default=None, help="decode steps per bench step (default: workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fit-weights", action="store_true",
+                    help="time the calibrate-once fit from weights (Llama-3.1-8B keys: 32 layers x 8 heads, "
+                         "d_model 4096) instead of the hot path; prints its own JSON line")
     ap.add_argument("--kappa", type=float, default=0.5,
                     help="key share of the combined K+V budget (asymmetric split; 0.5 = symmetric records)")
     ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
@@ -140,12 +143,52 @@ def cpu_baseline(w, p, budget_s=20.0, p_v=None):
     }
 
 
+def fit_weights_bench(args):
+    """Calibrate-once fit from weights at the Llama-3.1-8B key geometry: per layer a
+    synthetic SPD input second moment G (4096 x 4096, fp64) and mean, per KV head a
+    random fp32 projection W (4096 x 128). Times spectra_fit_weights (fp64 products
+    on the GPU, eigensolve of 256 streams on the host)."""
+    import torch
+
+    import paper_2608_07915_amd as S
+    dev = torch.device("cuda:0")
+    L, H, dm = 32, 8, 4096
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    lam = torch.arange(1, dm + 1, dtype=torch.float64, device=dev) ** -1.2
+    lam *= dm / lam.sum()
+    G = torch.empty(L, dm, dm, dtype=torch.float64, device=dev)
+    for l in range(L):
+        a = torch.randn(dm, dm, dtype=torch.float64, device=dev, generator=g) * lam.sqrt()[None, :]
+        G[l] = a @ a.T / dm
+    hbar = 0.5 * torch.randn(L, dm, dtype=torch.float64, device=dev, generator=g)
+    W = (torch.randn(L * H, dm, 128, device=dev, generator=g) / dm ** 0.5).contiguous()
+    codec = S.Codec(S.Params(ratio=8.0), L * H)
+    ws = torch.empty(S.spectra_fit_weights_workspace_bytes(codec, dm), dtype=torch.uint8, device=dev)
+    times = []
+    for _ in range(args.warmup + args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        S.spectra_fit_weights(codec, W, G, hbar, streams_per_layer=H, workspace=ws)
+        times.append(time.perf_counter() - t0)
+    ms = 1e3 * min(times[args.warmup:])
+    flops = L * H * (2.0 * dm * dm * 128 + 2.0 * dm * 128 * 128)
+    print(json.dumps({"metric": "calibrate-once fit from weights, wall ms (GPU fp64 products + host eigensolve)",
+                      "value": round(ms, 2), "unit": "ms", "higher_is_better": False, "steps": args.steps,
+                      "warmup": args.warmup, "data": "synthetic",
+                      "config": {"workload": "llama3.1-8b keys", "n_layers": L, "n_kv_heads": H, "d_model": dm},
+                      "product_gflop": round(flops / 1e9, 1),
+                      "bits_first_layer": codec.bits[:H].cpu().numpy().tolist()}))
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.fit_weights:
+        return fit_weights_bench(args)
     import numpy as np
     import torch
 
