@@ -147,3 +147,23 @@ def test_attention_asymmetric_budget_split(kappa, n_qh):
     pk, pv = O.split_budget(O.Params(ratio=8.0), kappa)
     assert O.record_words(pk) + O.record_words(pv) == 16
     run_and_check(w, 1500, 1, 0.0, p=pk, p_v=pv)
+
+
+def test_attention_zero_query_is_value_mean():
+    """q = 0: every score is 0, the softmax is uniform and the output is the mean of
+    the reconstructed values (App. E with a constant score)."""
+    w = synth.WORKLOADS["llama_layer_4x"]
+    T = 777
+    xk, xv = _workload_streams(w, T, 1)
+    p = O.Params(ratio=8.0)
+    t_cap = (T + 63) // 64 * 64
+    ck, pk = _fit_encode_with_bits(to_device(xk, w.dtype), p, t_cap, None)
+    cv, pv = _fit_encode_with_bits(to_device(xv, w.dtype), p, t_cap, None)
+    q = torch.zeros(1, w.n_q_heads, 128, dtype=torch.bfloat16, device="cuda")
+    out = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, T, q, w.n_kv_heads).cpu().numpy()[0]
+    for h in range(w.n_kv_heads):
+        basis, mean, bits = codec_state(cv, h)
+        vh = O.decode(records_of(pv, h, 0, T, t_cap, O.record_words(p)), basis, mean, bits, p)
+        want = vh.mean(axis=0)
+        for hq in range(h * w.n_qh, (h + 1) * w.n_qh):
+            assert rel_l2(out[hq], want) <= 2e-5, (h, hq)

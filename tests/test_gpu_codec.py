@@ -227,3 +227,45 @@ def test_fp32_and_bf16_inputs_agree_on_bf16_values():
     codec, pb = fit_and_encode(xb, p, 320)
     _, pf = fit_and_encode(xf, p, 320, fit=False, codec=codec)
     assert torch.equal(pb, pf)
+
+
+def test_degenerate_groups_identity_basis():
+    """Metadata and codes at the format's edges (Sec. 3.2 per-token min/max with fp16
+    scale and zero-point): constant groups (s = 0, all codes 0), values beyond the
+    fp16 range (z and s saturate at 65504), values in the fp16 subnormal range, and
+    all-zero groups. The identity basis makes the coefficients the input itself."""
+    T, t_cap = 300, 320
+    bits = [4, 3, 8, 2]
+    p = O.Params(budget_bits=32 * (4 + 4 + 3 + 8 + 2))   # metadata + payload words: W = 21
+    rng = np.random.default_rng(5)
+    x = np.zeros((T, 128), dtype=np.float32)
+    x[:, 0:32] = rng.standard_normal((T, 32))
+    const = np.arange(T) % 3 == 0
+    # one fp16-representable value per token: z = min exactly, so s = 0 and all codes 0
+    x[const, 0:32] = rng.standard_normal((int(const.sum()), 1)).astype(np.float16).astype(np.float32)
+    x[:, 32:64] = rng.uniform(-2e5, 2e5, (T, 32))                      # beyond fp16: saturating z and s
+    x[:, 64:96] = 1e-6 * rng.standard_normal((T, 32))                  # fp16 subnormal metadata
+    # x[:, 96:128] stays zero
+    codec = S.Codec(sparams(p), 1)
+    codec.basis.copy_(torch.eye(128, dtype=torch.float32)[None])
+    codec.mean.zero_()
+    codec.var.fill_(1.0)
+    codec.bits.copy_(torch.tensor([bits], dtype=torch.uint8))
+    packed = codec.empty_packed(t_cap)
+    xd = torch.from_numpy(x[None]).cuda()
+    S.spectra_encode(codec, xd, 0, packed, t_cap)
+    torch.cuda.synchronize()
+    basis, mean, _ = codec_state(codec, 0)
+    rec = records_of(packed, 0, 0, T, t_cap, O.record_words(p))
+    check_encoded_stream(x.astype(np.float64), basis, mean, bits, p, rec)
+    codes, meta = O.unpack(rec, bits, p)
+    assert np.all(codes[const, 0:32] == 0) and np.all(meta[const, 0] & 0xFFFF == 0)    # s = 0 on constant groups
+    assert np.all(codes[:, 96:128] == 0) and np.all(meta[:, 3] == 0)                    # zero groups
+    assert np.any((meta[:, 1] >> 16) == 0xFBFF)                                          # z saturated at -65504
+    dec = S.spectra_decode(codec, packed, t_cap, 0, T).cpu().numpy()[0]
+    ref = O.decode(rec, basis, mean, bits, p)
+    assert np.all(np.isfinite(dec))
+    for g in range(4):
+        sl = slice(32 * g, 32 * g + 32)
+        scale = np.abs(ref[:, sl]).max()
+        assert np.abs(dec[:, sl] - ref[:, sl]).max() <= 1e-6 * scale + 1e-30, g
