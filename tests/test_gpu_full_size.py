@@ -11,7 +11,8 @@ import pytest
 import oracle as O
 import paper_2608_07915_amd as S
 import synth
-from gpu_parity import check_encoded_stream, codec_state, host_values, records_of, rel_l2, sparams
+from gpu_parity import (check_encoded_stream, codec_state, host_values, records_of, rel_l2, sparams, to_device,
+                         values_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -65,3 +66,63 @@ def test_full_size_layer_two_decode_steps_sampled():
         for i, h in enumerate(heads):
             assert rel_l2(out[0, h], ref_same[i]) <= 2e-5, (kv, h)
             assert rel_l2(out[0, h], ref_own[i]) <= 2e-3, (kv, h)
+
+
+def _gather_records(packed, t, t_cap, W):
+    """Logical records [len(t), W] of stream 0 gathered on the device."""
+    idx = np.stack([O.physical_index(0, t, k, t_cap, W) for k in range(W)], axis=1)
+    got = packed[torch.from_numpy(idx.reshape(-1)).to(packed.device)].cpu().numpy().view(np.uint32)
+    return got.reshape(len(t), W)
+
+
+def test_largest_capacity_offsets():
+    """Record offsets at the largest capacity the attention accepts: t_capacity x W just
+    below 2^31 words per stream (W = 8, 2^28 - 64 slots, 8.6 GB per packed stream).
+    Tokens are encoded at both ends of the range; the slots between hold zero records,
+    which decode to the stream mean (z = s = 0). Attention over every slot is checked
+    by a property that holds at any size: the n0 identical zero-record tokens enter
+    the softmax as one term of multiplicity n0 (Mode A, App. E)."""
+    w = synth.WORKLOADS["llama_layer_4x"]
+    dev = torch.device("cuda:0")
+    p = O.Params(ratio=8.0)
+    W = O.record_words(p)
+    t_cap = (1 << 28) - 64
+    assert t_cap * W < (1 << 31)
+    n_end = 1000
+    xk = synth.numpy_stream(w, 0, 0, 0, 0, n_tokens=2 * n_end)[None]
+    xv = synth.numpy_stream(w, 0, 0, 0, 1, n_tokens=2 * n_end)[None]
+    ck, cv = S.Codec(sparams(p), 1), S.Codec(sparams(p), 1)
+    dk, dv = to_device(xk, w.dtype), to_device(xv, w.dtype)
+    S.spectra_fit_basis(ck, dk)
+    S.spectra_fit_basis(cv, dv)
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    for codec, packed, x in ((ck, pk, dk), (cv, pv, dv)):
+        S.spectra_encode(codec, x[:, :n_end].contiguous(), 0, packed, t_cap)
+        S.spectra_encode(codec, x[:, n_end:].contiguous(), t_cap - n_end, packed, t_cap)
+    q = synth.device_queries(w, 0, 0, dev)[:, :w.n_qh].contiguous()    # the 4 query heads of KV head 0
+    print("largest capacity: t_cap", t_cap, flush=True)
+    out = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, t_cap, q, 1).cpu().numpy()[0]
+    torch.cuda.synchronize()
+    dec = []
+    for codec, packed, x in ((ck, pk, xk), (cv, pv, xv)):
+        basis, mean, bits = codec_state(codec, 0)
+        xs = values_f64(x[0], w.dtype)
+        ends = np.concatenate([np.arange(n_end), np.arange(t_cap - n_end, t_cap)])
+        rec = _gather_records(packed, ends, t_cap, W)          # device gather: the caches are 8.6 GB
+        check_encoded_stream(xs, basis, mean, bits, p, rec)
+        zero = O.decode(np.zeros((1, W), dtype=np.uint32), basis, mean, bits, p)[0]
+        assert not _gather_records(packed, np.arange(t_cap // 2, t_cap // 2 + 64), t_cap, W).any()
+        dec.append((O.decode(rec, basis, mean, bits, p), zero))
+    (kh, k0), (vh, v0) = dec
+    n0 = t_cap - 2 * n_end
+    q64 = host_values(q)[0]
+    scale = 1.0 / np.sqrt(128.0)
+    for h in range(w.n_qh):
+        s_end = scale * (kh @ q64[h])
+        s_0 = scale * float(k0 @ q64[h])
+        m = max(s_end.max(), s_0)
+        e_end = np.exp(s_end - m)
+        e_0 = n0 * np.exp(s_0 - m)
+        want = (e_end @ vh + e_0 * v0) / (e_end.sum() + e_0)
+        # fp32 running sums over ~1400 tiles per lane: rounding up to ~1400 * 2^-24 relative
+        assert rel_l2(out[h], want) <= 2e-4, h
