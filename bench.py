@@ -319,6 +319,21 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    # ---- Mode A reconstruction (a9), outside the step: one layer's keys to fp32 ----
+    n_rec = T + max(n_dec, 0)
+    dec_out = torch.empty((H, n_rec, d), dtype=torch.float32, device=dev)
+    dec_ev = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        S.spectra_decode(layer_ck[0], layer_pk[0], t_cap, 0, n_rec, out=dec_out)
+        e1.record()
+        dec_ev.append((e0, e1))
+    torch.cuda.synchronize()
+    dec_ms = min(e0.elapsed_time(e1) for e0, e1 in dec_ev[1:])
+    dec_bytes = H * n_rec * (Wk * 4 + d * 4) + H * (d * d * 4 + d * 4)
+    del dec_out
+
     # ---- derived throughput ----
     ab = lambda n: algorithmic_bytes(w, Wk, Wv, n)  # noqa: E731
     enc_bytes = Sn * T * 2 * d * (2 if w.dtype == "bf16" else 4) + Sn * T * (Wk + Wv) * 4 + Sn * 2 * (d * d * 4 + d * 4)
@@ -368,6 +383,9 @@ def main():
                      "kernel": "decode_step (split-K scan with in-kernel query prep and append, then combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
         "traffic_detail": measured,
+        "mode_a_decode": {"ms_per_layer": round(dec_ms, 4), "GBps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
+                          "frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                          "what": "spectra_decode of one layer's keys (8 streams) to fp32, outside the step"},
         "decode_launch": "eager" if args.eager else "hip_graph",
         "fit_ms": round(fit_s * 1e3, 1),
         "input_generation_s": round(gen_s, 1),

@@ -396,7 +396,9 @@ hipError_t launch_encode(const EncodeArgs& a, bool f32_input, hipStream_t st) {
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
   const int64_t first_tile = a.t0 >> 6, last_tile = (a.t0 + a.n - 1) >> 6;
   const int64_t n_st = (last_tile - first_tile + 2) / 2;
-  int64_t per_stream = (2048 + a.n_streams - 1) / a.n_streams;
+  // one round of workgroups (two per CU): the basis operands are set up once per
+  // workgroup, and each workgroup streams many super-tiles
+  int64_t per_stream = (512 + a.n_streams - 1) / a.n_streams;
   if (per_stream > n_st) per_stream = n_st;
   if (per_stream < 1) per_stream = 1;
   hipLaunchKernelGGL(decode_kernel, dim3((unsigned)per_stream, (unsigned)a.n_streams), dim3(256), 0, st, a);
