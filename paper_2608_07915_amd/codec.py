@@ -47,6 +47,47 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
+def _need(ok: bool, msg: str) -> None:
+    """Shape and size checks the C ABI cannot make (it sees pointers only): a
+    mismatched tensor raises here instead of reaching a kernel."""
+    if not ok:
+        raise ValueError(msg)
+
+
+def _device_rows(codec: "Codec", x, name: str, n: int) -> None:
+    """x [n_streams, >= n, head_dim] on the device, unit stride along head_dim."""
+    _need(x.is_cuda, f"{name} must be a device tensor")
+    d = codec.params.head_dim
+    _need(x.dim() == 3 and x.shape[0] == codec.n_streams and x.shape[2] == d,
+          f"{name} must be [n_streams={codec.n_streams}, T, {d}], got {tuple(x.shape)}")
+    _need(x.stride(2) == 1, f"{name} needs unit stride along head_dim")
+    _need(0 <= n <= x.shape[1], f"n_tokens={n} exceeds {name}.shape[1]={x.shape[1]}")
+
+
+def _packed_words(codec: "Codec", packed, t_capacity: int, name: str) -> None:
+    import torch
+    _need(packed.is_cuda and packed.dtype == torch.int32 and packed.is_contiguous(),
+          f"{name} must be a contiguous int32 device tensor")
+    need = codec.packed_words(t_capacity)
+    _need(packed.numel() >= need, f"{name} holds {packed.numel()} words, the codec needs {need}")
+
+
+def _attention_shapes(ck: "Codec", cv: "Codec", packed_k, packed_v, t_capacity: int, q, n_kv_heads: int, out):
+    import torch
+    _need(q.is_cuda and q.dim() == 3 and q.is_contiguous(), "q must be a contiguous device tensor [batch, n_q_heads, d]")
+    batch, n_q_heads, d = q.shape
+    _need(d == ck.params.head_dim == cv.params.head_dim, f"q has head_dim {d}")
+    _need(n_kv_heads > 0 and n_q_heads % n_kv_heads == 0, f"n_q_heads={n_q_heads} is not a multiple of n_kv_heads={n_kv_heads}")
+    _need(ck.n_streams == cv.n_streams == batch * n_kv_heads,
+          f"codecs hold {ck.n_streams} / {cv.n_streams} streams, batch x n_kv_heads = {batch * n_kv_heads}")
+    _packed_words(ck, packed_k, t_capacity, "packed_k")
+    _packed_words(cv, packed_v, t_capacity, "packed_v")
+    if out is not None:
+        _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and tuple(out.shape) == (batch, n_q_heads, d),
+              f"out must be a contiguous float32 device tensor {(batch, n_q_heads, d)}")
+    return batch, n_q_heads, d
+
+
 def _stream(stream=None):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream()
@@ -118,6 +159,7 @@ def spectra_fit_basis(codec: Codec, x, n_tokens: Optional[int] = None, workspace
     """Fit every stream of ``codec`` on x [n_streams, T, d] (device; strides from the tensor)."""
     import torch
     n = x.shape[1] if n_tokens is None else int(n_tokens)
+    _device_rows(codec, x, "x", n)
     need = spectra_fit_workspace_bytes(codec, n)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
@@ -136,8 +178,15 @@ def spectra_fit_weights(codec: Codec, W, G, hbar=None, streams_per_layer: int = 
     import torch
     d_model = int(W.shape[1])
     for t, dt in ((W, torch.float32), (G, torch.float64)) + (((hbar, torch.float64),) if hbar is not None else ()):
-        if t.dtype != dt or not t.is_contiguous():
-            raise ValueError("W must be contiguous float32, G and hbar contiguous float64")
+        if t.dtype != dt or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("W must be contiguous float32, G and hbar contiguous float64, all on the device")
+    spl = int(streams_per_layer)
+    _need(spl > 0 and codec.n_streams % spl == 0, f"streams_per_layer={spl} must divide n_streams={codec.n_streams}")
+    layers = codec.n_streams // spl
+    _need(tuple(W.shape) == (codec.n_streams, d_model, codec.params.head_dim),
+          f"W must be [{codec.n_streams}, d_model, {codec.params.head_dim}], got {tuple(W.shape)}")
+    _need(tuple(G.shape) == (layers, d_model, d_model), f"G must be [{layers}, {d_model}, {d_model}], got {tuple(G.shape)}")
+    _need(hbar is None or tuple(hbar.shape) == (layers, d_model), f"hbar must be [{layers}, {d_model}]")
     if workspace is None:
         workspace = torch.empty(spectra_fit_weights_workspace_bytes(codec, d_model), dtype=torch.uint8,
                                 device=W.device)
@@ -150,7 +199,8 @@ def spectra_encode(codec: Codec, x, t0: int, packed, t_capacity: int, n_tokens: 
                    stream=None) -> None:
     """Encode tokens x[:, i] of every stream into record slots t0 + i of ``packed``."""
     n = x.shape[1] if n_tokens is None else int(n_tokens)
-    assert x.stride(2) == 1
+    _device_rows(codec, x, "x", n)
+    _packed_words(codec, packed, t_capacity, "packed")
     check(_lib.get().spectra_encode(ctypes.byref(codec.struct), x.data_ptr(), _dtype_code(x), x.stride(0),
                                     x.stride(1), int(t0), n, packed.data_ptr(), int(t_capacity), _stream(stream)))
 
@@ -158,9 +208,12 @@ def spectra_encode(codec: Codec, x, t0: int, packed, t_capacity: int, n_tokens: 
 def spectra_decode(codec: Codec, packed, t_capacity: int, t0: int, n_tokens: int, out=None, stream=None):
     """Reconstruct record slots [t0, t0 + n_tokens) of every stream -> float32 [n_streams, n_tokens, d]."""
     import torch
+    _packed_words(codec, packed, t_capacity, "packed")
+    shape = (codec.n_streams, int(n_tokens), codec.params.head_dim)
     if out is None:
-        out = torch.empty((codec.n_streams, n_tokens, codec.params.head_dim), dtype=torch.float32,
-                          device=packed.device)
+        out = torch.empty(shape, dtype=torch.float32, device=packed.device)
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and tuple(out.shape) == shape,
+          f"out must be a contiguous float32 device tensor {shape}")
     check(_lib.get().spectra_decode(ctypes.byref(codec.struct), packed.data_ptr(), int(t_capacity), int(t0),
                                     int(n_tokens), out.data_ptr(), _stream(stream)))
     return out
@@ -174,8 +227,7 @@ def spectra_decode_attention(ck: Codec, cv: Codec, packed_k, packed_v, t_capacit
                              n_kv_heads: int, softmax_scale: float = 0.0, out=None, workspace=None, stream=None):
     """One decode step over the packed caches: q [batch, n_q_heads, d] -> float32 [batch, n_q_heads, d]."""
     import torch
-    batch, n_q_heads, d = q.shape
-    assert q.is_contiguous()
+    batch, n_q_heads, d = _attention_shapes(ck, cv, packed_k, packed_v, t_capacity, q, n_kv_heads, out)
     if out is None:
         out = torch.empty((batch, n_q_heads, d), dtype=torch.float32, device=q.device)
     if workspace is None:
@@ -194,9 +246,11 @@ def spectra_decode_step(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: in
     """Append k_new, v_new [batch, n_kv_heads, d] at record slot t, then attend over slots [0, t]:
     q [batch, n_q_heads, d] -> float32 [batch, n_q_heads, d]."""
     import torch
-    batch, n_q_heads, d = q.shape
-    assert q.is_contiguous() and k_new.is_contiguous() and v_new.is_contiguous()
-    assert k_new.dtype == v_new.dtype and tuple(k_new.shape) == tuple(v_new.shape) == (batch, n_kv_heads, d)
+    batch, n_q_heads, d = _attention_shapes(ck, cv, packed_k, packed_v, t_capacity, q, n_kv_heads, out)
+    _need(k_new.is_cuda and v_new.is_cuda and k_new.is_contiguous() and v_new.is_contiguous(),
+          "k_new and v_new must be contiguous device tensors")
+    _need(k_new.dtype == v_new.dtype and tuple(k_new.shape) == tuple(v_new.shape) == (batch, n_kv_heads, d),
+          f"k_new and v_new must be [{batch}, {n_kv_heads}, {d}] of one dtype")
     if out is None:
         out = torch.empty((batch, n_q_heads, d), dtype=torch.float32, device=q.device)
     if workspace is None:
@@ -211,12 +265,20 @@ def spectra_decode_step(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: in
 
 
 def spectra_pack_codes(codec: Codec, codes, meta, packed, t_capacity: int, stream=None) -> None:
+    import torch
+    n = codes.shape[1]
+    _need(codes.is_cuda and codes.dtype == torch.uint8 and codes.is_contiguous()
+          and tuple(codes.shape) == (codec.n_streams, n, codec.params.head_dim), "codes must be contiguous uint8 [S, n, d]")
+    _need(meta.is_cuda and meta.dtype == torch.int32 and meta.is_contiguous()
+          and tuple(meta.shape) == (codec.n_streams, n, codec.params.n_groups), "meta must be contiguous int32 [S, n, d/g]")
+    _packed_words(codec, packed, t_capacity, "packed")
     check(_lib.get().spectra_pack_codes(ctypes.byref(codec.struct), codes.data_ptr(), meta.data_ptr(),
                                         codes.shape[1], packed.data_ptr(), int(t_capacity), _stream(stream)))
 
 
 def spectra_unpack_codes(codec: Codec, packed, t_capacity: int, n_tokens: int, stream=None):
     import torch
+    _packed_words(codec, packed, t_capacity, "packed")
     dev = packed.device
     codes = torch.empty((codec.n_streams, n_tokens, codec.params.head_dim), dtype=torch.uint8, device=dev)
     meta = torch.empty((codec.n_streams, n_tokens, codec.params.n_groups), dtype=torch.int32, device=dev)
