@@ -486,6 +486,37 @@ def attention_mode_a(q: np.ndarray, k_hat: np.ndarray, v_hat: np.ndarray, scale:
     return out
 
 
+def rope(x: np.ndarray, pos, inv_freq) -> np.ndarray:
+    """Rotary position embedding of vectors x [..., d] at positions pos [...] (broadcast).
+
+    Dimension i < d/2 is paired with i + d/2 (the pairing of Llama and Qwen) and the
+    pair is rotated by the angle pos * inv_freq[i], computed exactly in fp64 from the
+    given frequencies: x'_i = x_i cos - x_{i+d/2} sin, x'_{i+d/2} = x_{i+d/2} cos + x_i sin.
+    """
+    x = np.asarray(x, np.float64)
+    d = x.shape[-1]
+    h = d // 2
+    w = np.asarray(inv_freq, np.float64)
+    ang = np.asarray(pos, np.float64)[..., None] * w
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :h], x[..., h:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def attention_mode_a_rope(q: np.ndarray, k_hat: np.ndarray, v_hat: np.ndarray, inv_freq, q_pos: int,
+                          scale: float = 0.0) -> np.ndarray:
+    """Mode A with RoPE (Sec. 3.3): the cache holds latents of pre-RoPE keys, so each key
+    is reconstructed and then rotated at its own position, which is what makes Mode A
+    exact for rotary models. Key t sits at position t; the query at q_pos. Values are
+    not rotated. Otherwise as ``attention_mode_a``.
+    """
+    q = np.asarray(q, np.float64)
+    T = np.asarray(k_hat).shape[1]
+    k_rot = rope(k_hat, np.arange(T)[None, :], inv_freq)
+    q_rot = rope(q, q_pos, inv_freq)
+    return attention_mode_a(q_rot, k_rot, v_hat, scale)
+
+
 def attention_mode_b(q, ck_hat, cv_hat, basis_k, mean_k, basis_v, mean_v, scale: float = 0.0):
     """Latent-space attention (App. E): q' = q V_K once, scores q' (c_K + m_K), values in
     coefficient space, one inverse rotation per output. Equal to Mode A by linearity.
