@@ -41,7 +41,8 @@ CALIB_BYTES = 256 << 20
 # copy (FETCH_SIZE reads 131089 KiB for 256 MiB read: x2.0; WRITE_SIZE reads
 # 262148 KiB for 256 MiB written: x1.0). Valid only for the kernel sources they
 # were taken on (sha256 over DECODE_STEP_SOURCES); otherwise `traffic` is null.
-DECODE_STEP_SOURCES = ("kernels_attn.hip", "kplan.hpp", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
+DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "encode_dev.hpp", "device_common.hpp",
+                       "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
     "8020b6d0b9e3e7a3d1a819633499676ace6e96557e9881df35c9c3dab624f152": {

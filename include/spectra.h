@@ -199,6 +199,29 @@ spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_c
                                         void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Decode-step attention for rotary models (Sec. 3.3, Mode A): the cached latents are
+ * of pre-RoPE keys, so each key is reconstructed, k_hat_t = (c_hat_t + m_K) V_K^T, and
+ * rotated at its own position t (its record slot) before the dot product with the
+ * query rotated at q_position:
+ *   out[b][h] = sum_t softmax_t(scale * R(q_position) q_h . R(t) k_hat_t) v_hat_t,
+ * where R(p) turns each dimension pair (i, i + d/2), i < d/2, by the angle
+ * p * inv_freq[i] (x_i cos - x_{i+d/2} sin, x_{i+d/2} cos + x_i sin). Values are not
+ * rotated; their sums run over the kept value coefficients as in
+ * spectra_decode_attention. inv_freq: device fp32 [d/2], any frequencies (base^(-2i/d)
+ * or a scaled set). Angles are reduced in fp64 before fp32 cos/sin. Other arguments,
+ * the workspace (spectra_attention_workspace_bytes) and the errors as
+ * spectra_decode_attention; SPECTRA_EUNSUPPORTED for more than 4 query heads per KV
+ * head or records wider than 16 words. Asynchronous.
+ * ------------------------------------------------------------------------- */
+spectra_status spectra_decode_attention_rope(const spectra_codec* ck, const spectra_codec* cv,
+                                             const uint32_t* packed_k, const uint32_t* packed_v,
+                                             int64_t t_capacity, int64_t n_tokens, const void* q,
+                                             spectra_dtype q_dt, int32_t batch, int32_t n_q_heads,
+                                             int32_t n_kv_heads, float softmax_scale, const float* inv_freq,
+                                             int64_t q_position, float* out, void* workspace, size_t ws_bytes,
+                                             void* stream);
+
+/* ---------------------------------------------------------------------------
  * One decode step (Sec. 3.3: append-only latent cache, then App. E attention):
  * the new key and value of every stream, k_new[b][kv][c] and v_new[b][kv][c]
  * (device, dtype kv_dt, contiguous, 16-byte aligned), are encoded into record

@@ -53,6 +53,8 @@ _SIGNATURES = {
     "spectra_attention_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I64]),
     "spectra_decode_attention": (_I32, [_PC, _PC, _P, _P, _I64, _I64, _P, _I32, _I32, _I32, _I32, _F32, _P, _P,
                                         _SZ, _P]),
+    "spectra_decode_attention_rope": (_I32, [_PC, _PC, _P, _P, _I64, _I64, _P, _I32, _I32, _I32, _I32, _F32, _P, _I64,
+                                              _P, _P, _SZ, _P]),
     "spectra_decode_step": (_I32, [_PC, _PC, _P, _P, _I64, _I64, _P, _P, _I32, _P, _I32, _I32, _I32, _I32, _F32,
                                    _P, _P, _SZ, _P]),
     "spectra_allocate_bits": (_I32, [_P, _PP, _P]),

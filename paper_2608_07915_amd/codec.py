@@ -241,6 +241,30 @@ def spectra_decode_attention(ck: Codec, cv: Codec, packed_k, packed_v, t_capacit
     return out
 
 
+def spectra_decode_attention_rope(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, n_tokens: int, q,
+                                  n_kv_heads: int, inv_freq, q_position: Optional[int] = None, softmax_scale: float = 0.0,
+                                  out=None, workspace=None, stream=None):
+    """Decode-step attention for rotary models: keys reconstructed and rotated at their slot
+    positions, the query at q_position (default n_tokens - 1); inv_freq: float32 [d/2] device."""
+    import torch
+    batch, n_q_heads, d = _attention_shapes(ck, cv, packed_k, packed_v, t_capacity, q, n_kv_heads, out)
+    _need(inv_freq.is_cuda and inv_freq.dtype == torch.float32 and inv_freq.is_contiguous()
+          and tuple(inv_freq.shape) == (d // 2,), f"inv_freq must be a contiguous float32 device tensor [{d // 2}]")
+    pos = int(n_tokens) - 1 if q_position is None else int(q_position)
+    if out is None:
+        out = torch.empty((batch, n_q_heads, d), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        need = spectra_attention_workspace_bytes(batch, n_q_heads, n_kv_heads, n_tokens)
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    check(_lib.get().spectra_decode_attention_rope(ctypes.byref(ck.struct), ctypes.byref(cv.struct),
+                                                   packed_k.data_ptr(), packed_v.data_ptr(), int(t_capacity),
+                                                   int(n_tokens), q.data_ptr(), _dtype_code(q), batch, n_q_heads,
+                                                   int(n_kv_heads), float(softmax_scale), inv_freq.data_ptr(), pos,
+                                                   out.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                                   _stream(stream)))
+    return out
+
+
 def spectra_decode_step(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, t: int, k_new, v_new, q,
                         n_kv_heads: int, softmax_scale: float = 0.0, out=None, workspace=None, stream=None):
     """Append k_new, v_new [batch, n_kv_heads, d] at record slot t, then attend over slots [0, t]:

@@ -254,7 +254,9 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
 size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, int64_t n_tokens) {
   if (batch <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_tokens <= 0) return 0;
   int32_t tpc;
-  const int32_t nch = attention_chunks(batch, n_kv_heads, n_tokens, &tpc);
+  // one workspace serves both attention entry points (latent, and with rotary embeddings)
+  const int32_t nch = std::max(attention_chunks(batch, n_kv_heads, n_tokens, &tpc),
+                               rope_attention_chunks(batch, n_kv_heads, n_tokens, &tpc));
   return attention_partial_floats(batch, n_q_heads, nch) * sizeof(float);
 }
 
@@ -329,6 +331,27 @@ spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_c
   if (st != SPECTRA_OK) return st;
   hipError_t e = launch_attention(a, (hipStream_t)stream);
   return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "attention launch");
+}
+
+spectra_status spectra_decode_attention_rope(const spectra_codec* ck, const spectra_codec* cv, const uint32_t* packed_k,
+                                             const uint32_t* packed_v, int64_t t_capacity, int64_t n_tokens, const void* q,
+                                             spectra_dtype q_dt, int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                             float softmax_scale, const float* inv_freq, int64_t q_position, float* out,
+                                             void* workspace, size_t ws_bytes, void* stream) {
+  AttnArgs a{};
+  const spectra_status st = prepare_attention("decode_attention_rope", ck, cv, packed_k, packed_v, t_capacity, n_tokens,
+                                              q, q_dt, batch, n_q_heads, n_kv_heads, softmax_scale, out, workspace,
+                                              ws_bytes, &a);
+  if (st != SPECTRA_OK) return st;
+  if (a.n_qh > 4) return fail(SPECTRA_EUNSUPPORTED, "decode_attention_rope: at most 4 query heads per kv head");
+  if (a.Wk > 16 || a.Wv > 16) return fail(SPECTRA_EUNSUPPORTED, "decode_attention_rope: records of at most 16 words");
+  if (!inv_freq || !aligned(inv_freq, 4)) return fail(SPECTRA_EINVAL, "decode_attention_rope: inv_freq must be non-null");
+  if (q_position < 0) return fail(SPECTRA_EINVAL, "decode_attention_rope: q_position negative");
+  a.inv_freq = inv_freq;
+  a.q_pos = q_position;
+  a.n_chunks = rope_attention_chunks(batch, n_kv_heads, n_tokens, &a.tiles_per_chunk);
+  hipError_t e = launch_attention_rope(a, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "attention (rope) launch");
 }
 
 spectra_status spectra_decode_step(const spectra_codec* ck, const spectra_codec* cv, uint32_t* packed_k,

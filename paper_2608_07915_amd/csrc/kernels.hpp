@@ -79,6 +79,10 @@ struct AttnArgs {
   int32_t app_f32;
   float* partial;        // workspace: per-chunk softmax partials
   float* out;            // [batch][n_q_heads][128]
+  // attention with rotary position embeddings only: pair frequencies [64] (device)
+  // and the query's position (key t sits at position t)
+  const float* inv_freq;
+  int64_t q_pos;
 };
 
 // Batched fp64 product C_b = A_{b / a_div} B_b, element strides; M, N multiples
@@ -104,6 +108,12 @@ hipError_t launch_gram(const spectra_dev::GramArgs& a, bool f32_input, hipStream
 // Decode-step attention; with a.app_k != nullptr the new token of every stream is
 // appended first (the decode step).
 hipError_t launch_attention(const spectra_dev::AttnArgs& a, hipStream_t st);
+// Merge of the chunk partials in a.partial into a.out (+ m_V, inverse value rotation).
+hipError_t launch_combine(const spectra_dev::AttnArgs& a, hipStream_t st);
+// Attention with rotary position embeddings (Mode A keys, latent values), then the
+// combine; chunk split from rope_attention_chunks.
+hipError_t launch_attention_rope(const spectra_dev::AttnArgs& a, hipStream_t st);
+int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);

@@ -27,14 +27,13 @@
 // each wavefront streams 64-token record tiles with the next tile's words
 // prefetched into registers; the four wavefronts merge their online-softmax
 // states in LDS and write one partial per chunk; combine_kernel merges chunks.
+#include "attn_common.hpp"
 #include "device_common.hpp"
 #include "encode_dev.hpp"
 #include "kernels.hpp"
 #include "kplan.hpp"
 
 namespace spectra_dev {
-
-constexpr int PART = 136;  // floats per (chunk, query head): m, l, Z[4], pad[2], acc[128]
 
 constexpr int kplan_mfmas(int B) { return (make_kplan(B).n_ops + 1) / 2; }
 constexpr int KM_MAX = 14;  // score MFMAs per slot, widest plan (B = 7)
@@ -47,50 +46,6 @@ static_assert(KMFMA_MAX == KM_MAX, "plan sizes");
 constexpr int QA_SLOT = KM_MAX * 4 * 4;  // uint32
 constexpr int QA_QUAD = NG * QA_SLOT;
 constexpr int WAVES = 4;
-constexpr int WROW = 72;  // bf16 per weight row (64 tokens + pad: spreads rows over LDS banks)
-constexpr float RESCALE_SLACK = 4.0f;  // log2 units: weights exp2(score - m) stay <= 16
-constexpr int AROW = D + 4;  // floats per row of merged value sums (rows of one wave spread over banks)
-constexpr int TROW = 68;  // uint32 per staged record-word row (64 tokens + pad: distinct words of one
-                          // token group fall on distinct LDS banks)
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = __builtin_fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-
-// DPP lane moves (row = 16 lanes): quad_perm [1,0,3,2] 0xB1 and [2,3,0,1] 0x4E,
-// row_half_mirror 0x141, row_mirror 0x140, row_bcast:15 0x142, row_bcast:31 0x143.
-// Lanes outside ROWMASK, or with no source, receive IDENT.
-template <int CTRL, int ROWMASK>
-__device__ __forceinline__ float dpp(float v, float ident) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, ident), __builtin_bit_cast(int, v),
-                                                               CTRL, ROWMASK, 0xF, false));
-}
-// Sum over the 64 lanes, valid in lane 63: butterflies within each row of 16,
-// then the row totals are chained through row broadcasts.
-__device__ __forceinline__ float wave_sum_lane63(float v) {
-  v += dpp<0xB1, 0xF>(v, 0.0f);
-  v += dpp<0x4E, 0xF>(v, 0.0f);
-  v += dpp<0x141, 0xF>(v, 0.0f);
-  v += dpp<0x140, 0xF>(v, 0.0f);
-  v += dpp<0x142, 0xA>(v, 0.0f);
-  v += dpp<0x143, 0xC>(v, 0.0f);
-  return v;
-}
-// Maximum over the 64 lanes, returned in every lane.
-__device__ __forceinline__ float wave_max_all(float v) {
-  v = __builtin_fmaxf(v, dpp<0xB1, 0xF>(v, v));
-  v = __builtin_fmaxf(v, dpp<0x4E, 0xF>(v, v));
-  v = __builtin_fmaxf(v, dpp<0x141, 0xF>(v, v));
-  v = __builtin_fmaxf(v, dpp<0x140, 0xF>(v, v));
-  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
-  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
-  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
-  return __builtin_fmaxf(__builtin_fmaxf(r0, r1), __builtin_fmaxf(r2, r3));
-}
-
 
 // ---------------------------------------------------------------------------
 // Decode-step append, done by the workgroup whose chunk holds the last tile:
@@ -289,68 +244,6 @@ __device__ __forceinline__ float prepare_query(const AttnArgs& a, int s, int b, 
 // Bytes of LDS holding the softmax-weight rows of all wavefronts: per wave and kept
 // slot, 2*NH rows (hi parts of the NH heads, then lo parts) of 64 bf16 tokens.
 __host__ __device__ constexpr int attn_wt_bytes(int nq) { return WAVES * NG * (8 * nq) * WROW * 2; }
-
-// ---------------------------------------------------------------------------
-// Value-code operands: the codes of in-group coefficients n and n + 1 (bit
-// offsets off = n*b and off + b in the group payload at record word `pay`) for
-// 8 consecutive tokens, as bf16 pairs. CLS 0: b in {1,2,4} (both codes in one
-// byte: one byte gather per token pair); CLS 1: b in {3,5,6,7} (one 32-bit
-// funnel-shift window per token holds both); both give 128 + c, the OR with the
-// exponent of 128 (`magic`, held in a VGPR) fused into the mask. CLS 2: b = 8,
-// exact c.
-// ---------------------------------------------------------------------------
-template <int CLS>
-__device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, int pay, int used, int b, int off,
-                                             int tok0, uint32_t magic, u32x4& r0, u32x4& r1) {
-  // offsets fit in 24 bits: full-rate 24-bit multiplies instead of 32-bit ones
-  const int w = pay + (off >> 5), o = off & 31;
-  const uint32_t* row = vt + __umul24(w, TROW) + tok0;
-  const u32x4 a0 = *reinterpret_cast<const u32x4*>(row);
-  const u32x4 a1 = *reinterpret_cast<const u32x4*>(row + 4);
-  const uint32_t M = (1u << b) - 1u;
-  const uint32_t MM = M | (M << 16);
-  if constexpr (CLS == 0) {
-    // byte k of two tokens' words in both halves of one register, then shift and mask
-    const uint32_t k = (uint32_t)o >> 3, sh = (uint32_t)o & 7u;
-    // bytes k, k, 4 + k, 4 + k (a byte broadcast, not a 32-bit multiply)
-    const uint32_t sel = __builtin_amdgcn_perm(k, k, 0u) | 0x04040000u;
-    uint32_t y[4];
-    y[0] = __builtin_amdgcn_perm(a0[1], a0[0], sel);
-    y[1] = __builtin_amdgcn_perm(a0[3], a0[2], sel);
-    y[2] = __builtin_amdgcn_perm(a1[1], a1[0], sel);
-    y[3] = __builtin_amdgcn_perm(a1[3], a1[2], sel);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      r0[i] = ((y[i] >> sh) & MM) | magic;
-      r1[i] = ((y[i] >> (sh + b)) & MM) | magic;
-    }
-  } else {
-    const int wn = (w + 1 < used) ? w + 1 : w;  // the next word only matters when a code straddles
-    const uint32_t* rown = vt + __umul24(wn, TROW) + tok0;
-    const u32x4 b0 = *reinterpret_cast<const u32x4*>(rown);
-    const u32x4 b1 = *reinterpret_cast<const u32x4*>(rown + 4);
-    uint32_t c[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      c[i] = __builtin_amdgcn_alignbit(b0[i], a0[i], o);
-      c[4 + i] = __builtin_amdgcn_alignbit(b1[i], a1[i], o);
-    }
-    if constexpr (CLS == 2) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        r0[i] = int_to_bf16_pair(c[2 * i] & 0xFFu, c[2 * i + 1] & 0xFFu);
-        r1[i] = int_to_bf16_pair((c[2 * i] >> 8) & 0xFFu, (c[2 * i + 1] >> 8) & 0xFFu);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t y = __builtin_amdgcn_perm(c[2 * i + 1], c[2 * i], 0x05040100u);
-        r0[i] = (y & MM) | magic;
-        r1[i] = ((y >> b) & MM) | magic;
-      }
-    }
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Score contributions of one kept key slot of width B for the lane's token:
@@ -912,6 +805,11 @@ static void launch_nq(const AttnArgs& a, hipStream_t st) {
     launch_nq_pw<NQ, 0, 0, false>(a, st);
 }
 
+hipError_t launch_combine(const AttnArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(combine_kernel, dim3(a.n_q_heads, a.batch), dim3(1024), 0, st, a);
+  return hipGetLastError();
+}
+
 static hipError_t launch_scan_combine(const AttnArgs& a, hipStream_t st) {
   switch ((a.n_qh + 3) / 4) {
     case 1: launch_nq<1>(a, st); break;
@@ -921,8 +819,7 @@ static hipError_t launch_scan_combine(const AttnArgs& a, hipStream_t st) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(combine_kernel, dim3(a.n_q_heads, a.batch), dim3(1024), 0, st, a);
-  return hipGetLastError();
+  return launch_combine(a, st);
 }
 
 // Decode-step attention; with a.app_k set, the decode step (append first): the

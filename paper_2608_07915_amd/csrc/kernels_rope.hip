@@ -1,0 +1,447 @@
+// Decode-step attention for rotary models (Sec. 3.3, Mode A): the cache holds
+// latents of pre-RoPE keys, so each key is reconstructed and then rotated at its
+// own position before its dot product with the rotated query; this is what keeps
+// Mode A exact under RoPE. Values need no rotation and stay in the latent space:
+// their weighted sums run over the kept value coefficients and the chunk combine
+// (log-sum-exp merge, + m_V, one inverse rotation) is the latent kernel's.
+//
+// One workgroup of eight wavefronts per (token chunk, KV head, sequence), one
+// 64-token tile at a time (the next tile's record words prefetched in registers),
+// two half tiles of 32 tokens each:
+//   1. wavefront w reconstructs key dimensions 16w..16w+15 of the 32 tokens,
+//      k = sum_G (s_tG codes_tG + z_tG) V_G^T + m_K V^T, on v_mfma_f32_16x16x32_bf16
+//      (one kept group per MFMA; codes are exact in bf16, the basis enters as three
+//      bf16 parts whose products are exact in fp32), into LDS;
+//   2. each thread rotates eight dimension pairs (i, i + 64) of one token by
+//      t w_i and takes their dot products with the rotated, scaled queries;
+//      cos/sin of t w_i come from the half tile's base angle (reduced in fp64)
+//      and a 32 x 64 table of in-half offsets by angle addition;
+//   3. online softmax (lane = token), identical in every wavefront; wavefront w
+//      adds the softmax-weighted codes of kept value slot w on
+//      v_mfma_f32_16x16x32_bf16 exactly as the latent kernel does.
+#include "attn_common.hpp"
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace spectra_dev {
+
+constexpr int RHT = 32;           // tokens per half tile
+constexpr int RKROW = RHT + 4;    // floats per reconstructed-key row (dimension x token)
+constexpr int RCS = 65;           // floats per row of the in-half rotation table
+constexpr int RVROW = 40;         // bf16 per weight row (32 tokens + pad, 16-byte aligned rows)
+constexpr int RWMAX = 16;         // record words per tensor staged for this kernel
+constexpr int RWAVES = 8;         // wavefronts per workgroup
+constexpr int RTHREADS = 64 * RWAVES;
+constexpr int RPG = RTHREADS / RHT;  // dimension-pair groups of the score step (16 x 4 pairs)
+
+// LDS layout (bytes) for NH query heads per KV head
+__host__ __device__ constexpr int rope_off_rv() { return RWMAX * TROW * 4; }
+__host__ __device__ constexpr int rope_off_kh() { return 2 * RWMAX * TROW * 4; }
+__host__ __device__ constexpr int rope_off_tc() { return rope_off_kh() + D * RKROW * 4; }
+__host__ __device__ constexpr int rope_off_ts() { return rope_off_tc() + RHT * RCS * 4; }
+__host__ __device__ constexpr int rope_off_base() { return rope_off_ts() + RHT * RCS * 4; }   // [2 halves][cos, sin][64]
+__host__ __device__ constexpr int rope_off_qr() { return rope_off_base() + 2 * 2 * 64 * 4; }
+__host__ __device__ constexpr int rope_off_red(int nh) { return rope_off_qr() + nh * D * 4; }
+__host__ __device__ constexpr int rope_off_wt(int nh) { return rope_off_red(nh) + RPG * nh * RHT * 4; }
+__host__ __device__ constexpr int rope_lds_bytes(int nh) { return rope_off_wt(nh) + RWAVES * 2 * nh * RVROW * 2; }
+static_assert(rope_off_wt(4) % 16 == 0 && (RVROW * 2) % 16 == 0, "weight rows are read 16 bytes at a time");
+static_assert((2 * 4) * AROW * 4 <= D * RKROW * 4, "value sums reuse the key rows");
+
+// cos and sin of an angle given exactly in fp64 (a position below 2^28 times an
+// fp32 frequency needs at most 52 significant bits). Cody-Waite reduction by pi/2
+// (two-term split, fused multiply-adds), then the Taylor series of sin and cos on
+// [-pi/4, pi/4] to degree 15 and 16 (truncation below 2e-17) in fp64, then the
+// quadrant's signs and swap; the results are rounded to fp32.
+__device__ __forceinline__ void sincos_reduced(double ang, float* c, float* s) {
+  constexpr double PIO2_HI = 1.5707963267948966;     // pi/2 rounded to fp64
+  constexpr double PIO2_LO = 6.123233995736766e-17;  // pi/2 - PIO2_HI
+  constexpr double TWO_OVER_PI = 0.6366197723675814;
+  const double k = __builtin_rint(ang * TWO_OVER_PI);
+  double y = __builtin_fma(-k, PIO2_HI, ang);
+  y = __builtin_fma(-k, PIO2_LO, y);
+  const double y2 = y * y;
+  // 1/n! for n = 2..16
+  double sp = 1.0 / 1307674368000.0;                         // 1/15!
+  sp = __builtin_fma(sp, -y2, 1.0 / 6227020800.0);           // 1/13!
+  sp = __builtin_fma(sp, -y2, 1.0 / 39916800.0);             // 1/11!
+  sp = __builtin_fma(sp, -y2, 1.0 / 362880.0);               // 1/9!
+  sp = __builtin_fma(sp, -y2, 1.0 / 5040.0);                 // 1/7!
+  sp = __builtin_fma(sp, -y2, 1.0 / 120.0);                  // 1/5!
+  sp = __builtin_fma(sp, -y2, 1.0 / 6.0);                    // 1/3!
+  sp = __builtin_fma(sp, -y2, 1.0);
+  const double sy = sp * y;                                  // y - y^3/3! + ... - y^15/15!
+  double cp = 1.0 / 20922789888000.0;                        // 1/16!
+  cp = __builtin_fma(cp, -y2, 1.0 / 87178291200.0);          // 1/14!
+  cp = __builtin_fma(cp, -y2, 1.0 / 479001600.0);            // 1/12!
+  cp = __builtin_fma(cp, -y2, 1.0 / 3628800.0);              // 1/10!
+  cp = __builtin_fma(cp, -y2, 1.0 / 40320.0);                // 1/8!
+  cp = __builtin_fma(cp, -y2, 1.0 / 720.0);                  // 1/6!
+  cp = __builtin_fma(cp, -y2, 1.0 / 24.0);                   // 1/4!
+  cp = __builtin_fma(cp, -y2, 0.5);                          // 1/2!
+  const double cy = __builtin_fma(cp, -y2, 1.0);             // 1 - y^2/2! + ... + y^16/16!
+  const int q = (int)((int64_t)k & 3);
+  const double sv = (q == 0) ? sy : (q == 1) ? cy : (q == 2) ? -sy : -cy;
+  const double cv = (q == 0) ? cy : (q == 1) ? -sy : (q == 2) ? -cy : sy;
+  *s = (float)sv;
+  *c = (float)cv;
+}
+
+template <int NQ>
+__global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
+  constexpr int NH = 4 * NQ;
+  static_assert(2 * NH <= 16, "stacked hi/lo weight rows");
+  extern __shared__ __attribute__((aligned(16))) uint8_t rsm[];
+  uint32_t* recK = reinterpret_cast<uint32_t*>(rsm);
+  uint32_t* recV = reinterpret_cast<uint32_t*>(rsm + rope_off_rv());
+  float* khat = reinterpret_cast<float*>(rsm + rope_off_kh());
+  float* tc = reinterpret_cast<float*>(rsm + rope_off_tc());
+  float* ts = reinterpret_cast<float*>(rsm + rope_off_ts());
+  float* base = reinterpret_cast<float*>(rsm + rope_off_base());
+  float* qr = reinterpret_cast<float*>(rsm + rope_off_qr());
+  float* red = reinterpret_cast<float*>(rsm + rope_off_red(NH));
+  __shared__ float mst[NH], lst[NH], zst[NH][NG];
+
+  const int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int s = b * a.n_kv_heads + kv;
+  const int nqh = a.n_qh;
+  const int Wk = a.Wk, Wv = a.Wv;
+  const Kept Kk = read_kept(a.bits_k + (int64_t)s * NG);
+  const Kept Kv = read_kept(a.bits_v + (int64_t)s * NG);
+  const bool ok = Kk.ok && Kv.ok && Kk.used <= Wk && Kv.used <= Wv;
+  const int64_t n_tiles = (a.n_tokens + 63) >> 6;
+  const int64_t tile_begin = (int64_t)chunk * a.tiles_per_chunk;
+  const int64_t tile_end = tile_begin + a.tiles_per_chunk < n_tiles ? tile_begin + a.tiles_per_chunk : n_tiles;
+
+  // ---- prologue: in-half rotation table, rotated queries, key-basis operands ----
+  for (int e = tid; e < RHT * 64; e += RTHREADS) {
+    const int r = e >> 6, i = e & 63;
+    float c, sn;
+    sincos_reduced((double)r * (double)a.inv_freq[i], &c, &sn);
+    tc[r * RCS + i] = c;
+    ts[r * RCS + i] = sn;
+  }
+  for (int e = tid; e < NH * 64; e += RTHREADS) {
+    const int h = e >> 6, i = e & 63;
+    float q0 = 0.0f, q1 = 0.0f;
+    if (h < nqh) {
+      const int64_t qi = ((int64_t)b * a.n_q_heads + kv * nqh + h) * D + i;
+      q0 = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi]);
+      q1 = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi + 64] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi + 64]);
+    }
+    float c, sn;
+    sincos_reduced((double)a.q_pos * (double)a.inv_freq[i], &c, &sn);
+    qr[h * D + i] = (q0 * c - q1 * sn) * a.scale_log2;
+    qr[h * D + 64 + i] = (q1 * c + q0 * sn) * a.scale_log2;
+  }
+  // Key reconstruction operands of this lane (16x16x32 layout): output dimension
+  // ch = 16 wave + (lane & 15), in-group coefficients 8 kg .. 8 kg + 7 (kg = lane >> 4)
+  // of each kept key slot, as three bf16 parts.
+  const int kg = lane >> 4;
+  const int ch = 16 * wave + (lane & 15);
+  const float* Vk = a.basis_k + (int64_t)s * D * D;
+  bf16x8 Vb[NG][3];
+  float vsum[NG];
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl) {
+    vsum[sl] = 0.0f;
+    if (sl < Kk.n) {
+      const float* vr = Vk + (int64_t)ch * D + G * Kk.grp[sl];
+      uint32_t p0[8], p1[8], p2[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) split3(vr[8 * kg + i], p0[i], p1[i], p2[i]);
+      Vb[sl][0] = as_bf16x8(u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])});
+      Vb[sl][1] = as_bf16x8(u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])});
+      Vb[sl][2] = as_bf16x8(u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])});
+      float acc = 0.0f;
+      for (int j = 0; j < G; ++j) acc += vr[j];
+      vsum[sl] = acc;
+    } else {
+#pragma unroll
+      for (int p = 0; p < 3; ++p) Vb[sl][p] = bf16x8{};
+    }
+  }
+  float bias = 0.0f;  // (m_K V^T)_ch
+  {
+    const float* ms = a.mean_k + (int64_t)s * D;
+    const float* vr = Vk + (int64_t)ch * D;
+    for (int j = 0; j < D; ++j) bias = __builtin_fmaf(ms[j], vr[j], bias);
+  }
+
+  // value path of this wavefront: kept value slot `wave`
+  const bool vslot = wave < Kv.n;
+  const int vB = vslot ? pick4(Kv.bits, wave) : 0, vpay = vslot ? pick4(Kv.pay, wave) : 0;
+  const int vgrp = vslot ? pick4(Kv.grp, wave) : 0;
+  const int col16 = lane & 15, kq = lane >> 4;
+  const int voff = 2 * col16 * vB;
+  uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + rope_off_wt(NH)) + wave * (2 * NH * RVROW);
+
+  float m_run[NH], l_run[NH], zacc[NH];
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    m_run[h] = -__builtin_inff();
+    l_run[h] = 0.0f;
+    zacc[h] = 0.0f;
+  }
+  f32x4 vacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+
+  // record words of one tile (64 W contiguous words per tensor), two per thread
+  const uint32_t* kps = a.packed_k + (int64_t)s * a.t_cap * Wk;
+  const uint32_t* vps = a.packed_v + (int64_t)s * a.t_cap * Wv;
+  constexpr int PFR = 64 * RWMAX / RTHREADS;
+  uint32_t pk[PFR], pv[PFR];
+  auto load_tile = [&](int64_t tt) {
+#pragma unroll
+    for (int i = 0; i < PFR; ++i) {
+      const int k = tid + RTHREADS * i;
+      pk[i] = k < 64 * Wk ? kps[tt * 64 * Wk + k] : 0u;
+      pv[i] = k < 64 * Wv ? vps[tt * 64 * Wv + k] : 0u;
+    }
+  };
+  if (ok && tile_begin < tile_end) load_tile(tile_begin);
+
+  for (int64_t tt = tile_begin; ok && tt < tile_end; ++tt) {
+    __syncthreads();  // the previous tile's LDS reads are done (and the prologue's writes visible)
+#pragma unroll
+    for (int i = 0; i < PFR; ++i) {
+      const int k = tid + RTHREADS * i;
+      if (k < 64 * Wk) recK[(k >> 6) * TROW + (k & 63)] = pk[i];
+      if (k < 64 * Wv) recV[(k >> 6) * TROW + (k & 63)] = pv[i];
+    }
+    if (wave == 0) {
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        float c, sn;
+        sincos_reduced((double)(tt * 64 + RHT * hb) * (double)a.inv_freq[lane], &c, &sn);
+        base[(2 * hb) * 64 + lane] = c;
+        base[(2 * hb + 1) * 64 + lane] = sn;
+      }
+    }
+    __syncthreads();
+    if (tt + 1 < tile_end) load_tile(tt + 1);
+
+    for (int hb = 0; hb < 2; ++hb) {
+      // keep the loop-invariant LDS operands (rotated queries, rotation table) as LDS
+      // reads inside the loop rather than ~80 registers held across it
+      asm volatile("" ::: "memory");
+      const int tok0 = RHT * hb;
+      // ---- 1. key dimension ch of tokens tok0 + (0..31): two 16-token MFMA blocks ----
+      {
+        float out[2][4];
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) out[blk][j] = bias;
+#pragma unroll
+        for (int sl = 0; sl < NG; ++sl) {
+          if (sl < Kk.n) {
+            const int pay = Kk.pay[sl];
+#pragma unroll
+            for (int blk = 0; blk < 2; ++blk) {
+              // A operand: codes 8 kg .. 8 kg + 7 of token tok0 + 16 blk + (lane & 15)
+              const uint32_t* rtok = recK + tok0 + 16 * blk + (lane & 15);
+              f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+              with_bits(Kk.bits[sl], [&](auto bc) {
+                constexpr int B = decltype(bc)::value;
+                auto word = [&](int i) { return rtok[(pay + i) * TROW]; };
+                uint32_t cd[8];
+                extract8<B>(word, 8 * kg, cd);
+                const bf16x8 A = as_bf16x8(u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]),
+                                                 int_to_bf16_pair(cd[4], cd[5]), int_to_bf16_pair(cd[6], cd[7])});
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Vb[sl][0], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Vb[sl][1], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Vb[sl][2], acc, 0, 0, 0);
+              });
+              // acc[j]: token 16 blk + 4 kg + j of the half tile, dimension ch
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const uint32_t m = recK[sl * TROW + tok0 + 16 * blk + 4 * kg + j];
+                out[blk][j] += h2f(m) * acc[j] + h2f(m >> 16) * vsum[sl];
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) khat[ch * RKROW + 16 * blk + 4 * kg + j] = out[blk][j];
+      }
+      __syncthreads();
+      // ---- 2. rotation at the key's position and the dot products with the queries ----
+      {
+        const int t = tid & (RHT - 1), pg = tid >> 5;  // pg < RPG
+        const float* bcs = base + (2 * hb) * 64;
+        const float* bsn = base + (2 * hb + 1) * 64;
+        float sc[NH];
+#pragma unroll
+        for (int h = 0; h < NH; ++h) sc[h] = 0.0f;
+#pragma unroll
+        for (int ii = 0; ii < 64 / RPG; ++ii) {
+          const int i = (64 / RPG) * pg + ii;
+          const float x0 = khat[i * RKROW + t], x1 = khat[(i + 64) * RKROW + t];
+          const float c1 = tc[t * RCS + i], s1 = ts[t * RCS + i];
+          const float cc = bcs[i] * c1 - bsn[i] * s1;   // cos((t_half + t) w_i)
+          const float ss = bsn[i] * c1 + bcs[i] * s1;   // sin((t_half + t) w_i)
+          const float r0 = x0 * cc - x1 * ss, r1 = x1 * cc + x0 * ss;
+#pragma unroll
+          for (int h = 0; h < NH; ++h) sc[h] = __builtin_fmaf(qr[h * D + i], r0, __builtin_fmaf(qr[h * D + 64 + i], r1, sc[h]));
+        }
+#pragma unroll
+        for (int h = 0; h < NH; ++h) red[(pg * NH + h) * RHT + t] = sc[h];
+      }
+      __syncthreads();
+      // ---- 3. online softmax over the half tile (lanes 0..31 = tokens) and value sums ----
+      const int tk = lane & (RHT - 1);
+      const bool valid = lane < RHT && tt * 64 + tok0 + tk < a.n_tokens;
+      float x[NH];
+      bool over = false;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int pg = 0; pg < RPG; ++pg) acc += red[(pg * NH + h) * RHT + tk];
+        x[h] = (valid && h < nqh) ? acc : -__builtin_inff();
+        over = over || x[h] > m_run[h] + RESCALE_SLACK;
+      }
+      if (__any(over)) {
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          if (__any(x[h] > m_run[h] + RESCALE_SLACK)) {
+            const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x[h]));
+            const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
+            l_run[h] *= alpha;
+            zacc[h] *= alpha;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int row = 4 * kq + j;
+              const float f = (row == h || row == NH + h) ? alpha : 1.0f;
+              vacc[0][j] *= f;
+              vacc[1][j] *= f;
+            }
+            m_run[h] = mn;
+          }
+        }
+      }
+      float p[NH];
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        p[h] = x[h] != -__builtin_inff() ? __builtin_amdgcn_exp2f(x[h] - m_run[h]) : 0.0f;
+        l_run[h] += p[h];
+      }
+      if (vslot) {
+        const uint32_t meta = valid ? recV[wave * TROW + tok0 + tk] : 0u;
+        const float sv = h2f(meta), zv = h2f(meta >> 16);
+#pragma unroll
+        for (int h = 0; h < NH; h += 2) {  // two heads per packed conversion
+          zacc[h] = __builtin_fmaf(p[h], zv, zacc[h]);
+          zacc[h + 1] = __builtin_fmaf(p[h + 1], zv, zacc[h + 1]);
+          const float w0 = p[h] * sv, w1 = p[h + 1] * sv;
+          const uint32_t hb2 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0, w1}, bf16x2));
+          const float h0 = __builtin_bit_cast(float, hb2 << 16), h1 = __builtin_bit_cast(float, hb2 & 0xFFFF0000u);
+          const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0 - h0, w1 - h1}, bf16x2));
+          if (lane < RHT) {
+            ws[h * RVROW + tk] = (uint16_t)hb2;
+            ws[(h + 1) * RVROW + tk] = (uint16_t)(hb2 >> 16);
+            ws[(NH + h) * RVROW + tk] = (uint16_t)lb;
+            ws[(NH + h + 1) * RVROW + tk] = (uint16_t)(lb >> 16);
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+        // rows 0..NH-1: hi weights of the heads, NH..2NH-1: lo; MFMA rows past them
+        // re-read a weight row and are never read back
+        const int arow = col16 < 2 * NH ? col16 : col16 - 2 * NH;
+        const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * RVROW + 8 * kq));
+        const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
+        uint32_t vmagic = 0x43004300u;
+        asm volatile("" : "+v"(vmagic));
+        auto body = [&](auto cls) {
+          constexpr int CLS = decltype(cls)::value;
+          u32x4 vc[2];
+          value_codes2<CLS>(recV, vpay, Kv.used, vB, voff, tok0 + 8 * kq, vmagic, vc[0], vc[1]);
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2) {
+            f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, as_bf16x8(vc[c2]), vacc[c2], 0, 0, 0);
+            if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
+            vacc[c2] = acc;
+          }
+        };
+        if (vB == 8)
+          body(std::integral_constant<int, 2>{});
+        else if (vB == 1 || vB == 2 || vB == 4)
+          body(std::integral_constant<int, 0>{});
+        else
+          body(std::integral_constant<int, 1>{});
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+  }
+
+  // ---- chunk partial: m, l and the zero-point sums per head, value sums per coefficient ----
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    const float l = wave_sum_lane63(l_run[h]);
+    const float z = wave_sum_lane63(zacc[h]);
+    if (wave == 0 && lane == 63) {
+      mst[h] = ok ? m_run[h] : -__builtin_inff();
+      lst[h] = l;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) zst[h][g] = 0.0f;
+    }
+    __syncthreads();
+    if (vslot && lane == 63) zst[h][vgrp] = z;
+  }
+  __syncthreads();  // all tile buffers are free: the key rows hold the value sums now
+  float* accw = khat;
+  if (vslot) {
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = 4 * kq + j;
+        if (row < 2 * NH) accw[row * AROW + G * vgrp + 2 * col16 + c2] = vacc[c2][j];
+      }
+  }
+  uint32_t kept_groups = 0u;
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl)
+    if (sl < Kv.n) kept_groups |= 1u << pick4(Kv.grp, sl);
+  __syncthreads();
+  float* part = a.partial + ((int64_t)b * a.n_q_heads + kv * nqh) * a.n_chunks * PART + (int64_t)chunk * PART;
+  for (int e = tid; e < nqh * D; e += RTHREADS) {
+    const int h = e >> 7, j = e & 127;
+    const bool kept = ok && ((kept_groups >> (j >> 5)) & 1u);
+    float* ph = part + (int64_t)h * a.n_chunks * PART;
+    ph[8 + j] = kept ? accw[h * AROW + j] + accw[(NH + h) * AROW + j] : 0.0f;
+    if (j == 0) {
+      ph[0] = mst[h];
+      ph[1] = lst[h];
+    }
+    if (j < NG) ph[2 + j] = zst[h][j];
+  }
+}
+
+}  // namespace spectra_dev
+
+namespace spectra {
+using namespace spectra_dev;
+
+// About one workgroup per CU in one round, at least four tiles per chunk.
+int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk) {
+  const int64_t n_tiles = (n_tokens + 63) / 64;
+  const int64_t groups = (int64_t)batch * n_kv_heads;
+  const int64_t want = (256 + groups - 1) / groups;
+  int64_t tpc = (n_tiles + want - 1) / want;
+  if (tpc < 4) tpc = 4;
+  *tiles_per_chunk = (int32_t)tpc;
+  return (int32_t)((n_tiles + tpc - 1) / tpc);
+}
+
+hipError_t launch_attention_rope(const AttnArgs& a, hipStream_t st) {
+  const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
+  hipLaunchKernelGGL(rope_attn_kernel<1>, grid, dim3(RTHREADS), rope_lds_bytes(4), st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_combine(a, st);
+}
+
+}  // namespace spectra
