@@ -334,6 +334,20 @@ def main():
     dec_ms = min(e0.elapsed_time(e1) for e0, e1 in dec_ev[1:])
     dec_bytes = H * n_rec * (Wk * 4 + d * 4) + H * (d * d * 4 + d * 4)
     del dec_out
+    # ---- Mode A attention with rotary embeddings (outside the step): one layer call ----
+    inv_freq = (500000.0 ** (-torch.arange(d // 2, dtype=torch.float64, device=dev) / (d // 2))).float()
+    rope_out = torch.empty((1, Hq, d), dtype=torch.float32, device=dev)
+    rope_ev = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        S.spectra_decode_attention_rope(layer_ck[0], layer_cv[0], layer_pk[0], layer_pv[0], t_cap, n_rec, qs[0, 0],
+                                        H, inv_freq, out=rope_out, workspace=ws)
+        e1.record()
+        rope_ev.append((e0, e1))
+    torch.cuda.synchronize()
+    rope_ms = min(e0.elapsed_time(e1) for e0, e1 in rope_ev[1:])
+    rope_bytes = algorithmic_bytes(w, Wk, Wv, n_rec)["attn_call"]
 
     # ---- derived throughput ----
     ab = lambda n: algorithmic_bytes(w, Wk, Wv, n)  # noqa: E731
@@ -384,6 +398,10 @@ def main():
                      "kernel": "decode_step (split-K scan with in-kernel query prep and append, then combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
         "traffic_detail": measured,
+        "mode_a_rope_attention": {"us_per_layer_call": round(rope_ms * 1e3, 1),
+                                  "GBps": round(rope_bytes / (rope_ms * 1e-3) / 1e9, 1),
+                                  "what": "spectra_decode_attention_rope (keys reconstructed and rotated) over one "
+                                          "layer, outside the step"},
         "mode_a_decode": {"ms_per_layer": round(dec_ms, 4), "GBps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
                           "frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                           "what": "spectra_decode of one layer's keys (8 streams) to fp32, outside the step"},

@@ -26,13 +26,15 @@
 namespace spectra_dev {
 
 constexpr int RHT = 32;           // tokens per half tile
-constexpr int RKROW = RHT + 4;    // floats per reconstructed-key row (dimension x token)
+constexpr int RKROW = RHT + 1;    // floats per reconstructed-key row (dimension x token; odd: the
+                                  // rows a wavefront writes fall on distinct banks)
 constexpr int RCS = 65;           // floats per row of the in-half rotation table
 constexpr int RVROW = 40;         // bf16 per weight row (32 tokens + pad, 16-byte aligned rows)
 constexpr int RWMAX = 16;         // record words per tensor staged for this kernel
 constexpr int RWAVES = 8;         // wavefronts per workgroup
 constexpr int RTHREADS = 64 * RWAVES;
 constexpr int RPG = RTHREADS / RHT;  // dimension-pair groups of the score step (16 x 4 pairs)
+constexpr int RPW = RWAVES;          // partial score sets after the in-wavefront pair reduction
 
 // LDS layout (bytes) for NH query heads per KV head
 __host__ __device__ constexpr int rope_off_rv() { return RWMAX * TROW * 4; }
@@ -42,7 +44,7 @@ __host__ __device__ constexpr int rope_off_ts() { return rope_off_tc() + RHT * R
 __host__ __device__ constexpr int rope_off_base() { return rope_off_ts() + RHT * RCS * 4; }   // [2 halves][cos, sin][64]
 __host__ __device__ constexpr int rope_off_qr() { return rope_off_base() + 2 * 2 * 64 * 4; }
 __host__ __device__ constexpr int rope_off_red(int nh) { return rope_off_qr() + nh * D * 4; }
-__host__ __device__ constexpr int rope_off_wt(int nh) { return rope_off_red(nh) + RPG * nh * RHT * 4; }
+__host__ __device__ constexpr int rope_off_wt(int nh) { return rope_off_red(nh) + RPW * nh * RHT * 4; }
 __host__ __device__ constexpr int rope_lds_bytes(int nh) { return rope_off_wt(nh) + RWAVES * 2 * nh * RVROW * 2; }
 static_assert(rope_off_wt(4) % 16 == 0 && (RVROW * 2) % 16 == 0, "weight rows are read 16 bytes at a time");
 static_assert((2 * 4) * AROW * 4 <= D * RKROW * 4, "value sums reuse the key rows");
@@ -236,28 +238,41 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
         for (int sl = 0; sl < NG; ++sl) {
           if (sl < Kk.n) {
             const int pay = Kk.pay[sl];
+            // A operands of both 16-token blocks first, then the two blocks' MFMA
+            // chains interleaved so that one block's products fill the other's latency
+            const uint32_t* rt0 = recK + tok0 + (lane & 15);
+            const uint32_t* rt1 = rt0 + 16;
+            float sc0[4], zc0[4], sc1[4], zc1[4];
 #pragma unroll
-            for (int blk = 0; blk < 2; ++blk) {
-              // A operand: codes 8 kg .. 8 kg + 7 of token tok0 + 16 blk + (lane & 15)
-              const uint32_t* rtok = recK + tok0 + 16 * blk + (lane & 15);
-              f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-              with_bits(Kk.bits[sl], [&](auto bc) {
-                constexpr int B = decltype(bc)::value;
-                auto word = [&](int i) { return rtok[(pay + i) * TROW]; };
-                uint32_t cd[8];
-                extract8<B>(word, 8 * kg, cd);
-                const bf16x8 A = as_bf16x8(u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]),
-                                                 int_to_bf16_pair(cd[4], cd[5]), int_to_bf16_pair(cd[6], cd[7])});
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Vb[sl][0], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Vb[sl][1], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Vb[sl][2], acc, 0, 0, 0);
-              });
-              // acc[j]: token 16 blk + 4 kg + j of the half tile, dimension ch
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t m0 = recK[sl * TROW + tok0 + 4 * kg + j];
+              const uint32_t m1 = recK[sl * TROW + tok0 + 16 + 4 * kg + j];
+              sc0[j] = h2f(m0);
+              zc0[j] = h2f(m0 >> 16);
+              sc1[j] = h2f(m1);
+              zc1[j] = h2f(m1 >> 16);
+            }
+            f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+            with_bits(Kk.bits[sl], [&](auto bc) {
+              constexpr int B = decltype(bc)::value;
+              uint32_t cd0[8], cd1[8];
+              extract8<B>([&](int i) { return rt0[(pay + i) * TROW]; }, 8 * kg, cd0);
+              extract8<B>([&](int i) { return rt1[(pay + i) * TROW]; }, 8 * kg, cd1);
+              const bf16x8 A0 = as_bf16x8(u32x4{int_to_bf16_pair(cd0[0], cd0[1]), int_to_bf16_pair(cd0[2], cd0[3]),
+                                                int_to_bf16_pair(cd0[4], cd0[5]), int_to_bf16_pair(cd0[6], cd0[7])});
+              const bf16x8 A1 = as_bf16x8(u32x4{int_to_bf16_pair(cd1[0], cd1[1]), int_to_bf16_pair(cd1[2], cd1[3]),
+                                                int_to_bf16_pair(cd1[4], cd1[5]), int_to_bf16_pair(cd1[6], cd1[7])});
 #pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const uint32_t m = recK[sl * TROW + tok0 + 16 * blk + 4 * kg + j];
-                out[blk][j] += h2f(m) * acc[j] + h2f(m >> 16) * vsum[sl];
+              for (int part = 0; part < 3; ++part) {
+                acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, Vb[sl][part], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, Vb[sl][part], acc1, 0, 0, 0);
               }
+            });
+            // acc_b[j]: token 16 b + 4 kg + j of the half tile, dimension ch
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              out[0][j] += sc0[j] * acc0[j] + zc0[j] * vsum[sl];
+              out[1][j] += sc1[j] * acc1[j] + zc1[j] * vsum[sl];
             }
           }
         }
@@ -286,8 +301,13 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
 #pragma unroll
           for (int h = 0; h < NH; ++h) sc[h] = __builtin_fmaf(qr[h * D + i], r0, __builtin_fmaf(qr[h * D + 64 + i], r1, sc[h]));
         }
+        // lanes t and t + 32 of a wavefront hold the same token: add their pair groups
 #pragma unroll
-        for (int h = 0; h < NH; ++h) red[(pg * NH + h) * RHT + t] = sc[h];
+        for (int h = 0; h < NH; ++h) sc[h] += __shfl_xor(sc[h], 32);
+        if (lane < RHT) {
+#pragma unroll
+          for (int h = 0; h < NH; ++h) red[(wave * NH + h) * RHT + t] = sc[h];
+        }
       }
       __syncthreads();
       // ---- 3. online softmax over the half tile (lanes 0..31 = tokens) and value sums ----
@@ -299,7 +319,7 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       for (int h = 0; h < NH; ++h) {
         float acc = 0.0f;
 #pragma unroll
-        for (int pg = 0; pg < RPG; ++pg) acc += red[(pg * NH + h) * RHT + tk];
+        for (int w = 0; w < RPW; ++w) acc += red[(w * NH + h) * RHT + tk];
         x[h] = (valid && h < nqh) ? acc : -__builtin_inff();
         over = over || x[h] > m_run[h] + RESCALE_SLACK;
       }
