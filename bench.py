@@ -45,9 +45,9 @@ DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "enco
                        "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "8020b6d0b9e3e7a3d1a819633499676ace6e96557e9881df35c9c3dab624f152": {
-        "fetch_bytes": 74546790, "write_bytes": 1674240,
-        "per_kernel": {"attn_kernel<1,8,8,true>": [70706790, 1657856], "combine_kernel": [3840000, 16384]}},
+    "b9f6b8d34df74539f80ce511cdfd029384db6b10edf384cc3c7ffe5576ae1b9b": {
+        "fetch_bytes": 74550682, "write_bytes": 1674240,
+        "per_kernel": {"attn_kernel<1,8,8,true>": [70710682, 1657856], "combine_kernel": [3840000, 16384]}},
 }
 
 
@@ -72,6 +72,9 @@ def _parse():
     ap.add_argument("--fit-weights", action="store_true",
                     help="time the calibrate-once fit from weights (Llama-3.1-8B keys: 32 layers x 8 heads, "
                          "d_model 4096) instead of the hot path; prints its own JSON line")
+    ap.add_argument("--skip-extras", action="store_true",
+                    help="skip the measurements outside the step (Mode A decode, attention with rotary embeddings), "
+                         "e.g. for counter passes over the step's kernels only")
     ap.add_argument("--kappa", type=float, default=0.5,
                     help="key share of the combined K+V budget (asymmetric split; 0.5 = symmetric records)")
     ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
@@ -180,6 +183,47 @@ def fit_weights_bench(args):
                       "config": {"workload": "llama3.1-8b keys", "n_layers": L, "n_kv_heads": H, "d_model": dm},
                       "product_gflop": round(flops / 1e9, 1),
                       "bits_first_layer": codec.bits[:H].cpu().numpy().tolist()}))
+
+
+def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_rec, qs, ws, Wk, Wv, H, Hq, d, dev):
+    """Timings outside the step on layer 0: Mode A reconstruction of the keys to fp32,
+    and attention with rotary embeddings (keys reconstructed and rotated)."""
+    dec_out = torch.empty((H, n_rec, d), dtype=torch.float32, device=dev)
+    dec_ev = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        S.spectra_decode(layer_ck[0], layer_pk[0], t_cap, 0, n_rec, out=dec_out)
+        e1.record()
+        dec_ev.append((e0, e1))
+    torch.cuda.synchronize()
+    dec_ms = min(e0.elapsed_time(e1) for e0, e1 in dec_ev[1:])
+    dec_bytes = H * n_rec * (Wk * 4 + d * 4) + H * (d * d * 4 + d * 4)
+    del dec_out
+    # ---- Mode A attention with rotary embeddings (outside the step): one layer call ----
+    inv_freq = (500000.0 ** (-torch.arange(d // 2, dtype=torch.float64, device=dev) / (d // 2))).float()
+    rope_out = torch.empty((1, Hq, d), dtype=torch.float32, device=dev)
+    rope_ev = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        S.spectra_decode_attention_rope(layer_ck[0], layer_cv[0], layer_pk[0], layer_pv[0], t_cap, n_rec, qs[0, 0],
+                                        H, inv_freq, out=rope_out, workspace=ws)
+        e1.record()
+        rope_ev.append((e0, e1))
+    torch.cuda.synchronize()
+    rope_ms = min(e0.elapsed_time(e1) for e0, e1 in rope_ev[1:])
+    rope_bytes = algorithmic_bytes(w, Wk, Wv, n_rec)["attn_call"]
+
+    return {
+        "mode_a_rope_attention": {"us_per_layer_call": round(rope_ms * 1e3, 1),
+                                  "GBps": round(rope_bytes / (rope_ms * 1e-3) / 1e9, 1),
+                                  "what": "spectra_decode_attention_rope (keys reconstructed and rotated) over one "
+                                          "layer, outside the step"},
+        "mode_a_decode": {"ms_per_layer": round(dec_ms, 4), "GBps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
+                          "frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                          "what": "spectra_decode of one layer's keys (8 streams) to fp32, outside the step"},
+    }
 
 
 def main():
@@ -322,32 +366,10 @@ def main():
 
     # ---- Mode A reconstruction (a9), outside the step: one layer's keys to fp32 ----
     n_rec = T + max(n_dec, 0)
-    dec_out = torch.empty((H, n_rec, d), dtype=torch.float32, device=dev)
-    dec_ev = []
-    for _ in range(4):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        S.spectra_decode(layer_ck[0], layer_pk[0], t_cap, 0, n_rec, out=dec_out)
-        e1.record()
-        dec_ev.append((e0, e1))
-    torch.cuda.synchronize()
-    dec_ms = min(e0.elapsed_time(e1) for e0, e1 in dec_ev[1:])
-    dec_bytes = H * n_rec * (Wk * 4 + d * 4) + H * (d * d * 4 + d * 4)
-    del dec_out
-    # ---- Mode A attention with rotary embeddings (outside the step): one layer call ----
-    inv_freq = (500000.0 ** (-torch.arange(d // 2, dtype=torch.float64, device=dev) / (d // 2))).float()
-    rope_out = torch.empty((1, Hq, d), dtype=torch.float32, device=dev)
-    rope_ev = []
-    for _ in range(4):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        S.spectra_decode_attention_rope(layer_ck[0], layer_cv[0], layer_pk[0], layer_pv[0], t_cap, n_rec, qs[0, 0],
-                                        H, inv_freq, out=rope_out, workspace=ws)
-        e1.record()
-        rope_ev.append((e0, e1))
-    torch.cuda.synchronize()
-    rope_ms = min(e0.elapsed_time(e1) for e0, e1 in rope_ev[1:])
-    rope_bytes = algorithmic_bytes(w, Wk, Wv, n_rec)["attn_call"]
+    extras = {}
+    if not args.skip_extras:
+        extras = outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_rec, qs, ws, Wk, Wv, H, Hq,
+                              d, dev)
 
     # ---- derived throughput ----
     ab = lambda n: algorithmic_bytes(w, Wk, Wv, n)  # noqa: E731
@@ -398,13 +420,7 @@ def main():
                      "kernel": "decode_step (split-K scan with in-kernel query prep and append, then combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
         "traffic_detail": measured,
-        "mode_a_rope_attention": {"us_per_layer_call": round(rope_ms * 1e3, 1),
-                                  "GBps": round(rope_bytes / (rope_ms * 1e-3) / 1e9, 1),
-                                  "what": "spectra_decode_attention_rope (keys reconstructed and rotated) over one "
-                                          "layer, outside the step"},
-        "mode_a_decode": {"ms_per_layer": round(dec_ms, 4), "GBps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
-                          "frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-                          "what": "spectra_decode of one layer's keys (8 streams) to fp32, outside the step"},
+        **extras,
         "decode_launch": "eager" if args.eager else "hip_graph",
         "fit_ms": round(fit_s * 1e3, 1),
         "input_generation_s": round(gen_s, 1),
