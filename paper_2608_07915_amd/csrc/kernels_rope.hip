@@ -7,15 +7,16 @@
 //
 // One workgroup of eight wavefronts per (token chunk, KV head, sequence), one
 // 64-token tile at a time (the next tile's record words prefetched in registers),
-// two half tiles of 32 tokens each:
-//   1. wavefront w reconstructs key dimensions 16w..16w+15 of the 32 tokens,
+// four workgroup barriers per tile:
+//   1. wavefront w reconstructs key dimensions 16w..16w+15 of the 64 tokens,
 //      k = sum_G (s_tG codes_tG + z_tG) V_G^T + m_K V^T, on v_mfma_f32_16x16x32_bf16
 //      (one kept group per MFMA; codes are exact in bf16, the basis enters as three
 //      bf16 parts whose products are exact in fp32), into LDS;
 //   2. each thread rotates eight dimension pairs (i, i + 64) of one token by
 //      t w_i and takes their dot products with the rotated, scaled queries;
-//      cos/sin of t w_i come from the half tile's base angle (reduced in fp64)
-//      and a 32 x 64 table of in-half offsets by angle addition;
+//      cos/sin of t w_i come from the tile's base angle (reduced in fp64, computed
+//      one tile ahead by a wavefront without value work) and a 64 x 64 table of
+//      in-tile offsets, by angle addition;
 //   3. online softmax (lane = token), identical in every wavefront; wavefront w
 //      adds the softmax-weighted codes of kept value slot w on
 //      v_mfma_f32_16x16x32_bf16 exactly as the latent kernel does.
@@ -25,29 +26,28 @@
 
 namespace spectra_dev {
 
-constexpr int RHT = 32;           // tokens per half tile
-constexpr int RKROW = RHT + 1;    // floats per reconstructed-key row (dimension x token; odd: the
+constexpr int RTT = 64;           // tokens per tile
+constexpr int RKROW = RTT + 1;    // floats per reconstructed-key row (dimension x token; odd: the
                                   // rows a wavefront writes fall on distinct banks)
-constexpr int RCS = 65;           // floats per row of the in-half rotation table
-constexpr int RVROW = 40;         // bf16 per weight row (32 tokens + pad, 16-byte aligned rows)
+constexpr int RCS = 65;           // floats per row of the in-tile rotation table
 constexpr int RWMAX = 16;         // record words per tensor staged for this kernel
 constexpr int RWAVES = 8;         // wavefronts per workgroup
 constexpr int RTHREADS = 64 * RWAVES;
-constexpr int RPG = RTHREADS / RHT;  // dimension-pair groups of the score step (16 x 4 pairs)
-constexpr int RPW = RWAVES;          // partial score sets after the in-wavefront pair reduction
+constexpr int RPP = 64 / RWAVES;  // dimension pairs per thread in the score step
 
 // LDS layout (bytes) for NH query heads per KV head
 __host__ __device__ constexpr int rope_off_rv() { return RWMAX * TROW * 4; }
 __host__ __device__ constexpr int rope_off_kh() { return 2 * RWMAX * TROW * 4; }
 __host__ __device__ constexpr int rope_off_tc() { return rope_off_kh() + D * RKROW * 4; }
-__host__ __device__ constexpr int rope_off_ts() { return rope_off_tc() + RHT * RCS * 4; }
-__host__ __device__ constexpr int rope_off_base() { return rope_off_ts() + RHT * RCS * 4; }   // [2 halves][cos, sin][64]
+__host__ __device__ constexpr int rope_off_ts() { return rope_off_tc() + RTT * RCS * 4; }
+__host__ __device__ constexpr int rope_off_base() { return rope_off_ts() + RTT * RCS * 4; }   // [2 tiles][cos, sin][64]
 __host__ __device__ constexpr int rope_off_qr() { return rope_off_base() + 2 * 2 * 64 * 4; }
 __host__ __device__ constexpr int rope_off_red(int nh) { return rope_off_qr() + nh * D * 4; }
-__host__ __device__ constexpr int rope_off_wt(int nh) { return rope_off_red(nh) + RPW * nh * RHT * 4; }
-__host__ __device__ constexpr int rope_lds_bytes(int nh) { return rope_off_wt(nh) + RWAVES * 2 * nh * RVROW * 2; }
-static_assert(rope_off_wt(4) % 16 == 0 && (RVROW * 2) % 16 == 0, "weight rows are read 16 bytes at a time");
+__host__ __device__ constexpr int rope_off_wt(int nh) { return rope_off_red(nh) + RWAVES * nh * RTT * 4; }
+__host__ __device__ constexpr int rope_lds_bytes(int nh) { return rope_off_wt(nh) + RWAVES * 2 * nh * WROW * 2; }
+static_assert(rope_off_wt(4) % 16 == 0 && (WROW * 2) % 16 == 0, "weight rows are read 16 bytes at a time");
 static_assert((2 * 4) * AROW * 4 <= D * RKROW * 4, "value sums reuse the key rows");
+static_assert(rope_lds_bytes(4) <= 160 * 1024, "LDS of one CU");
 
 // cos and sin of an angle given exactly in fp64 (a position below 2^28 times an
 // fp32 frequency needs at most 52 significant bits). Cody-Waite reduction by pi/2
@@ -115,8 +115,8 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   const int64_t tile_begin = (int64_t)chunk * a.tiles_per_chunk;
   const int64_t tile_end = tile_begin + a.tiles_per_chunk < n_tiles ? tile_begin + a.tiles_per_chunk : n_tiles;
 
-  // ---- prologue: in-half rotation table, rotated queries, key-basis operands ----
-  for (int e = tid; e < RHT * 64; e += RTHREADS) {
+  // ---- prologue: in-tile rotation table, rotated queries, key-basis operands ----
+  for (int e = tid; e < RTT * 64; e += RTHREADS) {
     const int r = e >> 6, i = e & 63;
     float c, sn;
     sincos_reduced((double)r * (double)a.inv_freq[i], &c, &sn);
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   const int vgrp = vslot ? pick4(Kv.grp, wave) : 0;
   const int col16 = lane & 15, kq = lane >> 4;
   const int voff = 2 * col16 * vB;
-  uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + rope_off_wt(NH)) + wave * (2 * NH * RVROW);
+  uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + rope_off_wt(NH)) + wave * (2 * NH * WROW);
 
   float m_run[NH], l_run[NH], zacc[NH];
 #pragma unroll
@@ -200,199 +200,201 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       pv[i] = k < 64 * Wv ? vps[tt * 64 * Wv + k] : 0u;
     }
   };
-  if (ok && tile_begin < tile_end) load_tile(tile_begin);
+  // cos/sin of the base angle 64 tt w_i of tile tt (lane = pair) into buffer `buf`
+  auto base_angles = [&](int64_t tt, int buf) {
+    float c, sn;
+    sincos_reduced((double)(tt * 64) * (double)a.inv_freq[lane], &c, &sn);
+    base[(2 * buf) * 64 + lane] = c;
+    base[(2 * buf + 1) * 64 + lane] = sn;
+  };
+  if (ok && tile_begin < tile_end) {
+    load_tile(tile_begin);
+    if (wave == 0) base_angles(tile_begin, 0);
+  }
 
   for (int64_t tt = tile_begin; ok && tt < tile_end; ++tt) {
-    __syncthreads();  // the previous tile's LDS reads are done (and the prologue's writes visible)
+    const int buf = (int)((tt - tile_begin) & 1);
+    __syncthreads();  // the previous tile's LDS reads are done; the prologue's and the base angles' writes visible
 #pragma unroll
     for (int i = 0; i < PFR; ++i) {
       const int k = tid + RTHREADS * i;
       if (k < 64 * Wk) recK[(k >> 6) * TROW + (k & 63)] = pk[i];
       if (k < 64 * Wv) recV[(k >> 6) * TROW + (k & 63)] = pv[i];
     }
-    if (wave == 0) {
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        float c, sn;
-        sincos_reduced((double)(tt * 64 + RHT * hb) * (double)a.inv_freq[lane], &c, &sn);
-        base[(2 * hb) * 64 + lane] = c;
-        base[(2 * hb + 1) * 64 + lane] = sn;
-      }
-    }
     __syncthreads();
     if (tt + 1 < tile_end) load_tile(tt + 1);
+    // keep the loop-invariant LDS operands (rotated queries, rotation table) as LDS
+    // reads inside the loop rather than registers held across it
+    asm volatile("" ::: "memory");
 
-    for (int hb = 0; hb < 2; ++hb) {
-      // keep the loop-invariant LDS operands (rotated queries, rotation table) as LDS
-      // reads inside the loop rather than ~80 registers held across it
-      asm volatile("" ::: "memory");
-      const int tok0 = RHT * hb;
-      // ---- 1. key dimension ch of tokens tok0 + (0..31): two 16-token MFMA blocks ----
-      {
-        float out[2][4];
+    // ---- 1. key dimension ch of the 64 tokens: four 16-token MFMA blocks, two at a time ----
 #pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
+    for (int pass = 0; pass < 2; ++pass) {
+      const int tok0 = 32 * pass;
+      float out[2][4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) out[blk][j] = bias;
+      for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int sl = 0; sl < NG; ++sl) {
-          if (sl < Kk.n) {
-            const int pay = Kk.pay[sl];
-            // A operands of both 16-token blocks first, then the two blocks' MFMA
-            // chains interleaved so that one block's products fill the other's latency
-            const uint32_t* rt0 = recK + tok0 + (lane & 15);
-            const uint32_t* rt1 = rt0 + 16;
-            float sc0[4], zc0[4], sc1[4], zc1[4];
+        for (int j = 0; j < 4; ++j) out[blk][j] = bias;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const uint32_t m0 = recK[sl * TROW + tok0 + 4 * kg + j];
-              const uint32_t m1 = recK[sl * TROW + tok0 + 16 + 4 * kg + j];
-              sc0[j] = h2f(m0);
-              zc0[j] = h2f(m0 >> 16);
-              sc1[j] = h2f(m1);
-              zc1[j] = h2f(m1 >> 16);
+      for (int sl = 0; sl < NG; ++sl) {
+        if (sl < Kk.n) {
+          const int pay = Kk.pay[sl];
+          // A operands of both 16-token blocks first, then the two blocks' MFMA
+          // chains interleaved so that one block's products fill the other's latency
+          const uint32_t* rt0 = recK + tok0 + (lane & 15);
+          const uint32_t* rt1 = rt0 + 16;
+          float sc0[4], zc0[4], sc1[4], zc1[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t m0 = recK[sl * TROW + tok0 + 4 * kg + j];
+            const uint32_t m1 = recK[sl * TROW + tok0 + 16 + 4 * kg + j];
+            sc0[j] = h2f(m0);
+            zc0[j] = h2f(m0 >> 16);
+            sc1[j] = h2f(m1);
+            zc1[j] = h2f(m1 >> 16);
+          }
+          f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+          with_bits(Kk.bits[sl], [&](auto bc) {
+            constexpr int B = decltype(bc)::value;
+            uint32_t cd0[8], cd1[8];
+            extract8<B>([&](int i) { return rt0[(pay + i) * TROW]; }, 8 * kg, cd0);
+            extract8<B>([&](int i) { return rt1[(pay + i) * TROW]; }, 8 * kg, cd1);
+            const bf16x8 A0 = as_bf16x8(u32x4{int_to_bf16_pair(cd0[0], cd0[1]), int_to_bf16_pair(cd0[2], cd0[3]),
+                                              int_to_bf16_pair(cd0[4], cd0[5]), int_to_bf16_pair(cd0[6], cd0[7])});
+            const bf16x8 A1 = as_bf16x8(u32x4{int_to_bf16_pair(cd1[0], cd1[1]), int_to_bf16_pair(cd1[2], cd1[3]),
+                                              int_to_bf16_pair(cd1[4], cd1[5]), int_to_bf16_pair(cd1[6], cd1[7])});
+#pragma unroll
+            for (int part = 0; part < 3; ++part) {
+              acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, Vb[sl][part], acc0, 0, 0, 0);
+              acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, Vb[sl][part], acc1, 0, 0, 0);
             }
-            f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-            with_bits(Kk.bits[sl], [&](auto bc) {
-              constexpr int B = decltype(bc)::value;
-              uint32_t cd0[8], cd1[8];
-              extract8<B>([&](int i) { return rt0[(pay + i) * TROW]; }, 8 * kg, cd0);
-              extract8<B>([&](int i) { return rt1[(pay + i) * TROW]; }, 8 * kg, cd1);
-              const bf16x8 A0 = as_bf16x8(u32x4{int_to_bf16_pair(cd0[0], cd0[1]), int_to_bf16_pair(cd0[2], cd0[3]),
-                                                int_to_bf16_pair(cd0[4], cd0[5]), int_to_bf16_pair(cd0[6], cd0[7])});
-              const bf16x8 A1 = as_bf16x8(u32x4{int_to_bf16_pair(cd1[0], cd1[1]), int_to_bf16_pair(cd1[2], cd1[3]),
-                                                int_to_bf16_pair(cd1[4], cd1[5]), int_to_bf16_pair(cd1[6], cd1[7])});
+          });
+          // acc_b[j]: token tok0 + 16 b + 4 kg + j of the tile, dimension ch
 #pragma unroll
-              for (int part = 0; part < 3; ++part) {
-                acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, Vb[sl][part], acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, Vb[sl][part], acc1, 0, 0, 0);
-              }
-            });
-            // acc_b[j]: token 16 b + 4 kg + j of the half tile, dimension ch
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              out[0][j] += sc0[j] * acc0[j] + zc0[j] * vsum[sl];
-              out[1][j] += sc1[j] * acc1[j] + zc1[j] * vsum[sl];
-            }
+          for (int j = 0; j < 4; ++j) {
+            out[0][j] += sc0[j] * acc0[j] + zc0[j] * vsum[sl];
+            out[1][j] += sc1[j] * acc1[j] + zc1[j] * vsum[sl];
           }
         }
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) khat[ch * RKROW + 16 * blk + 4 * kg + j] = out[blk][j];
       }
-      __syncthreads();
-      // ---- 2. rotation at the key's position and the dot products with the queries ----
-      {
-        const int t = tid & (RHT - 1), pg = tid >> 5;  // pg < RPG
-        const float* bcs = base + (2 * hb) * 64;
-        const float* bsn = base + (2 * hb + 1) * 64;
-        float sc[NH];
 #pragma unroll
-        for (int h = 0; h < NH; ++h) sc[h] = 0.0f;
+      for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int ii = 0; ii < 64 / RPG; ++ii) {
-          const int i = (64 / RPG) * pg + ii;
-          const float x0 = khat[i * RKROW + t], x1 = khat[(i + 64) * RKROW + t];
-          const float c1 = tc[t * RCS + i], s1 = ts[t * RCS + i];
-          const float cc = bcs[i] * c1 - bsn[i] * s1;   // cos((t_half + t) w_i)
-          const float ss = bsn[i] * c1 + bcs[i] * s1;   // sin((t_half + t) w_i)
-          const float r0 = x0 * cc - x1 * ss, r1 = x1 * cc + x0 * ss;
+        for (int j = 0; j < 4; ++j) khat[ch * RKROW + tok0 + 16 * blk + 4 * kg + j] = out[blk][j];
+    }
+    __syncthreads();
+
+    // ---- 2. rotation at the key's position and the dot products with the queries:
+    // thread (token lane, pairs RPP wave ..) ----
+    {
+      const int t = lane;
+      const float* bcs = base + (2 * buf) * 64;
+      const float* bsn = base + (2 * buf + 1) * 64;
+      float sc[NH];
 #pragma unroll
-          for (int h = 0; h < NH; ++h) sc[h] = __builtin_fmaf(qr[h * D + i], r0, __builtin_fmaf(qr[h * D + 64 + i], r1, sc[h]));
-        }
-        // lanes t and t + 32 of a wavefront hold the same token: add their pair groups
+      for (int h = 0; h < NH; ++h) sc[h] = 0.0f;
+#pragma unroll 4
+      for (int ii = 0; ii < RPP; ++ii) {
+        const int i = RPP * wave + ii;
+        const float x0 = khat[i * RKROW + t], x1 = khat[(i + 64) * RKROW + t];
+        const float c1 = tc[t * RCS + i], s1 = ts[t * RCS + i];
+        const float cc = bcs[i] * c1 - bsn[i] * s1;   // cos((64 tt + t) w_i)
+        const float ss = bsn[i] * c1 + bcs[i] * s1;   // sin((64 tt + t) w_i)
+        const float r0 = x0 * cc - x1 * ss, r1 = x1 * cc + x0 * ss;
 #pragma unroll
-        for (int h = 0; h < NH; ++h) sc[h] += __shfl_xor(sc[h], 32);
-        if (lane < RHT) {
-#pragma unroll
-          for (int h = 0; h < NH; ++h) red[(wave * NH + h) * RHT + t] = sc[h];
-        }
+        for (int h = 0; h < NH; ++h) sc[h] = __builtin_fmaf(qr[h * D + i], r0, __builtin_fmaf(qr[h * D + 64 + i], r1, sc[h]));
       }
-      __syncthreads();
-      // ---- 3. online softmax over the half tile (lanes 0..31 = tokens) and value sums ----
-      const int tk = lane & (RHT - 1);
-      const bool valid = lane < RHT && tt * 64 + tok0 + tk < a.n_tokens;
-      float x[NH];
-      bool over = false;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) red[(wave * NH + h) * RTT + t] = sc[h];
+    }
+    __syncthreads();
+    // the next tile's base angles, by the last wavefront (value slots are wavefronts 0..3)
+    if (wave == RWAVES - 1 && tt + 1 < tile_end) base_angles(tt + 1, buf ^ 1);
+
+    // ---- 3. online softmax over the tile (lane = token) and value sums ----
+    const bool valid = tt * 64 + lane < a.n_tokens;
+    float x[NH];
+    bool over = false;
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int w = 0; w < RWAVES; ++w) acc += red[(w * NH + h) * RTT + lane];
+      x[h] = (valid && h < nqh) ? acc : -__builtin_inff();
+      over = over || x[h] > m_run[h] + RESCALE_SLACK;
+    }
+    if (__any(over)) {
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
-        float acc = 0.0f;
+        if (__any(x[h] > m_run[h] + RESCALE_SLACK)) {
+          const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x[h]));
+          const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
+          l_run[h] *= alpha;
+          zacc[h] *= alpha;
 #pragma unroll
-        for (int w = 0; w < RPW; ++w) acc += red[(w * NH + h) * RHT + tk];
-        x[h] = (valid && h < nqh) ? acc : -__builtin_inff();
-        over = over || x[h] > m_run[h] + RESCALE_SLACK;
-      }
-      if (__any(over)) {
-#pragma unroll
-        for (int h = 0; h < NH; ++h) {
-          if (__any(x[h] > m_run[h] + RESCALE_SLACK)) {
-            const float mn = __builtin_fmaxf(m_run[h], wave_max_all(x[h]));
-            const float alpha = (m_run[h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - mn);
-            l_run[h] *= alpha;
-            zacc[h] *= alpha;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int row = 4 * kq + j;
-              const float f = (row == h || row == NH + h) ? alpha : 1.0f;
-              vacc[0][j] *= f;
-              vacc[1][j] *= f;
-            }
-            m_run[h] = mn;
+          for (int j = 0; j < 4; ++j) {
+            const int row = 4 * kq + j;
+            const float f = (row == h || row == NH + h) ? alpha : 1.0f;
+            vacc[0][j] *= f;
+            vacc[1][j] *= f;
           }
+          m_run[h] = mn;
         }
       }
-      float p[NH];
+    }
+    float p[NH];
 #pragma unroll
-      for (int h = 0; h < NH; ++h) {
-        p[h] = x[h] != -__builtin_inff() ? __builtin_amdgcn_exp2f(x[h] - m_run[h]) : 0.0f;
-        l_run[h] += p[h];
+    for (int h = 0; h < NH; ++h) {
+      p[h] = x[h] != -__builtin_inff() ? __builtin_amdgcn_exp2f(x[h] - m_run[h]) : 0.0f;
+      l_run[h] += p[h];
+    }
+    if (vslot) {
+      const uint32_t meta = valid ? recV[wave * TROW + lane] : 0u;
+      const float sv = h2f(meta), zv = h2f(meta >> 16);
+#pragma unroll
+      for (int h = 0; h < NH; h += 2) {  // two heads per packed conversion
+        zacc[h] = __builtin_fmaf(p[h], zv, zacc[h]);
+        zacc[h + 1] = __builtin_fmaf(p[h + 1], zv, zacc[h + 1]);
+        const float w0 = p[h] * sv, w1 = p[h + 1] * sv;
+        const uint32_t hb2 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0, w1}, bf16x2));
+        const float h0 = __builtin_bit_cast(float, hb2 << 16), h1 = __builtin_bit_cast(float, hb2 & 0xFFFF0000u);
+        const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0 - h0, w1 - h1}, bf16x2));
+        ws[h * WROW + lane] = (uint16_t)hb2;
+        ws[(h + 1) * WROW + lane] = (uint16_t)(hb2 >> 16);
+        ws[(NH + h) * WROW + lane] = (uint16_t)lb;
+        ws[(NH + h + 1) * WROW + lane] = (uint16_t)(lb >> 16);
       }
-      if (vslot) {
-        const uint32_t meta = valid ? recV[wave * TROW + tok0 + tk] : 0u;
-        const float sv = h2f(meta), zv = h2f(meta >> 16);
+      __builtin_amdgcn_wave_barrier();
+      // rows 0..NH-1: hi weights of the heads, NH..2NH-1: lo; MFMA rows past them
+      // re-read a weight row and are never read back
+      const int arow = col16 < 2 * NH ? col16 : col16 - 2 * NH;
+      const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
+      uint32_t vmagic = 0x43004300u;
+      asm volatile("" : "+v"(vmagic));
+      auto body = [&](auto cls) {
+        constexpr int CLS = decltype(cls)::value;
 #pragma unroll
-        for (int h = 0; h < NH; h += 2) {  // two heads per packed conversion
-          zacc[h] = __builtin_fmaf(p[h], zv, zacc[h]);
-          zacc[h + 1] = __builtin_fmaf(p[h + 1], zv, zacc[h + 1]);
-          const float w0 = p[h] * sv, w1 = p[h + 1] * sv;
-          const uint32_t hb2 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0, w1}, bf16x2));
-          const float h0 = __builtin_bit_cast(float, hb2 << 16), h1 = __builtin_bit_cast(float, hb2 & 0xFFFF0000u);
-          const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0 - h0, w1 - h1}, bf16x2));
-          if (lane < RHT) {
-            ws[h * RVROW + tk] = (uint16_t)hb2;
-            ws[(h + 1) * RVROW + tk] = (uint16_t)(hb2 >> 16);
-            ws[(NH + h) * RVROW + tk] = (uint16_t)lb;
-            ws[(NH + h + 1) * RVROW + tk] = (uint16_t)(lb >> 16);
-          }
-        }
-        __builtin_amdgcn_wave_barrier();
-        // rows 0..NH-1: hi weights of the heads, NH..2NH-1: lo; MFMA rows past them
-        // re-read a weight row and are never read back
-        const int arow = col16 < 2 * NH ? col16 : col16 - 2 * NH;
-        const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * RVROW + 8 * kq));
-        const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
-        uint32_t vmagic = 0x43004300u;
-        asm volatile("" : "+v"(vmagic));
-        auto body = [&](auto cls) {
-          constexpr int CLS = decltype(cls)::value;
+        for (int th = 0; th < 2; ++th) {
+          const int tok0 = 32 * th + 8 * kq;
+          const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * WROW + tok0));
           u32x4 vc[2];
-          value_codes2<CLS>(recV, vpay, Kv.used, vB, voff, tok0 + 8 * kq, vmagic, vc[0], vc[1]);
+          value_codes2<CLS>(recV, vpay, Kv.used, vB, voff, tok0, vmagic, vc[0], vc[1]);
 #pragma unroll
           for (int c2 = 0; c2 < 2; ++c2) {
             f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, as_bf16x8(vc[c2]), vacc[c2], 0, 0, 0);
             if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
             vacc[c2] = acc;
           }
-        };
-        if (vB == 8)
-          body(std::integral_constant<int, 2>{});
-        else if (vB == 1 || vB == 2 || vB == 4)
-          body(std::integral_constant<int, 0>{});
-        else
-          body(std::integral_constant<int, 1>{});
-        __builtin_amdgcn_wave_barrier();
-      }
+        }
+      };
+      if (vB == 8)
+        body(std::integral_constant<int, 2>{});
+      else if (vB == 1 || vB == 2 || vB == 4)
+        body(std::integral_constant<int, 0>{});
+      else
+        body(std::integral_constant<int, 1>{});
+      __builtin_amdgcn_wave_barrier();
     }
   }
 
@@ -457,9 +459,15 @@ int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_token
 }
 
 hipError_t launch_attention_rope(const AttnArgs& a, hipStream_t st) {
+  // the tile buffers need more than 64 KB of LDS: refuse a device that has less
+  int dev = 0, lds = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return e;
+  if (lds < rope_lds_bytes(4)) return hipErrorInvalidConfiguration;
   const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
   hipLaunchKernelGGL(rope_attn_kernel<1>, grid, dim3(RTHREADS), rope_lds_bytes(4), st, a);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_combine(a, st);
 }
