@@ -5,21 +5,23 @@
 // their weighted sums run over the kept value coefficients and the chunk combine
 // (log-sum-exp merge, + m_V, one inverse rotation) is the latent kernel's.
 //
-// One workgroup of eight wavefronts per (token chunk, KV head, sequence), one
-// 64-token tile at a time (the next tile's record words prefetched in registers),
-// four workgroup barriers per tile:
+// One workgroup of eight wavefronts per (token chunk, KV head, sequence), 64-token
+// tiles, three workgroup barriers per tile. While tile tt is processed, the record
+// words of tile tt + 1 are staged and its key codes unpacked, once for the whole
+// workgroup, into a bf16 tile in LDS:
 //   1. wavefront w reconstructs key dimensions 16w..16w+15 of the 64 tokens,
 //      k = sum_G (s_tG codes_tG + z_tG) V_G^T + m_K V^T, on v_mfma_f32_16x16x32_bf16
 //      (one kept group per MFMA; codes are exact in bf16, the basis enters as three
 //      bf16 parts whose products are exact in fp32), into LDS;
-//   2. each thread rotates eight dimension pairs (i, i + 64) of one token by
-//      t w_i and takes their dot products with the rotated, scaled queries;
-//      cos/sin of t w_i come from the tile's base angle (reduced in fp64, computed
-//      one tile ahead by a wavefront without value work) and a 64 x 64 table of
-//      in-tile offsets, by angle addition;
-//   3. online softmax (lane = token), identical in every wavefront; wavefront w
-//      adds the softmax-weighted codes of kept value slot w on
-//      v_mfma_f32_16x16x32_bf16 exactly as the latent kernel does.
+//   2. each thread rotates eight dimension pairs (i, i + 64) of one token by its
+//      in-tile offset t w_i (a 64 x 64 table) and takes their dot products with the
+//      queries rotated by (p_q - 64 tt) w_i, an angle reduced in fp64 once per tile;
+//      the product is the query at p_q against the key at 64 tt + t, since rotations
+//      compose and are orthogonal. The same threads unpack the next tile's key codes;
+//   3. online softmax (lane = token), identical in every wavefront; wavefront w adds
+//      the softmax-weighted codes of kept value slot w mod 4 over token half w / 4 on
+//      v_mfma_f32_16x16x32_bf16 exactly as the latent kernel does, and the last
+//      wavefront rotates the queries for the next tile.
 #include "attn_common.hpp"
 #include "device_common.hpp"
 #include "kernels.hpp"
@@ -27,9 +29,9 @@
 namespace spectra_dev {
 
 constexpr int RTT = 64;           // tokens per tile
-constexpr int RKROW = RTT + 1;    // floats per reconstructed-key row (dimension x token; odd: the
-                                  // rows a wavefront writes fall on distinct banks)
-constexpr int RCS = 65;           // floats per row of the in-tile rotation table
+constexpr int RKROW = RTT + 4;    // floats per reconstructed-key row (dimension x token, 16-byte rows)
+constexpr int RCS2 = 2 * 64 + 2;  // floats per row of the interleaved in-tile cos/sin table
+constexpr int RCP = 136;          // bf16 per token row of the unpacked key codes (4 kept groups + pad)
 constexpr int RWMAX = 16;         // record words per tensor staged for this kernel
 constexpr int RWAVES = 8;         // wavefronts per workgroup
 constexpr int RTHREADS = 64 * RWAVES;
@@ -37,16 +39,18 @@ constexpr int RPP = 64 / RWAVES;  // dimension pairs per thread in the score ste
 
 // LDS layout (bytes) for NH query heads per KV head
 __host__ __device__ constexpr int rope_off_rv() { return RWMAX * TROW * 4; }
-__host__ __device__ constexpr int rope_off_kh() { return 2 * RWMAX * TROW * 4; }
-__host__ __device__ constexpr int rope_off_tc() { return rope_off_kh() + D * RKROW * 4; }
-__host__ __device__ constexpr int rope_off_ts() { return rope_off_tc() + RTT * RCS * 4; }
-__host__ __device__ constexpr int rope_off_base() { return rope_off_ts() + RTT * RCS * 4; }   // [2 tiles][cos, sin][64]
-__host__ __device__ constexpr int rope_off_qr() { return rope_off_base() + 2 * 2 * 64 * 4; }
-__host__ __device__ constexpr int rope_off_red(int nh) { return rope_off_qr() + nh * D * 4; }
+__host__ __device__ constexpr int rope_off_codes() { return 2 * RWMAX * TROW * 4; }
+__host__ __device__ constexpr int rope_off_kmeta() { return rope_off_codes() + RTT * RCP * 2; }
+__host__ __device__ constexpr int rope_off_kh() { return rope_off_kmeta() + NG * RTT * 2 * 4; }
+__host__ __device__ constexpr int rope_off_tcs() { return rope_off_kh() + D * RKROW * 4; }
+__host__ __device__ constexpr int rope_off_qs(int) { return rope_off_tcs() + RTT * RCS2 * 4; }
+__host__ __device__ constexpr int rope_off_qpp(int nh) { return rope_off_qs(nh) + nh * D * 4; }
+__host__ __device__ constexpr int rope_off_red(int nh) { return rope_off_qpp(nh) + 64 * nh * 2 * 4; }
 __host__ __device__ constexpr int rope_off_wt(int nh) { return rope_off_red(nh) + RWAVES * nh * RTT * 4; }
 __host__ __device__ constexpr int rope_lds_bytes(int nh) { return rope_off_wt(nh) + RWAVES * 2 * nh * WROW * 2; }
+static_assert(rope_off_kmeta() % 16 == 0 && rope_off_kh() % 16 == 0 && rope_off_qpp(4) % 16 == 0, "16-byte reads");
 static_assert(rope_off_wt(4) % 16 == 0 && (WROW * 2) % 16 == 0, "weight rows are read 16 bytes at a time");
-static_assert((2 * 4) * AROW * 4 <= D * RKROW * 4, "value sums reuse the key rows");
+static_assert(2 * (2 * 4) * AROW * 4 <= D * RKROW * 4, "value sums of both token halves reuse the key rows");
 static_assert(rope_lds_bytes(4) <= 160 * 1024, "LDS of one CU");
 
 // cos and sin of an angle given exactly in fp64 (a position below 2^28 times an
@@ -95,11 +99,12 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t rsm[];
   uint32_t* recK = reinterpret_cast<uint32_t*>(rsm);
   uint32_t* recV = reinterpret_cast<uint32_t*>(rsm + rope_off_rv());
+  uint16_t* codes = reinterpret_cast<uint16_t*>(rsm + rope_off_codes());
+  float* kmeta = reinterpret_cast<float*>(rsm + rope_off_kmeta());
   float* khat = reinterpret_cast<float*>(rsm + rope_off_kh());
-  float* tc = reinterpret_cast<float*>(rsm + rope_off_tc());
-  float* ts = reinterpret_cast<float*>(rsm + rope_off_ts());
-  float* base = reinterpret_cast<float*>(rsm + rope_off_base());
-  float* qr = reinterpret_cast<float*>(rsm + rope_off_qr());
+  float* tcs = reinterpret_cast<float*>(rsm + rope_off_tcs());
+  float* qs = reinterpret_cast<float*>(rsm + rope_off_qs(NH));
+  float* qpp = reinterpret_cast<float*>(rsm + rope_off_qpp(NH));
   float* red = reinterpret_cast<float*>(rsm + rope_off_red(NH));
   __shared__ float mst[NH], lst[NH], zst[NH][NG];
 
@@ -115,13 +120,13 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   const int64_t tile_begin = (int64_t)chunk * a.tiles_per_chunk;
   const int64_t tile_end = tile_begin + a.tiles_per_chunk < n_tiles ? tile_begin + a.tiles_per_chunk : n_tiles;
 
-  // ---- prologue: in-tile rotation table, rotated queries, key-basis operands ----
+  // ---- prologue: in-tile rotation table, scaled queries, key-basis operands ----
   for (int e = tid; e < RTT * 64; e += RTHREADS) {
     const int r = e >> 6, i = e & 63;
     float c, sn;
     sincos_reduced((double)r * (double)a.inv_freq[i], &c, &sn);
-    tc[r * RCS + i] = c;
-    ts[r * RCS + i] = sn;
+    tcs[r * RCS2 + 2 * i] = c;
+    tcs[r * RCS2 + 2 * i + 1] = sn;
   }
   for (int e = tid; e < NH * 64; e += RTHREADS) {
     const int h = e >> 6, i = e & 63;
@@ -131,10 +136,8 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       q0 = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi]);
       q1 = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi + 64] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi + 64]);
     }
-    float c, sn;
-    sincos_reduced((double)a.q_pos * (double)a.inv_freq[i], &c, &sn);
-    qr[h * D + i] = (q0 * c - q1 * sn) * a.scale_log2;
-    qr[h * D + 64 + i] = (q1 * c + q0 * sn) * a.scale_log2;
+    qs[h * D + i] = q0 * a.scale_log2;
+    qs[h * D + 64 + i] = q1 * a.scale_log2;
   }
   // Key reconstruction operands of this lane (16x16x32 layout): output dimension
   // ch = 16 wave + (lane & 15), in-group coefficients 8 kg .. 8 kg + 7 (kg = lane >> 4)
@@ -170,10 +173,11 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
     for (int j = 0; j < D; ++j) bias = __builtin_fmaf(ms[j], vr[j], bias);
   }
 
-  // value path of this wavefront: kept value slot `wave`
-  const bool vslot = wave < Kv.n;
-  const int vB = vslot ? pick4(Kv.bits, wave) : 0, vpay = vslot ? pick4(Kv.pay, wave) : 0;
-  const int vgrp = vslot ? pick4(Kv.grp, wave) : 0;
+  // value path of this wavefront: kept value slot wave mod 4 over tokens 32 (wave / 4) ..
+  const int vsl = wave & 3, vhalf = wave >> 2;
+  const bool vslot = vsl < Kv.n;
+  const int vB = vslot ? pick4(Kv.bits, vsl) : 0, vpay = vslot ? pick4(Kv.pay, vsl) : 0;
+  const int vgrp = vslot ? pick4(Kv.grp, vsl) : 0;
   const int col16 = lane & 15, kq = lane >> 4;
   const int voff = 2 * col16 * vB;
   uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + rope_off_wt(NH)) + wave * (2 * NH * WROW);
@@ -192,39 +196,86 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   const uint32_t* vps = a.packed_v + (int64_t)s * a.t_cap * Wv;
   constexpr int PFR = 64 * RWMAX / RTHREADS;
   uint32_t pk[PFR], pv[PFR];
-  auto load_tile = [&](int64_t tt) {
+  auto load_k = [&](int64_t tt) {
 #pragma unroll
     for (int i = 0; i < PFR; ++i) {
       const int k = tid + RTHREADS * i;
       pk[i] = k < 64 * Wk ? kps[tt * 64 * Wk + k] : 0u;
+    }
+  };
+  auto load_v = [&](int64_t tt) {
+#pragma unroll
+    for (int i = 0; i < PFR; ++i) {
+      const int k = tid + RTHREADS * i;
       pv[i] = k < 64 * Wv ? vps[tt * 64 * Wv + k] : 0u;
     }
   };
-  // cos/sin of the base angle 64 tt w_i of tile tt (lane = pair) into buffer `buf`
-  auto base_angles = [&](int64_t tt, int buf) {
-    float c, sn;
-    sincos_reduced((double)(tt * 64) * (double)a.inv_freq[lane], &c, &sn);
-    base[(2 * buf) * 64 + lane] = c;
-    base[(2 * buf + 1) * 64 + lane] = sn;
-  };
-  if (ok && tile_begin < tile_end) {
-    load_tile(tile_begin);
-    if (wave == 0) base_angles(tile_begin, 0);
-  }
-
-  for (int64_t tt = tile_begin; ok && tt < tile_end; ++tt) {
-    const int buf = (int)((tt - tile_begin) & 1);
-    __syncthreads();  // the previous tile's LDS reads are done; the prologue's and the base angles' writes visible
+  auto stage_k = [&]() {
 #pragma unroll
     for (int i = 0; i < PFR; ++i) {
       const int k = tid + RTHREADS * i;
       if (k < 64 * Wk) recK[(k >> 6) * TROW + (k & 63)] = pk[i];
+    }
+  };
+  // codes of the staged key words as bf16 [token][slot * 32 + coefficient] and the
+  // per-token scale and zero point [slot][token]: thread (token lane, eight
+  // coefficients of one slot); the slot is uniform in a wavefront
+  auto unpack_k = [&]() {
+#pragma unroll
+    for (int r = 0; r < (NG * 4 * 64) / RTHREADS; ++r) {
+      const int g8 = wave + RWAVES * r, sl = g8 >> 2, k8 = g8 & 3;
+      if (sl < Kk.n) {
+        const int pay = pick4(Kk.pay, sl);
+        const uint32_t* rt = recK + lane;
+        with_bits(pick4(Kk.bits, sl), [&](auto bc) {
+          constexpr int B = decltype(bc)::value;
+          uint32_t cd[8];
+          extract8<B>([&](int i) { return rt[(pay + i) * TROW]; }, 8 * k8, cd);
+          *reinterpret_cast<u32x4*>(codes + lane * RCP + sl * G + 8 * k8) =
+              u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]), int_to_bf16_pair(cd[4], cd[5]),
+                    int_to_bf16_pair(cd[6], cd[7])};
+        });
+        if (k8 == 0) {
+          const uint32_t m = rt[sl * TROW];
+          *reinterpret_cast<f32x2*>(kmeta + 2 * (sl * RTT + lane)) = f32x2{h2f(m), h2f(m >> 16)};
+        }
+      }
+    }
+  };
+  // queries rotated by (p_q - 64 tt) w_i for tile tt, [pair i][head][2] (lane = pair)
+  auto rotate_queries = [&](int64_t tt) {
+    float c, sn;
+    sincos_reduced((double)(a.q_pos - tt * 64) * (double)a.inv_freq[lane], &c, &sn);
+#pragma unroll
+    for (int h = 0; h < NH; h += 2) {
+      const float a0 = qs[h * D + lane], a1 = qs[h * D + 64 + lane];
+      const float b0 = qs[(h + 1) * D + lane], b1 = qs[(h + 1) * D + 64 + lane];
+      *reinterpret_cast<f32x4*>(qpp + (lane * NH + h) * 2) =
+          f32x4{a0 * c - a1 * sn, a1 * c + a0 * sn, b0 * c - b1 * sn, b1 * c + b0 * sn};
+    }
+  };
+  if (ok && tile_begin < tile_end) {
+    load_k(tile_begin);
+    stage_k();
+    __syncthreads();  // staged words, the query and table writes visible
+    unpack_k();
+    if (wave == RWAVES - 1) rotate_queries(tile_begin);
+    if (tile_begin + 1 < tile_end) load_k(tile_begin + 1);
+    load_v(tile_begin);
+  }
+
+  for (int64_t tt = tile_begin; ok && tt < tile_end; ++tt) {
+    __syncthreads();  // the previous tile's LDS reads done; this tile's codes and rotated queries visible
+    if (tt + 1 < tile_end) stage_k();
+#pragma unroll
+    for (int i = 0; i < PFR; ++i) {
+      const int k = tid + RTHREADS * i;
       if (k < 64 * Wv) recV[(k >> 6) * TROW + (k & 63)] = pv[i];
     }
-    __syncthreads();
-    if (tt + 1 < tile_end) load_tile(tt + 1);
-    // keep the loop-invariant LDS operands (rotated queries, rotation table) as LDS
-    // reads inside the loop rather than registers held across it
+    if (tt + 2 < tile_end) load_k(tt + 2);
+    if (tt + 1 < tile_end) load_v(tt + 1);
+    // keep the loop-invariant LDS operands (rotation table) as LDS reads inside
+    // the loop rather than registers held across it
     asm volatile("" ::: "memory");
 
     // ---- 1. key dimension ch of the 64 tokens: four 16-token MFMA blocks, two at a time ----
@@ -239,58 +290,40 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int sl = 0; sl < NG; ++sl) {
         if (sl < Kk.n) {
-          const int pay = Kk.pay[sl];
-          // A operands of both 16-token blocks first, then the two blocks' MFMA
-          // chains interleaved so that one block's products fill the other's latency
-          const uint32_t* rt0 = recK + tok0 + (lane & 15);
-          const uint32_t* rt1 = rt0 + 16;
-          float sc0[4], zc0[4], sc1[4], zc1[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t m0 = recK[sl * TROW + tok0 + 4 * kg + j];
-            const uint32_t m1 = recK[sl * TROW + tok0 + 16 + 4 * kg + j];
-            sc0[j] = h2f(m0);
-            zc0[j] = h2f(m0 >> 16);
-            sc1[j] = h2f(m1);
-            zc1[j] = h2f(m1 >> 16);
-          }
+          const bf16x8 A0 = as_bf16x8(*reinterpret_cast<const u32x4*>(codes + (tok0 + (lane & 15)) * RCP + sl * G + 8 * kg));
+          const bf16x8 A1 =
+              as_bf16x8(*reinterpret_cast<const u32x4*>(codes + (tok0 + 16 + (lane & 15)) * RCP + sl * G + 8 * kg));
           f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-          with_bits(Kk.bits[sl], [&](auto bc) {
-            constexpr int B = decltype(bc)::value;
-            uint32_t cd0[8], cd1[8];
-            extract8<B>([&](int i) { return rt0[(pay + i) * TROW]; }, 8 * kg, cd0);
-            extract8<B>([&](int i) { return rt1[(pay + i) * TROW]; }, 8 * kg, cd1);
-            const bf16x8 A0 = as_bf16x8(u32x4{int_to_bf16_pair(cd0[0], cd0[1]), int_to_bf16_pair(cd0[2], cd0[3]),
-                                              int_to_bf16_pair(cd0[4], cd0[5]), int_to_bf16_pair(cd0[6], cd0[7])});
-            const bf16x8 A1 = as_bf16x8(u32x4{int_to_bf16_pair(cd1[0], cd1[1]), int_to_bf16_pair(cd1[2], cd1[3]),
-                                              int_to_bf16_pair(cd1[4], cd1[5]), int_to_bf16_pair(cd1[6], cd1[7])});
 #pragma unroll
-            for (int part = 0; part < 3; ++part) {
-              acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, Vb[sl][part], acc0, 0, 0, 0);
-              acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, Vb[sl][part], acc1, 0, 0, 0);
-            }
-          });
-          // acc_b[j]: token tok0 + 16 b + 4 kg + j of the tile, dimension ch
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            out[0][j] += sc0[j] * acc0[j] + zc0[j] * vsum[sl];
-            out[1][j] += sc1[j] * acc1[j] + zc1[j] * vsum[sl];
+          for (int part = 0; part < 3; ++part) {
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0, Vb[sl][part], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1, Vb[sl][part], acc1, 0, 0, 0);
           }
+          // acc_b[j]: token tok0 + 16 b + 4 kg + j of the tile, dimension ch
+          const float* mt0 = kmeta + 2 * (sl * RTT + tok0 + 4 * kg);
+          const f32x4 m00 = *reinterpret_cast<const f32x4*>(mt0), m01 = *reinterpret_cast<const f32x4*>(mt0 + 4);
+          const f32x4 m10 = *reinterpret_cast<const f32x4*>(mt0 + 32), m11 = *reinterpret_cast<const f32x4*>(mt0 + 36);
+          out[0][0] += m00[0] * acc0[0] + m00[1] * vsum[sl];
+          out[0][1] += m00[2] * acc0[1] + m00[3] * vsum[sl];
+          out[0][2] += m01[0] * acc0[2] + m01[1] * vsum[sl];
+          out[0][3] += m01[2] * acc0[3] + m01[3] * vsum[sl];
+          out[1][0] += m10[0] * acc1[0] + m10[1] * vsum[sl];
+          out[1][1] += m10[2] * acc1[1] + m10[3] * vsum[sl];
+          out[1][2] += m11[0] * acc1[2] + m11[1] * vsum[sl];
+          out[1][3] += m11[2] * acc1[3] + m11[3] * vsum[sl];
         }
       }
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) khat[ch * RKROW + tok0 + 16 * blk + 4 * kg + j] = out[blk][j];
+        *reinterpret_cast<f32x4*>(khat + ch * RKROW + tok0 + 16 * blk + 4 * kg) =
+            f32x4{out[blk][0], out[blk][1], out[blk][2], out[blk][3]};
     }
     __syncthreads();
 
-    // ---- 2. rotation at the key's position and the dot products with the queries:
-    // thread (token lane, pairs RPP wave ..) ----
+    // ---- 2. in-tile rotation and the dot products with the tile's rotated queries:
+    // thread (token lane, pairs RPP wave ..); then the next tile's key codes ----
     {
       const int t = lane;
-      const float* bcs = base + (2 * buf) * 64;
-      const float* bsn = base + (2 * buf + 1) * 64;
       float sc[NH];
 #pragma unroll
       for (int h = 0; h < NH; ++h) sc[h] = 0.0f;
@@ -298,19 +331,22 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       for (int ii = 0; ii < RPP; ++ii) {
         const int i = RPP * wave + ii;
         const float x0 = khat[i * RKROW + t], x1 = khat[(i + 64) * RKROW + t];
-        const float c1 = tc[t * RCS + i], s1 = ts[t * RCS + i];
-        const float cc = bcs[i] * c1 - bsn[i] * s1;   // cos((64 tt + t) w_i)
-        const float ss = bsn[i] * c1 + bcs[i] * s1;   // sin((64 tt + t) w_i)
-        const float r0 = x0 * cc - x1 * ss, r1 = x1 * cc + x0 * ss;
+        const f32x2 cs = *reinterpret_cast<const f32x2*>(tcs + t * RCS2 + 2 * i);
+        const float r0 = x0 * cs[0] - x1 * cs[1], r1 = x1 * cs[0] + x0 * cs[1];
 #pragma unroll
-        for (int h = 0; h < NH; ++h) sc[h] = __builtin_fmaf(qr[h * D + i], r0, __builtin_fmaf(qr[h * D + 64 + i], r1, sc[h]));
+        for (int h = 0; h < NH; h += 2) {
+          const f32x4 qv = *reinterpret_cast<const f32x4*>(qpp + (i * NH + h) * 2);
+          sc[h] = __builtin_fmaf(qv[0], r0, __builtin_fmaf(qv[1], r1, sc[h]));
+          sc[h + 1] = __builtin_fmaf(qv[2], r0, __builtin_fmaf(qv[3], r1, sc[h + 1]));
+        }
       }
 #pragma unroll
       for (int h = 0; h < NH; ++h) red[(wave * NH + h) * RTT + t] = sc[h];
     }
+    if (tt + 1 < tile_end) unpack_k();
     __syncthreads();
-    // the next tile's base angles, by the last wavefront (value slots are wavefronts 0..3)
-    if (wave == RWAVES - 1 && tt + 1 < tile_end) base_angles(tt + 1, buf ^ 1);
+    // the next tile's rotated queries, by the last wavefront
+    if (wave == RWAVES - 1 && tt + 1 < tile_end) rotate_queries(tt + 1);
 
     // ---- 3. online softmax over the tile (lane = token) and value sums ----
     const bool valid = tt * 64 + lane < a.n_tokens;
@@ -350,12 +386,14 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       l_run[h] += p[h];
     }
     if (vslot) {
-      const uint32_t meta = valid ? recV[wave * TROW + lane] : 0u;
+      const uint32_t meta = valid ? recV[vsl * TROW + lane] : 0u;
       const float sv = h2f(meta), zv = h2f(meta >> 16);
 #pragma unroll
       for (int h = 0; h < NH; h += 2) {  // two heads per packed conversion
-        zacc[h] = __builtin_fmaf(p[h], zv, zacc[h]);
-        zacc[h + 1] = __builtin_fmaf(p[h + 1], zv, zacc[h + 1]);
+        if (vhalf == 0) {  // zero-point sums over the whole tile once per slot
+          zacc[h] = __builtin_fmaf(p[h], zv, zacc[h]);
+          zacc[h + 1] = __builtin_fmaf(p[h + 1], zv, zacc[h + 1]);
+        }
         const float w0 = p[h] * sv, w1 = p[h + 1] * sv;
         const uint32_t hb2 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0, w1}, bf16x2));
         const float h0 = __builtin_bit_cast(float, hb2 << 16), h1 = __builtin_bit_cast(float, hb2 & 0xFFFF0000u);
@@ -372,20 +410,17 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
       uint32_t vmagic = 0x43004300u;
       asm volatile("" : "+v"(vmagic));
+      const int tok0 = 32 * vhalf + 8 * kq;
       auto body = [&](auto cls) {
         constexpr int CLS = decltype(cls)::value;
+        const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * WROW + tok0));
+        u32x4 vc[2];
+        value_codes2<CLS>(recV, vpay, Kv.used, vB, voff, tok0, vmagic, vc[0], vc[1]);
 #pragma unroll
-        for (int th = 0; th < 2; ++th) {
-          const int tok0 = 32 * th + 8 * kq;
-          const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * WROW + tok0));
-          u32x4 vc[2];
-          value_codes2<CLS>(recV, vpay, Kv.used, vB, voff, tok0, vmagic, vc[0], vc[1]);
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2) {
-            f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, as_bf16x8(vc[c2]), vacc[c2], 0, 0, 0);
-            if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
-            vacc[c2] = acc;
-          }
+        for (int c2 = 0; c2 < 2; ++c2) {
+          f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, as_bf16x8(vc[c2]), vacc[c2], 0, 0, 0);
+          if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
+          vacc[c2] = acc;
         }
       };
       if (vB == 8)
@@ -410,10 +445,10 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       for (int g = 0; g < NG; ++g) zst[h][g] = 0.0f;
     }
     __syncthreads();
-    if (vslot && lane == 63) zst[h][vgrp] = z;
+    if (vslot && vhalf == 0 && lane == 63) zst[h][vgrp] = z;
   }
-  __syncthreads();  // all tile buffers are free: the key rows hold the value sums now
-  float* accw = khat;
+  __syncthreads();  // all tile buffers are free: the key rows hold the value sums of both token halves now
+  float* accw = khat + vhalf * (2 * NH * AROW);
   if (vslot) {
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2)
@@ -428,12 +463,16 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   for (int sl = 0; sl < NG; ++sl)
     if (sl < Kv.n) kept_groups |= 1u << pick4(Kv.grp, sl);
   __syncthreads();
+  const float* acc_lo = khat;
+  const float* acc_hi = khat + 2 * NH * AROW;
   float* part = a.partial + ((int64_t)b * a.n_q_heads + kv * nqh) * a.n_chunks * PART + (int64_t)chunk * PART;
   for (int e = tid; e < nqh * D; e += RTHREADS) {
     const int h = e >> 7, j = e & 127;
     const bool kept = ok && ((kept_groups >> (j >> 5)) & 1u);
     float* ph = part + (int64_t)h * a.n_chunks * PART;
-    ph[8 + j] = kept ? accw[h * AROW + j] + accw[(NH + h) * AROW + j] : 0.0f;
+    ph[8 + j] = kept ? (acc_lo[h * AROW + j] + acc_lo[(NH + h) * AROW + j]) +
+                           (acc_hi[h * AROW + j] + acc_hi[(NH + h) * AROW + j])
+                     : 0.0f;
     if (j == 0) {
       ph[0] = mst[h];
       ph[1] = lst[h];
