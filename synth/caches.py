@@ -30,6 +30,7 @@ Two backends draw the same *distribution*:
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass, field
 from typing import Optional, Tuple
 
@@ -202,3 +203,27 @@ def device_queries(w: Workload, layer: int, step: int, device, seed: int = 0):
     if w.dtype == "f32":
         return torch.from_numpy(q).to(device)
     return torch.from_numpy(q.view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def numpy_layer_stream(w: Workload, seq: int, layer: int, tensor: int, n_tokens: int, seed: int = 0,
+                       shared_rank: int = 16, shared_frac: float = 0.3) -> np.ndarray:
+    """One per-layer stream, [T, n_kv_heads * 128]: the layer's KV heads side by side
+    (each drawn by ``numpy_stream``) plus a component shared across heads.
+
+    Real layers correlate their heads, which is what a transform over the whole
+    d_kv = n_kv_heads * 128 vector exploits and a per-head one cannot. Recipe: rng
+    ``default_rng([seed, workload_id, seq, layer, 1000 + tensor])``; U ~ N(0,1)^{d_kv x r}
+    scaled so the shared part carries ``shared_frac`` of the heads' mean channel
+    energy, Z ~ N(0,1)^{T x r}; X = [X_1 .. X_H] + Z U^T, then rounded like the heads
+    (fp32, or bf16 round-to-nearest-even). Returns float32 or uint16 bf16 bits.
+    """
+    heads = [numpy_stream(w, seq, layer, h, tensor, n_tokens=n_tokens, seed=seed) for h in range(w.n_kv_heads)]
+    x = np.concatenate([hh if w.dtype == "f32" else bf16_bits_to_f32(hh) for hh in heads], axis=1).astype(np.float64)
+    d_kv = x.shape[1]
+    rng = np.random.default_rng([seed, w.wid, seq, layer, 1000 + tensor])
+    u = rng.standard_normal((d_kv, shared_rank))
+    energy = float(np.mean(x * x))
+    u *= math.sqrt(shared_frac * energy / shared_rank)
+    z = rng.standard_normal((n_tokens, shared_rank))
+    x = (x + z @ u.T).astype(np.float32)
+    return x if w.dtype == "f32" else f32_to_bf16_bits(x)
