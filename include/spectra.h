@@ -47,7 +47,12 @@
  * inputs give unspecified (but in-bounds) codes.
  *
  * GPU support: head_dim = 128, group_size = 32, b_max <= 8, meta_bits = 32,
- * records of at most 64 words.
+ * records of at most 64 words. Per-layer geometry (Sec. 4.1, App. F: one
+ * transform over a layer's whole KV vector, a stream being one (sequence, layer,
+ * tensor) matrix with head_dim = d_kv = n_kv_heads x 128): head_dim a multiple
+ * of 128 in [256, 1024] with group_size = 64 and records of at most 128 words,
+ * for spectra_fit_basis, spectra_encode (bf16 tokens) and spectra_decode; the
+ * other GPU entry points return SPECTRA_EUNSUPPORTED for it.
  * The host-only functions (allocation, eigensolver, fit from moments) accept
  * any head_dim <= 1024 that group_size divides.
  */
@@ -74,8 +79,8 @@ typedef enum { SPECTRA_F32 = 0, SPECTRA_BF16 = 1 } spectra_dtype;
 
 /* Parameters shared by all streams of a codec. */
 typedef struct {
-  int32_t head_dim;    /* d (128 on the GPU) */
-  int32_t group_size;  /* g: adjacent energy-ordered coefficients sharing one width (32 on the GPU) */
+  int32_t head_dim;    /* d (128 on the GPU; 256..1024 for the per-layer geometry) */
+  int32_t group_size;  /* g: adjacent energy-ordered coefficients sharing one width (32 on the GPU; 64 per layer) */
   int32_t b_max;       /* largest code width, <= 8 */
   int32_t meta_bits;   /* bits of metadata per kept group per token: 32 (fp16 s + fp16 z) */
   int32_t centered;    /* 0: basis of the uncentered second moment (Sec. 3.1); 1: of the covariance */

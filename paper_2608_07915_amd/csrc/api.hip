@@ -28,10 +28,13 @@ spectra_status hip_fail(hipError_t e, const char* what) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-spectra_status check_codec(const spectra_codec* c, const char* name) {
+spectra_status check_codec(const spectra_codec* c, const char* name, bool layer_ok = false) {
   if (!c) return fail(SPECTRA_EINVAL, "%s: null codec", name);
   spectra_status st = check_params_gpu(c->p);
   if (st != SPECTRA_OK) return st;
+  if (!layer_ok && layer_geometry(c->p))
+    return fail(SPECTRA_EUNSUPPORTED, "%s: the per-layer geometry (head_dim %d, group_size 64) supports fit, encode and decode only",
+                name, c->p.head_dim);
   if (c->record_words != record_words(c->p))
     return fail(SPECTRA_EINVAL, "%s: record_words %d does not match the parameters (%d); call spectra_codec_init",
                 name, c->record_words, record_words(c->p));
@@ -51,17 +54,19 @@ spectra_status check_slots(int64_t t0, int64_t n, int64_t t_cap) {
 }
 
 spectra_status check_input(const void* x, spectra_dtype dt, int64_t stream_stride, int64_t token_stride, int64_t n_streams,
-                           int64_t n_tokens) {
+                           int64_t n_tokens, int64_t d) {
   if (dt != SPECTRA_F32 && dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "dtype %d not supported", (int)dt);
   if (!x) return fail(SPECTRA_EINVAL, "null input");
   const int64_t vec = dt == SPECTRA_F32 ? 4 : 8;  // elements per 16 bytes
   if (!aligned(x, 16)) return fail(SPECTRA_EINVAL, "input must be 16-byte aligned");
   if (stream_stride < 0 || token_stride < 0 || stream_stride % vec || token_stride % vec)
     return fail(SPECTRA_EINVAL, "strides must be non-negative multiples of %lld elements", (long long)vec);
-  if (n_tokens > 1 && token_stride < kD) return fail(SPECTRA_EINVAL, "token_stride must be >= head_dim");
+  if (n_tokens > 1 && token_stride < d) return fail(SPECTRA_EINVAL, "token_stride must be >= head_dim");
   if (n_streams > 1 && stream_stride == 0) return fail(SPECTRA_EINVAL, "stream_stride is 0 for several streams");
   return SPECTRA_OK;
 }
+
+size_t round256(size_t b) { return (b + 255) / 256 * 256; }
 
 void moments_layout(int64_t n_streams, int64_t n_tokens, int32_t* n_chunks, int64_t* chunk_tokens) {
   int64_t want = (1024 + n_streams - 1) / n_streams;
@@ -80,17 +85,26 @@ size_t fit_ws_bytes(int64_t n_streams, int64_t n_tokens) {
   return (size_t)n_streams * (size_t)(nch + 1) * (size_t)kMoments * sizeof(double);
 }
 
-size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+// Per-layer geometry: moments [S][d*d + d], then the token-split partials [S][k_split][d*d].
+size_t layer_fit_ws_bytes(int32_t d, int64_t n_streams, int64_t n_tokens) {
+  int32_t ks;
+  int64_t ct;
+  layer_gram_layout(d, n_streams, n_tokens, &ks, &ct);
+  const size_t dd = (size_t)d * d;
+  return round256((size_t)n_streams * (dd + d) * sizeof(double)) + (size_t)n_streams * ks * dd * sizeof(double);
+}
 
 // Host half of a fit: eigenbasis, mean, variances and widths of every stream from
 // its moments (gram, column sums over n_tokens), in parallel, then copied into the
 // codec arrays. Synchronises hs.
 spectra_status finish_fit(spectra_codec* c, const std::vector<double>& mom, int64_t n_tokens, hipStream_t hs) {
   const int64_t S = c->n_streams;
+  const int d = c->p.head_dim;
+  const int64_t mstride = (int64_t)d * d + d;
   hipError_t e = hipSuccess;
-  std::vector<float> basis((size_t)S * kD * kD), mean((size_t)S * kD), var32((size_t)S * kD);
-  std::vector<double> var((size_t)S * kD);
-  const int nG = kD / c->p.group_size;
+  std::vector<float> basis((size_t)S * d * d), mean((size_t)S * d), var32((size_t)S * d);
+  std::vector<double> var((size_t)S * d);
+  const int nG = d / c->p.group_size;
   std::vector<uint8_t> bits((size_t)S * nG);
   std::vector<spectra_status> res((size_t)S, SPECTRA_OK);
   std::vector<std::string> msgs((size_t)S);
@@ -99,9 +113,9 @@ spectra_status finish_fit(spectra_codec* c, const std::vector<double>& mom, int6
   for (int w = 0; w < nthreads; ++w) {
     pool.emplace_back([&, w]() {
       for (int64_t s = w; s < S; s += nthreads) {
-        const double* m = &mom[(size_t)(s * kMoments)];
-        res[(size_t)s] = fit_from_moments(c->p, n_tokens, m, m + kD * kD, &basis[(size_t)s * kD * kD], &mean[(size_t)s * kD],
-                                          &var[(size_t)s * kD], &bits[(size_t)s * nG]);
+        const double* m = &mom[(size_t)(s * mstride)];
+        res[(size_t)s] = fit_from_moments(c->p, n_tokens, m, m + (size_t)d * d, &basis[(size_t)s * d * d], &mean[(size_t)s * d],
+                                          &var[(size_t)s * d], &bits[(size_t)s * nG]);
         if (res[(size_t)s] != SPECTRA_OK) msgs[(size_t)s] = spectra_last_error();
       }
     });
@@ -125,19 +139,45 @@ extern "C" {
 
 size_t spectra_fit_workspace_bytes(const spectra_codec* c, int64_t n_tokens) {
   if (!c || n_tokens <= 0 || c->n_streams <= 0) return 0;
+  if (layer_geometry(c->p)) return layer_fit_ws_bytes(c->p.head_dim, c->n_streams, n_tokens);
   return fit_ws_bytes(c->n_streams, n_tokens);
 }
 
 spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype dt, int64_t n_tokens,
                                  int64_t stream_stride, int64_t token_stride, void* workspace, size_t ws_bytes,
                                  void* stream) {
-  spectra_status st = check_codec(c, "fit_basis");
+  spectra_status st = check_codec(c, "fit_basis", true);
   if (st != SPECTRA_OK) return st;
   if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "fit_basis needs n_tokens >= 1");
-  st = check_input(x, dt, stream_stride, token_stride, c->n_streams, n_tokens);
+  st = check_input(x, dt, stream_stride, token_stride, c->n_streams, n_tokens, c->p.head_dim);
   if (st != SPECTRA_OK) return st;
   const int64_t S = c->n_streams;
   if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "fit workspace must be 256-byte aligned");
+  if (layer_geometry(c->p)) {
+    const int d = c->p.head_dim;
+    const size_t need = layer_fit_ws_bytes(d, S, n_tokens);
+    if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "fit workspace %zu < %zu bytes", ws_bytes, need);
+    hipStream_t hs = (hipStream_t)stream;
+    spectra_dev::LayerGramArgs g{};
+    g.x = x;
+    g.stream_stride = stream_stride;
+    g.token_stride = token_stride;
+    g.n = n_tokens;
+    g.n_streams = (int32_t)S;
+    g.d = d;
+    layer_gram_layout(d, S, n_tokens, &g.k_split, &g.chunk_tokens);
+    g.moments = reinterpret_cast<double*>(workspace);
+    g.partial = reinterpret_cast<double*>(static_cast<char*>(workspace) +
+                                          round256((size_t)S * ((size_t)d * d + d) * sizeof(double)));
+    hipError_t e = launch_layer_moments(g, dt == SPECTRA_F32, hs);
+    if (e != hipSuccess) return hip_fail(e, "fit moments launch");
+    std::vector<double> mom((size_t)S * ((size_t)d * d + d));
+    e = hipMemcpyAsync(mom.data(), g.moments, mom.size() * sizeof(double), hipMemcpyDeviceToHost, hs);
+    if (e != hipSuccess) return hip_fail(e, "fit moments copy");
+    e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return hip_fail(e, "fit moments sync");
+    return finish_fit(c, mom, n_tokens, hs);
+  }
   if (ws_bytes < fit_ws_bytes(S, n_tokens))
     return fail(SPECTRA_EWORKSPACE, "fit workspace %zu < %zu bytes", ws_bytes, fit_ws_bytes(S, n_tokens));
   hipStream_t hs = (hipStream_t)stream;
@@ -200,15 +240,34 @@ spectra_status spectra_fit_weights(spectra_codec* c, const float* W, int32_t d_m
 spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dtype dt, int64_t stream_stride,
                               int64_t token_stride, int64_t t0, int64_t n_tokens, uint32_t* packed, int64_t t_capacity,
                               void* stream) {
-  spectra_status st = check_codec(c, "encode");
+  spectra_status st = check_codec(c, "encode", true);
   if (st != SPECTRA_OK) return st;
   st = check_slots(t0, n_tokens, t_capacity);
   if (st != SPECTRA_OK) return st;
   if (n_tokens == 0) return SPECTRA_OK;
-  st = check_input(x, dt, stream_stride, token_stride, c->n_streams, n_tokens);
+  st = check_input(x, dt, stream_stride, token_stride, c->n_streams, n_tokens, c->p.head_dim);
   if (st != SPECTRA_OK) return st;
   if (!packed || !aligned(packed, 4)) return fail(SPECTRA_EINVAL, "packed must be non-null and 4-byte aligned");
   if (c->record_words == 0) return SPECTRA_OK;
+  if (layer_geometry(c->p)) {
+    if (dt != SPECTRA_BF16) return fail(SPECTRA_EUNSUPPORTED, "encode: the per-layer geometry takes bf16 tokens");
+    spectra_dev::LayerEncodeArgs a{};
+    a.x = x;
+    a.stream_stride = stream_stride;
+    a.token_stride = token_stride;
+    a.t0 = t0;
+    a.n = n_tokens;
+    a.basis = c->basis;
+    a.mean = c->mean;
+    a.bits = c->bits;
+    a.packed = packed;
+    a.t_cap = t_capacity;
+    a.W = c->record_words;
+    a.d = c->p.head_dim;
+    a.n_streams = (int32_t)c->n_streams;
+    hipError_t e = launch_layer_encode(a, (hipStream_t)stream);
+    return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "encode launch");
+  }
   EncodeArgs a{};
   a.x = x;
   a.stream_stride = stream_stride;
@@ -228,7 +287,7 @@ spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dty
 
 spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, int64_t t_capacity, int64_t t0,
                               int64_t n_tokens, float* out, void* stream) {
-  spectra_status st = check_codec(c, "decode");
+  spectra_status st = check_codec(c, "decode", true);
   if (st != SPECTRA_OK) return st;
   st = check_slots(t0, n_tokens, t_capacity);
   if (st != SPECTRA_OK) return st;
@@ -236,6 +295,23 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
   if (!out || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "out must be non-null and 4-byte aligned");
   if (c->record_words > 0 && (!packed || !aligned(packed, 4)))
     return fail(SPECTRA_EINVAL, "packed must be non-null and 4-byte aligned");
+  if (layer_geometry(c->p)) {
+    if (!aligned(out, 16)) return fail(SPECTRA_EINVAL, "decode: out must be 16-byte aligned for the per-layer geometry");
+    spectra_dev::LayerDecodeArgs a{};
+    a.packed = packed;
+    a.t_cap = t_capacity;
+    a.t0 = t0;
+    a.n = n_tokens;
+    a.basis = c->basis;
+    a.mean = c->mean;
+    a.bits = c->bits;
+    a.out = out;
+    a.W = c->record_words;
+    a.d = c->p.head_dim;
+    a.n_streams = (int32_t)c->n_streams;
+    hipError_t e = launch_layer_decode(a, (hipStream_t)stream);
+    return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "decode launch");
+  }
   DecodeArgs a{};
   a.packed = packed;
   a.t_cap = t_capacity;

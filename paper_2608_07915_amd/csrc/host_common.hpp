@@ -20,6 +20,9 @@ inline int32_t record_words(const spectra_params& p) { return budget_bits(p) / 3
 // Host-side validation of parameters (any head_dim); GPU limits are checked separately.
 spectra_status check_params(const spectra_params& p);
 spectra_status check_params_gpu(const spectra_params& p);
+// Per-layer geometry on the GPU: one stream per (sequence, layer, tensor), d = n_kv_heads x 128
+// in [256, 1024], groups of 64 (fit, encode and decode only).
+bool layer_geometry(const spectra_params& p);
 
 // Exact integer allocation (App. D objective, Sec. 3.2 groups, App. F rate).
 spectra_status allocate_bits(const double* var, const spectra_params& p, uint8_t* bits);

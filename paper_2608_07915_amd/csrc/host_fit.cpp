@@ -45,12 +45,22 @@ spectra_status check_params(const spectra_params& p) {
   return SPECTRA_OK;
 }
 
+bool layer_geometry(const spectra_params& p) {
+  return p.head_dim >= 256 && p.head_dim <= 1024 && p.head_dim % 128 == 0 && p.group_size == 64;
+}
+
 spectra_status check_params_gpu(const spectra_params& p) {
   spectra_status st = check_params(p);
   if (st != SPECTRA_OK) return st;
-  if (p.head_dim != 128) return fail(SPECTRA_EUNSUPPORTED, "GPU path needs head_dim=128 (got %d)", p.head_dim);
-  if (p.group_size != 32) return fail(SPECTRA_EUNSUPPORTED, "GPU path needs group_size=32 (got %d)", p.group_size);
   if (p.meta_bits != 32) return fail(SPECTRA_EUNSUPPORTED, "GPU path needs meta_bits=32 (got %d)", p.meta_bits);
+  if (layer_geometry(p)) {
+    if (record_words(p) > 128) return fail(SPECTRA_EUNSUPPORTED, "record of %d words exceeds 128", record_words(p));
+    return SPECTRA_OK;
+  }
+  if (p.head_dim != 128)
+    return fail(SPECTRA_EUNSUPPORTED, "GPU path needs head_dim=128, or a multiple of 128 in [256, 1024] with group_size=64 (got %d)",
+                p.head_dim);
+  if (p.group_size != 32) return fail(SPECTRA_EUNSUPPORTED, "GPU path needs group_size=32 at head_dim=128 (got %d)", p.group_size);
   if (record_words(p) > 64) return fail(SPECTRA_EUNSUPPORTED, "record of %d words exceeds 64", record_words(p));
   return SPECTRA_OK;
 }

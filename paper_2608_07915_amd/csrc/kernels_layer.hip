@@ -1,0 +1,455 @@
+// Per-layer cross-head latent (Sec. 3.1 applied to a layer's whole KV vector, the
+// geometry of Sec. 4.1 and App. F: d = d_kv = n_kv_heads x 128, latent groups of
+// g = 64 coefficients). A stream is one (sequence, layer, tensor) T x d matrix; the
+// record format is the per-head one with 64-coefficient groups (one metadata word
+// per kept group, then 2b payload words per kept group at b bits).
+//
+// Kernels:
+//   layer_gram_kernel     fp64 second moment x^T x of every stream, split over
+//                         token ranges (deterministic partial sums), 64 x 64 tiles;
+//   layer_moments_kernel  sums the partials in a fixed order and adds the column sums;
+//   layer_encode_kernel   c = x V - m on v_mfma_f32_32x32x16_bf16 (bf16 tokens exact,
+//                         the fp32 basis as three bf16 parts staged through LDS), then
+//                         per token and kept group fp16 zero-point and scale, codes,
+//                         packing; one workgroup per (256 tokens, kept group, stream);
+//   layer_decode_kernel   x_hat = sum_G (s_tG q_tG + z_tG 1) V_G^T + m V^T: codes
+//                         unpacked once per workgroup into LDS as bf16, the basis
+//                         columns of the group as three bf16 parts, the group's
+//                         per-token scale applied after its product; one workgroup per
+//                         (128 tokens, 128 channels, stream).
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace spectra_dev {
+
+constexpr int LG = 64;  // latent group size of the per-layer geometry
+
+// Kept group `slot` of a per-layer stream (widths bits_s[0..ng)): group index, width
+// and first payload word; also the number of kept groups and the record words used.
+struct LayerSlot {
+  int grp, b, pay, n_kept, used;
+  bool ok;  // every width in [0, 8]
+};
+__device__ __forceinline__ LayerSlot layer_slot(const uint8_t* __restrict__ bits_s, int ng, int slot) {
+  LayerSlot r{-1, 0, 0, 0, 0, true};
+  int n = 0, payw = 0;
+  for (int g = 0; g < ng; ++g) {
+    const int b = bits_s[g];
+    if (b > 8) r.ok = false;
+    if (b > 0) {
+      if (n == slot) {
+        r.grp = g;
+        r.b = b;
+        r.pay = payw;  // relative to the end of the metadata words
+      }
+      ++n;
+      payw += 2 * b;
+    }
+  }
+  r.n_kept = n;
+  r.pay += n;
+  r.used = n + payw;
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Moments
+// ---------------------------------------------------------------------------
+template <bool F32IN>
+__device__ __forceinline__ double load_x(const void* x, int64_t i) {
+  if constexpr (F32IN)
+    return (double)reinterpret_cast<const float*>(x)[i];
+  else
+    return (double)bf2f(reinterpret_cast<const uint16_t*>(x)[i]);
+}
+
+// partial[s][kc] (d x d) = sum over tokens [kc * ck, min(n, (kc + 1) ck)) of x_t^T x_t,
+// 64 x 64 output tile per workgroup, 16-token steps staged in LDS, 4 x 4 outputs per thread.
+template <bool F32IN>
+__global__ __launch_bounds__(256) void layer_gram_kernel(LayerGramArgs g) {
+  __shared__ double As[16][65];
+  __shared__ double Bs[16][65];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int i0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
+  const int s = blockIdx.z / g.k_split, kc = blockIdx.z % g.k_split;
+  const int64_t t_begin = (int64_t)kc * g.chunk_tokens;
+  const int64_t t_end = t_begin + g.chunk_tokens < g.n ? t_begin + g.chunk_tokens : g.n;
+  const int64_t xb = (int64_t)s * g.stream_stride;
+  double acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
+  for (int64_t t0 = t_begin; t0 < t_end; t0 += 16) {
+    // 16 tokens x 64 channels of each operand: thread -> (token tid >> 4, channels 4 (tid & 15) ..)
+    {
+      const int tk = tid >> 4, c4 = 4 * (tid & 15);
+      const int64_t t = t0 + tk;
+      const bool in = t < t_end;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        As[tk][c4 + e] = in ? load_x<F32IN>(g.x, xb + t * g.token_stride + i0 + c4 + e) : 0.0;
+        Bs[tk][c4 + e] = in ? load_x<F32IN>(g.x, xb + t * g.token_stride + j0 + c4 + e) : 0.0;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      double a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) a[q] = As[k][ty + 16 * q];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) b[q] = Bs[k][tx + 16 * q];
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[p][q] = __builtin_fma(a[p], b[q], acc[p][q]);
+    }
+    __syncthreads();
+  }
+  double* out = g.partial + ((int64_t)s * g.k_split + kc) * g.d * g.d;
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[(int64_t)(i0 + ty + 16 * p) * g.d + j0 + tx + 16 * q] = acc[p][q];
+}
+
+// moments[s] = [sum_kc partial[s][kc] (d x d), column sums (d)], partials added in
+// ascending kc, column sums over ascending tokens.
+template <bool F32IN>
+__global__ __launch_bounds__(256) void layer_moments_kernel(LayerGramArgs g) {
+  const int s = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t dd = (int64_t)g.d * g.d;
+  double* mom = g.moments + (int64_t)s * (dd + g.d);
+  if (e < dd) {
+    const double* p = g.partial + (int64_t)s * g.k_split * dd + e;
+    double acc = 0.0;
+    for (int kc = 0; kc < g.k_split; ++kc) acc += p[kc * dd];
+    mom[e] = acc;
+  } else if (e < dd + g.d) {
+    const int c = (int)(e - dd);
+    const int64_t xb = (int64_t)s * g.stream_stride + c;
+    double acc = 0.0;
+    for (int64_t t = 0; t < g.n; ++t) acc += load_x<F32IN>(g.x, xb + t * g.token_stride);
+    mom[e] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Encode
+// ---------------------------------------------------------------------------
+constexpr int LE_TOK = 256;       // tokens per workgroup (eight wavefronts of 32)
+constexpr int LE_KC = 64;         // basis rows per staged chunk
+constexpr int LE_KP = LE_KC + 8;  // bf16 per staged row (144-byte rows, 16-byte aligned)
+
+// Row of the staged 64-row operand that holds group coefficient c: within each
+// 32-row block, row r feeds coefficient 16 ((r >> 2) & 1) + (r & 3) + 4 (r >> 3), so
+// that after the 32x32 product lane half h holds coefficients 16h .. 16h + 15.
+__device__ __forceinline__ int le_row(int c) {
+  const int cc = c & 31;
+  return 32 * (c >> 5) + (cc & 3) + 4 * (cc >> 4) + 8 * ((cc >> 2) & 3);
+}
+
+__global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t vs[3][64][LE_KP];
+  const int s = blockIdx.z, slot = blockIdx.y;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
+  const int d = a.d, ng = d / LG;
+  const LayerSlot ks = layer_slot(a.bits + (int64_t)s * ng, ng, slot);
+  const int64_t sbase = (int64_t)s * a.t_cap * a.W;
+  const int64_t wg_tok = (int64_t)blockIdx.x * LE_TOK;
+  if (!ks.ok || ks.used > a.W) return;  // width table inconsistent with the record: write nothing
+
+  // words past the used ones are zero: written by the slot-0 workgroup
+  if (slot == 0 && ks.used < a.W) {
+    const int nw = a.W - ks.used;
+    for (int e = tid; e < LE_TOK * nw; e += 512) {
+      const int64_t i = wg_tok + (e % LE_TOK);
+      if (i < a.n) a.packed[rec_word(sbase, a.t0 + i, a.W, ks.used + e / LE_TOK)] = 0u;
+    }
+  }
+  if (slot >= ks.n_kept) return;  // uniform over the workgroup
+
+  const int64_t i_tok = wg_tok + 32 * wave + col;
+  const bool valid = i_tok < a.n;
+  const int64_t i_ld = valid ? i_tok : a.n - 1;
+  const uint16_t* xr = reinterpret_cast<const uint16_t*>(a.x) + (int64_t)s * a.stream_stride + i_ld * a.token_stride;
+  const float* V = a.basis + (int64_t)s * d * d + LG * ks.grp;
+
+  // staging map: thread -> (group coefficient sc, basis rows sk .. sk + 7 of the chunk)
+  const int sc = tid & 63, sk = 8 * (tid >> 6), srow = le_row(sc);
+  float pre[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) pre[i] = V[(int64_t)(sk + i) * d + sc];
+  u32x4 xb[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) xb[k] = *reinterpret_cast<const u32x4*>(xr + 16 * k + 8 * h);
+
+  // Accumulation order, for fp32 accuracy over d up to 1024 terms: the products with
+  // the basis' high bf16 part are summed per 64-row chunk and the chunk sums added
+  // into the running totals; the two low parts (2^-8 and 2^-16 of the value) go to a
+  // separate accumulator whose rounding is correspondingly small.
+  f32x16 acc0 = {}, acc1 = {}, sm0 = {}, sm1 = {};
+  const int nk = d / LE_KC;
+  for (int kc = 0; kc < nk; ++kc) {
+    {
+      uint32_t p0[8], p1[8], p2[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) split3(pre[i], p0[i], p1[i], p2[i]);
+      *reinterpret_cast<u32x4*>(&vs[0][srow][sk]) = u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])};
+      *reinterpret_cast<u32x4*>(&vs[1][srow][sk]) = u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])};
+      *reinterpret_cast<u32x4*>(&vs[2][srow][sk]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
+    }
+    __syncthreads();
+    u32x4 xn[4];
+    if (kc + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pre[i] = V[(int64_t)((kc + 1) * LE_KC + sk + i) * d + sc];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) xn[k] = *reinterpret_cast<const u32x4*>(xr + (kc + 1) * LE_KC + 16 * k + 8 * h);
+    }
+    f32x16 ch0 = {}, ch1 = {};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bf16x8 xk = as_bf16x8(xb[k]);
+#pragma unroll
+      for (int p = 0; p < 3; ++p) {
+        const bf16x8 a0 = as_bf16x8(*reinterpret_cast<const u32x4*>(&vs[p][col][16 * k + 8 * h]));
+        const bf16x8 a1 = as_bf16x8(*reinterpret_cast<const u32x4*>(&vs[p][32 + col][16 * k + 8 * h]));
+        if (p == 0) {
+          ch0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, xk, ch0, 0, 0, 0);
+          ch1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xk, ch1, 0, 0, 0);
+        } else {
+          sm0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, xk, sm0, 0, 0, 0);
+          sm1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xk, sm1, 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      acc0[i] += ch0[i];
+      acc1[i] += ch1[i];
+    }
+    if (kc + 1 < nk) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) xb[k] = xn[k];
+    }
+    __syncthreads();
+  }
+
+  // lane (h, col): coefficients 16h + i (acc0) and 32 + 16h + i (acc1) of token col
+  const float* mg = a.mean + (int64_t)s * d + LG * ks.grp;
+  float c[32];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    c[i] = (acc0[i] + sm0[i]) - mg[16 * h + i];
+    c[16 + i] = (acc1[i] + sm1[i]) - mg[32 + 16 * h + i];
+  }
+  float lo = c[0], hi = c[0];
+#pragma unroll
+  for (int i = 1; i < 32; ++i) {
+    lo = __builtin_fminf(lo, c[i]);
+    hi = __builtin_fmaxf(hi, c[i]);
+  }
+  lo = __builtin_fminf(lo, __shfl_xor(lo, 32));
+  hi = __builtin_fmaxf(hi, __shfl_xor(hi, 32));
+  const int64_t base = rec_word(sbase, a.t0 + i_ld, a.W, 0);
+  with_bits(ks.b, [&](auto bc) {
+    constexpr int B = decltype(bc)::value;
+    constexpr float LEV = (float)((1 << B) - 1);
+    const uint32_t z16 = f2h_sat(lo);
+    const float z = h2f(z16);
+    const uint32_t s16 = f2h_sat(__builtin_fmaxf(hi - z, 0.0f) / LEV);
+    const float sf = h2f(s16);
+    const float rinv = sf > 0.0f ? 1.0f / sf : 0.0f;
+    uint32_t q0[16], q1[16], P0[4], P1[4];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      q0[i] = (uint32_t)__builtin_fminf(__builtin_fmaxf(__builtin_rintf((c[i] - z) * rinv), 0.0f), LEV);
+      q1[i] = (uint32_t)__builtin_fminf(__builtin_fmaxf(__builtin_rintf((c[16 + i] - z) * rinv), 0.0f), LEV);
+    }
+    pack16<B>(q0, P0);
+    pack16<B>(q1, P1);
+    if (h == 0 && valid) a.packed[base + (int64_t)slot * TILE] = s16 | (z16 << 16);
+    store_payload<B>(a.packed, base, ks.pay, P0, h, valid);
+    store_payload<B>(a.packed, base, ks.pay + B, P1, h, valid);
+  });
+}
+
+// ---------------------------------------------------------------------------
+// Decode (Mode A)
+// ---------------------------------------------------------------------------
+constexpr int LD_TOK = 128;       // tokens per workgroup
+constexpr int LD_CH = 128;        // output channels per workgroup
+constexpr int LD_P = LG + 8;      // bf16 per LDS row (144 bytes)
+
+__global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t vsl[3][LD_CH][LD_P];   // basis columns of the group, [channel][coef]
+  __shared__ __attribute__((aligned(16))) uint16_t cod[LD_TOK][LD_P];     // codes, [token][coef]
+  __shared__ float sl[LD_TOK], zl[LD_TOK], vsum[LD_CH], bias[LD_CH];
+  const int s = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
+  const int d = a.d, ng = d / LG;
+  const int ch0 = blockIdx.y * LD_CH;
+  const int64_t tok0 = (int64_t)blockIdx.x * LD_TOK;
+  const int64_t sbase = (int64_t)s * a.t_cap * a.W;
+  const float* Vs = a.basis + (int64_t)s * d * d;
+  const uint8_t* bits_s = a.bits + (int64_t)s * ng;
+  const LayerSlot k0 = layer_slot(bits_s, ng, 0);
+  if (!k0.ok || k0.used > a.W) return;  // width table inconsistent with the record: write nothing
+
+  // bias = m V^T over all d coefficients: thread -> (channel tid >> 2, quarter tid & 3)
+  {
+    const int c = tid >> 2, q = tid & 3, span = d / 4;
+    const float* vr = Vs + (int64_t)(ch0 + c) * d + q * span;
+    const float* mr = a.mean + (int64_t)s * d + q * span;
+    float acc = 0.0f;
+    for (int j = 0; j < span; ++j) acc = __builtin_fmaf(mr[j], vr[j], acc);
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    if (q == 0) bias[c] = acc;
+  }
+
+  // wavefront -> channel block cb (32 channels), token blocks 2 tp, 2 tp + 1 (32 tokens each)
+  const int cb = wave & 3, tp = wave >> 2;
+  f32x16 out[2] = {f32x16{}, f32x16{}};
+  const int n_kept = k0.n_kept;
+  for (int slot = 0; slot < n_kept; ++slot) {
+    const LayerSlot ks = layer_slot(bits_s, ng, slot);
+    // codes of the group as bf16: thread -> (token e & 127, coefficients 8 (e >> 7) ..), two items
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int e = tid + 512 * r, u = e & (LD_TOK - 1), k8 = e >> 7;
+      const int64_t t = a.t0 + (tok0 + u < a.n ? tok0 + u : a.n - 1);
+      const int64_t base = rec_word(sbase, t, a.W, 0);
+      with_bits(ks.b, [&](auto bc) {
+        constexpr int B = decltype(bc)::value;
+        uint32_t cd[8];
+        extract8<B>([&](int i) { return a.packed[base + (int64_t)(ks.pay + i) * TILE]; }, 8 * k8, cd);
+        *reinterpret_cast<u32x4*>(&cod[u][8 * k8]) =
+            u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]), int_to_bf16_pair(cd[4], cd[5]),
+                  int_to_bf16_pair(cd[6], cd[7])};
+      });
+      if (k8 == 0) {
+        const uint32_t m = a.packed[base + (int64_t)slot * TILE];
+        sl[u] = h2f(m);
+        zl[u] = h2f(m >> 16);
+      }
+    }
+    // basis columns of the group, three bf16 parts, and their sums: thread -> (channel tid >> 2, 16 coefficients)
+    {
+      const int c = tid >> 2, q = tid & 3;
+      const float* vr = Vs + (int64_t)(ch0 + c) * d + LG * ks.grp + 16 * q;
+      float v[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] = vr[i];
+      float sum = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sum += v[i];
+      sum += __shfl_xor(sum, 1);
+      sum += __shfl_xor(sum, 2);
+      if (q == 0) vsum[c] = sum;
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        uint32_t p0[8], p1[8], p2[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) split3(v[8 * half + i], p0[i], p1[i], p2[i]);
+        const int j = 16 * q + 8 * half;
+        *reinterpret_cast<u32x4*>(&vsl[0][c][j]) = u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])};
+        *reinterpret_cast<u32x4*>(&vsl[1][c][j]) = u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])};
+        *reinterpret_cast<u32x4*>(&vsl[2][c][j]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
+      }
+    }
+    __syncthreads();
+    // D[channel][token] = sum_j V[channel][j] q[token][j] for this group
+    f32x16 g[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bf16x8 b0 = as_bf16x8(*reinterpret_cast<const u32x4*>(&cod[64 * tp + col][16 * k + 8 * h]));
+      const bf16x8 b1 = as_bf16x8(*reinterpret_cast<const u32x4*>(&cod[64 * tp + 32 + col][16 * k + 8 * h]));
+#pragma unroll
+      for (int p = 0; p < 3; ++p) {
+        const bf16x8 av = as_bf16x8(*reinterpret_cast<const u32x4*>(&vsl[p][32 * cb + col][16 * k + 8 * h]));
+        g[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, b0, g[0], 0, 0, 0);
+        g[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, b1, g[1], 0, 0, 0);
+      }
+    }
+    // lane (h, col): rows 4h + (i & 3) + 8 (i >> 2) = channels, column col = token
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int u = 64 * tp + 32 * tb + col;
+      const float st = sl[u], zt = zl[u];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int row = 4 * h + (i & 3) + 8 * (i >> 2);
+        out[tb][i] += st * g[tb][i] + zt * vsum[32 * cb + row];
+      }
+    }
+    __syncthreads();
+  }
+  if (n_kept == 0) __syncthreads();  // bias visible
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb) {
+    const int64_t i = tok0 + 64 * tp + 32 * tb + col;
+    if (i < a.n) {
+      float* o = a.out + ((int64_t)s * a.n + i) * d + ch0 + 32 * cb + 4 * h;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r0 = 32 * cb + 4 * h + 8 * q;
+        *reinterpret_cast<f32x4*>(o + 8 * q) =
+            f32x4{out[tb][4 * q] + bias[r0], out[tb][4 * q + 1] + bias[r0 + 1], out[tb][4 * q + 2] + bias[r0 + 2],
+                  out[tb][4 * q + 3] + bias[r0 + 3]};
+      }
+    }
+  }
+}
+
+}  // namespace spectra_dev
+
+namespace spectra {
+using namespace spectra_dev;
+
+// Token split of the second moment: enough workgroups to fill the chip, chunks of
+// at least 256 tokens.
+void layer_gram_layout(int32_t d, int64_t n_streams, int64_t n_tokens, int32_t* k_split, int64_t* chunk_tokens) {
+  const int64_t tiles = (int64_t)(d / 64) * (d / 64) * n_streams;
+  int64_t ks = (2048 + tiles - 1) / tiles;
+  const int64_t max_ks = (n_tokens + 255) / 256;
+  ks = ks < 1 ? 1 : (ks > max_ks ? max_ks : ks);
+  int64_t ct = (n_tokens + ks - 1) / ks;
+  ct = (ct + 15) / 16 * 16;
+  *chunk_tokens = ct;
+  *k_split = (int32_t)((n_tokens + ct - 1) / ct);
+}
+
+hipError_t launch_layer_moments(const LayerGramArgs& g, bool f32_in, hipStream_t st) {
+  const dim3 grid(g.d / 64, g.d / 64, g.n_streams * g.k_split);
+  if (f32_in)
+    hipLaunchKernelGGL(layer_gram_kernel<true>, grid, dim3(256), 0, st, g);
+  else
+    hipLaunchKernelGGL(layer_gram_kernel<false>, grid, dim3(256), 0, st, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t per = (int64_t)g.d * g.d + g.d;
+  const dim3 grid2((unsigned)((per + 255) / 256), g.n_streams);
+  if (f32_in)
+    hipLaunchKernelGGL(layer_moments_kernel<true>, grid2, dim3(256), 0, st, g);
+  else
+    hipLaunchKernelGGL(layer_moments_kernel<false>, grid2, dim3(256), 0, st, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_encode(const LayerEncodeArgs& a, hipStream_t st) {
+  const dim3 grid((unsigned)((a.n + LE_TOK - 1) / LE_TOK), a.d / LG, a.n_streams);
+  hipLaunchKernelGGL(layer_encode_kernel, grid, dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_decode(const LayerDecodeArgs& a, hipStream_t st) {
+  const dim3 grid((unsigned)((a.n + LD_TOK - 1) / LD_TOK), a.d / LD_CH, a.n_streams);
+  hipLaunchKernelGGL(layer_decode_kernel, grid, dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace spectra

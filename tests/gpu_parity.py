@@ -82,8 +82,14 @@ def _fp16_boundary_ok(pre: np.ndarray, got_bits: np.ndarray, want_bits: np.ndarr
     return adjacent & near
 
 
-def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gpu: np.ndarray) -> EncodeReport:
-    """P3-P5 for one stream: x64 [n, d] input values, rec_gpu [n, W] GPU records."""
+def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gpu: np.ndarray,
+                         dot_bound: bool = False) -> EncodeReport:
+    """P3-P5 for one stream: x64 [n, d] input values, rec_gpu [n, W] GPU records.
+
+    dot_bound (long projections, d > 128): a code may differ only where the oracle's
+    u = (c - z)/s lies within the forward error bound of the GPU's fp32 projection of
+    a half-integer: |dc| <= n_r 2^-24 sum_k |x_k V_kj| + 2^-23 |c| (n_r = d/16 + 16
+    sequential roundings: 16-term MFMA steps chained over d, then the chunk adds)."""
     W = O.record_words(p)
     coef = x64 @ basis.astype(np.float64) - mean.astype(np.float64)[None, :]
     codes_o, meta_o = O.quantize(coef, bits, p)
@@ -119,7 +125,18 @@ def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gp
     if np.any(mism):
         uu = u[:, kept][mism]
         assert np.all(np.abs(diff[mism]) == 1), "code off by more than one level"
-        assert np.all(np.abs(uu - np.floor(uu) - 0.5) <= TIE_TOL), "code mismatch away from a rounding tie"
+        if dot_bound:
+            d = x64.shape[1]
+            A = np.abs(x64) @ np.abs(basis.astype(np.float64))
+            s_tok = np.zeros_like(coef)
+            for G, b in enumerate(bits):
+                if b:
+                    s_tok[:, G * g:(G + 1) * g] = O.f16_bits_to_f64(meta_g[:, G] & 0xFFFF)[:, None]
+            dc = (d / 16 + 16) * 2.0 ** -24 * A + 2.0 ** -23 * np.abs(coef)
+            bound = (dc[:, kept] / np.where(s_tok[:, kept] > 0, s_tok[:, kept], np.inf))[mism] + 1e-6
+            assert np.all(np.abs(uu - np.floor(uu) - 0.5) <= bound), "code mismatch outside the fp32 projection bound"
+        else:
+            assert np.all(np.abs(uu - np.floor(uu) - 0.5) <= TIE_TOL), "code mismatch away from a rounding tie"
     assert frac <= 1e-4, f"code mismatch fraction {frac}"
     assert np.all(codes_g[:, ~kept] == 0)
     return EncodeReport(meta_frac, frac, n_codes)

@@ -1,0 +1,146 @@
+"""GPU parity of the per-layer geometry (one transform over a layer's whole KV
+vector, d = n_kv_heads x 128, latent groups of 64) against the oracle, through the
+C ABI: fit, encode (ragged token counts, offsets, appends) and decode (Mode A).
+Comparison rules are those of the per-head path (tests/gpu_parity.py), except that
+codes are judged against the forward error bound of a d-term fp32 projection."""
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2608_07915_amd as S
+import synth
+from gpu_parity import check_encoded_stream, codec_state, records_of, rel_l2, sparams, to_device, values_f64
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+
+def _layers(name, tensor, T, n_layers=1, seed=0):
+    w = synth.WORKLOADS[name]
+    return w, np.stack([synth.numpy_layer_stream(w, 0, l, tensor, T, seed=seed) for l in range(n_layers)])
+
+
+# The fit sees at least 2 d tokens: with fewer tokens than channels the second moment
+# is rank-deficient and the trailing coefficients are pure rounding noise, whose codes
+# no two correct implementations need to share.
+T_FIT = 2304
+
+
+def _fit(x_dev, p):
+    codec = S.Codec(sparams(p), x_dev.shape[0])
+    S.spectra_fit_basis(codec, x_dev)
+    return codec
+
+
+@pytest.mark.parametrize("name,tensor", [("qwen_layer_8x", 0), ("llama_layer_4x", 1)])
+def test_layer_fit_matches_oracle(name, tensor):
+    w, x = _layers(name, tensor, 3000)   # 3000 tokens: ragged 16-token steps and token split
+    d = x.shape[2]
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    codec = _fit(to_device(x, w.dtype), p)
+    basis, mean, bits = codec_state(codec, 0)
+    f = O.fit(values_f64(x[0], w.dtype), p)
+    V = basis.astype(np.float64)
+    assert np.abs(V.T @ V - np.eye(d)).max() <= 1e-5
+    D = V.T @ f.second_moment @ V
+    assert np.abs(D - np.diag(np.diag(D))).max() <= 1e-6 * f.eigvals[0]
+    assert np.allclose(np.diag(D), f.eigvals, rtol=0, atol=1e-5 * f.eigvals[0])
+    gap = np.minimum(np.abs(np.diff(f.eigvals, prepend=np.inf)), np.abs(np.diff(f.eigvals, append=-np.inf)))
+    clear = gap > 1e-3 * f.eigvals[0]
+    cos = np.sum(V * f.basis.astype(np.float64), axis=0)
+    assert np.all(cos[clear] >= 1 - 1e-6)
+    assert bits == O.allocate_bits(f.var, p)
+    assert np.abs(mean - f.mean).max() <= 1e-5 * np.abs(f.mean).max() + 1e-6
+
+
+CASES = [
+    ("qwen_layer_8x", 0, 1000, 0, 8.0),      # d = 512, several 256-token blocks, ragged tail
+    ("qwen_layer_8x", 1, 777, 64, 4.0),      # offset slots
+    ("llama_layer_4x", 0, 600, 0, 8.0),      # d = 1024, 64 words per record
+    ("llama_layer_4x", 1, 333, 128, 12.0),
+    ("qwen_layer_8x", 0, 300, 0, 2.0),       # 128-word records, most groups at 7-8 bits
+]
+
+
+@pytest.mark.parametrize("name,tensor,T,t0,ratio", CASES)
+def test_layer_encode_decode_parity(name, tensor, T, t0, ratio):
+    w, xf = _layers(name, tensor, max(T_FIT, T), n_layers=2)
+    x = np.ascontiguousarray(xf[:, :T])
+    d = x.shape[2]
+    p = O.Params(head_dim=d, group_size=64, ratio=ratio)
+    x_dev = to_device(x, w.dtype)
+    codec = _fit(to_device(xf, w.dtype), p)
+    W = O.record_words(p)
+    t_cap = (t0 + T + 63) // 64 * 64 + 64
+    packed = codec.empty_packed(t_cap)
+    packed.fill_(-1)
+    S.spectra_encode(codec, x_dev, t0, packed, t_cap)
+    dec_gpu = S.spectra_decode(codec, packed, t_cap, t0, T).cpu().numpy()
+    words = packed.cpu().numpy().view(np.uint32)
+    for s in range(x.shape[0]):
+        basis, mean, bits = codec_state(codec, s)
+        xs = values_f64(x[s], w.dtype)
+        rec = records_of(packed, s, t0, T, t_cap, W)
+        check_encoded_stream(xs, basis, mean, bits, p, rec, dot_bound=True)
+        dec_same = O.decode(rec, basis, mean, bits, p)
+        assert rel_l2(dec_gpu[s], dec_same) <= 1e-6
+        rec_o, *_ = O.encode(xs, basis, mean, bits, p)
+        dec_o = O.decode(rec_o, basis, mean, bits, p)
+        assert rel_l2(dec_gpu[s], dec_o) <= 1e-3
+        # slots outside [t0, t0 + T) untouched
+        outside = np.concatenate([np.arange(0, t0), np.arange(t0 + T, t_cap)])
+        for w_ in (0, W - 1):
+            assert np.all(words[O.physical_index(s, outside, w_, t_cap, W)] == 0xFFFFFFFF)
+
+
+def test_layer_appends_equal_one_shot_and_dropped_groups():
+    w, xf = _layers("qwen_layer_8x", 0, T_FIT)
+    x = np.ascontiguousarray(xf[:, :400])
+    d = x.shape[2]
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    x_dev = to_device(x, w.dtype)
+    codec = _fit(to_device(xf, w.dtype), p)
+    t_cap = 448
+    one = codec.empty_packed(t_cap)
+    S.spectra_encode(codec, x_dev, 0, one, t_cap)
+    pieces = codec.empty_packed(t_cap)
+    S.spectra_encode(codec, x_dev[:, :300], 0, pieces, t_cap)
+    for i in range(300, 303):
+        S.spectra_encode(codec, x_dev[:, i:i + 1], i, pieces, t_cap)
+    S.spectra_encode(codec, x_dev[:, 303:], 303, pieces, t_cap)
+    torch.cuda.synchronize()
+    assert torch.equal(one, pieces)
+    # groups kept out of order and everything dropped
+    ng = d // 64
+    for bits in ([0, 3, 0, 5, 0, 0, 2, 0], [0] * ng):
+        codec.bits.copy_(torch.tensor([bits[:ng]], dtype=torch.uint8))
+        packed = codec.empty_packed(t_cap)
+        packed.fill_(-1)
+        S.spectra_encode(codec, x_dev, 0, packed, t_cap)
+        dec = S.spectra_decode(codec, packed, t_cap, 0, 400).cpu().numpy()[0]
+        basis, mean, b = codec_state(codec, 0)
+        rec = records_of(packed, 0, 0, 400, t_cap, O.record_words(p))
+        xs = values_f64(x[0], w.dtype)
+        check_encoded_stream(xs, basis, mean, b, p, rec, dot_bound=True)
+        assert rel_l2(dec, O.decode(rec, basis, mean, b, p)) <= 1e-6
+        if not any(bits):
+            assert np.all(rec == 0)
+            want = np.tile(mean.astype(np.float64) @ basis.astype(np.float64).T, (400, 1))
+            assert rel_l2(dec, want) <= 1e-6
+
+
+def test_layer_rejects_what_it_does_not_run():
+    w, x = _layers("qwen_layer_8x", 0, 128)
+    d = x.shape[2]
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    codec = _fit(to_device(x, w.dtype), p)
+    t_cap = 128
+    packed = codec.empty_packed(t_cap)
+    with pytest.raises(S.SpectraError):
+        S.spectra_encode(codec, torch.from_numpy(synth.bf16_bits_to_f32(x)).cuda(), 0, packed, t_cap)  # fp32 tokens
+    q = torch.zeros((1, 28, d), dtype=torch.float32, device="cuda")
+    with pytest.raises((S.SpectraError, ValueError)):
+        S.spectra_decode_attention(codec, codec, packed, packed, t_cap, 128, q, 1)
