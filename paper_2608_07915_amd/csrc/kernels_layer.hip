@@ -287,7 +287,7 @@ constexpr int LD_P = LG + 8;      // bf16 per LDS row (144 bytes)
 __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vsl[3][LD_CH][LD_P];   // basis columns of the group, [channel][coef]
   __shared__ __attribute__((aligned(16))) uint16_t cod[LD_TOK][LD_P];     // codes, [token][coef]
-  __shared__ float sl[LD_TOK], zl[LD_TOK], vsum[LD_CH], bias[LD_CH];
+  __shared__ __attribute__((aligned(16))) float sl[LD_TOK], zl[LD_TOK], vsum[LD_CH], bias[LD_CH];
   const int s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
   const int d = a.d, ng = d / LG;
@@ -298,70 +298,107 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
   const uint8_t* bits_s = a.bits + (int64_t)s * ng;
   const LayerSlot k0 = layer_slot(bits_s, ng, 0);
   if (!k0.ok || k0.used > a.W) return;  // width table inconsistent with the record: write nothing
+  const int n_kept = k0.n_kept;
 
-  // bias = m V^T over all d coefficients: thread -> (channel tid >> 2, quarter tid & 3)
+  // per-thread shares of a slot's staging: basis row (channel tid >> 2) coefficients
+  // 16 (tid & 3) .. + 15; codes of tokens u_r = (tid + 512 r) & 127, coefficients
+  // 8 k8_r .. + 7 with k8_r = (tid + 512 r) >> 7 (uniform in a wavefront)
+  const int vc = tid >> 2, vq = tid & 3;
+  int64_t tbase[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int u = (tid + 512 * r) & (LD_TOK - 1);
+    tbase[r] = rec_word(sbase, a.t0 + (tok0 + u < a.n ? tok0 + u : a.n - 1), a.W, 0);
+  }
+  float vpre[16];
+  uint32_t wpre[2][3], mpre[2];
+  auto prefetch = [&](const LayerSlot& ks, int slot) {
+    const float* vr = Vs + (int64_t)(ch0 + vc) * d + LG * ks.grp + 16 * vq;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) vpre[i] = vr[i];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int k8 = (tid + 512 * r) >> 7;
+      const int P = 8 * k8 * ks.b, w0 = P >> 5, wl = (P + 8 * ks.b - 1) >> 5;  // payload words extract8 reads
+#pragma unroll
+      for (int i = 0; i < 3; ++i) wpre[r][i] = (w0 + i <= wl) ? a.packed[tbase[r] + (int64_t)(ks.pay + w0 + i) * TILE] : 0u;
+      mpre[r] = a.packed[tbase[r] + (int64_t)slot * TILE];
+    }
+  };
+
+  // bias = m V^T over all d coefficients: wavefront w takes channels 16w .. 16w + 15,
+  // each row read by the whole wavefront (16 values per lane), then a wavefront sum
   {
-    const int c = tid >> 2, q = tid & 3, span = d / 4;
-    const float* vr = Vs + (int64_t)(ch0 + c) * d + q * span;
-    const float* mr = a.mean + (int64_t)s * d + q * span;
-    float acc = 0.0f;
-    for (int j = 0; j < span; ++j) acc = __builtin_fmaf(mr[j], vr[j], acc);
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    if (q == 0) bias[c] = acc;
+    const float* mr = a.mean + (int64_t)s * d;
+    float mv[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mv[i] = (64 * i + lane < d) ? mr[64 * i + lane] : 0.0f;
+    float part[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const float* vr = Vs + (int64_t)(ch0 + 16 * wave + c) * d;
+      float acc = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (64 * i + lane < d) acc = __builtin_fmaf(mv[i], vr[64 * i + lane], acc);
+      part[c] = acc;
+    }
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      float v = part[c];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+      if (lane == c) bias[16 * wave + c] = v;
+    }
   }
 
   // wavefront -> channel block cb (32 channels), token blocks 2 tp, 2 tp + 1 (32 tokens each)
   const int cb = wave & 3, tp = wave >> 2;
   f32x16 out[2] = {f32x16{}, f32x16{}};
-  const int n_kept = k0.n_kept;
+  LayerSlot ks = k0;
+  if (n_kept > 0) prefetch(ks, 0);
   for (int slot = 0; slot < n_kept; ++slot) {
-    const LayerSlot ks = layer_slot(bits_s, ng, slot);
-    // codes of the group as bf16: thread -> (token e & 127, coefficients 8 (e >> 7) ..), two items
+    // stage the prefetched slot: codes as bf16 and metadata, basis parts and sums
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int e = tid + 512 * r, u = e & (LD_TOK - 1), k8 = e >> 7;
-      const int64_t t = a.t0 + (tok0 + u < a.n ? tok0 + u : a.n - 1);
-      const int64_t base = rec_word(sbase, t, a.W, 0);
+      const int w0 = (8 * k8 * ks.b) >> 5;
       with_bits(ks.b, [&](auto bc) {
         constexpr int B = decltype(bc)::value;
         uint32_t cd[8];
-        extract8<B>([&](int i) { return a.packed[base + (int64_t)(ks.pay + i) * TILE]; }, 8 * k8, cd);
+        extract8<B>([&](int i) { return wpre[r][i - w0]; }, 8 * k8, cd);
         *reinterpret_cast<u32x4*>(&cod[u][8 * k8]) =
             u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]), int_to_bf16_pair(cd[4], cd[5]),
                   int_to_bf16_pair(cd[6], cd[7])};
       });
       if (k8 == 0) {
-        const uint32_t m = a.packed[base + (int64_t)slot * TILE];
-        sl[u] = h2f(m);
-        zl[u] = h2f(m >> 16);
+        sl[u] = h2f(mpre[r]);
+        zl[u] = h2f(mpre[r] >> 16);
       }
     }
-    // basis columns of the group, three bf16 parts, and their sums: thread -> (channel tid >> 2, 16 coefficients)
     {
-      const int c = tid >> 2, q = tid & 3;
-      const float* vr = Vs + (int64_t)(ch0 + c) * d + LG * ks.grp + 16 * q;
-      float v[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) v[i] = vr[i];
       float sum = 0.0f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sum += v[i];
+      for (int i = 0; i < 16; ++i) sum += vpre[i];
       sum += __shfl_xor(sum, 1);
       sum += __shfl_xor(sum, 2);
-      if (q == 0) vsum[c] = sum;
+      if (vq == 0) vsum[vc] = sum;
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         uint32_t p0[8], p1[8], p2[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) split3(v[8 * half + i], p0[i], p1[i], p2[i]);
-        const int j = 16 * q + 8 * half;
-        *reinterpret_cast<u32x4*>(&vsl[0][c][j]) = u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])};
-        *reinterpret_cast<u32x4*>(&vsl[1][c][j]) = u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])};
-        *reinterpret_cast<u32x4*>(&vsl[2][c][j]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
+        for (int i = 0; i < 8; ++i) split3(vpre[8 * half + i], p0[i], p1[i], p2[i]);
+        const int j = 16 * vq + 8 * half;
+        *reinterpret_cast<u32x4*>(&vsl[0][vc][j]) = u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])};
+        *reinterpret_cast<u32x4*>(&vsl[1][vc][j]) = u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])};
+        *reinterpret_cast<u32x4*>(&vsl[2][vc][j]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
       }
     }
     __syncthreads();
+    if (slot + 1 < n_kept) {
+      ks = layer_slot(bits_s, ng, slot + 1);
+      prefetch(ks, slot + 1);
+    }
     // D[channel][token] = sum_j V[channel][j] q[token][j] for this group
     f32x16 g[2] = {f32x16{}, f32x16{}};
 #pragma unroll
@@ -381,9 +418,10 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
       const int u = 64 * tp + 32 * tb + col;
       const float st = sl[u], zt = zl[u];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int row = 4 * h + (i & 3) + 8 * (i >> 2);
-        out[tb][i] += st * g[tb][i] + zt * vsum[32 * cb + row];
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 vs4 = *reinterpret_cast<const f32x4*>(&vsum[32 * cb + 4 * h + 8 * q]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) out[tb][4 * q + j] += st * g[tb][4 * q + j] + zt * vs4[j];
       }
     }
     __syncthreads();
