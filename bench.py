@@ -45,9 +45,9 @@ DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "enco
                        "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "b9f6b8d34df74539f80ce511cdfd029384db6b10edf384cc3c7ffe5576ae1b9b": {
-        "fetch_bytes": 74550682, "write_bytes": 1674240,
-        "per_kernel": {"attn_kernel<1,8,8,true>": [70710682, 1657856], "combine_kernel": [3840000, 16384]}},
+    "dfce811c5237b2c556736516433317251562ec403fd53a11520edf9d65fdd320": {
+        "fetch_bytes": 74540646, "write_bytes": 1674240,
+        "per_kernel": {"attn_kernel<1,8,8,true>": [70700646, 1657856], "combine_kernel": [3840000, 16384]}},
 }
 
 
@@ -188,6 +188,7 @@ def fit_weights_bench(args):
 def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_rec, qs, ws, Wk, Wv, H, Hq, d, dev):
     """Timings outside the step on layer 0: Mode A reconstruction of the keys to fp32,
     and attention with rotary embeddings (keys reconstructed and rotated)."""
+    import synth
     dec_out = torch.empty((H, n_rec, d), dtype=torch.float32, device=dev)
     dec_ev = []
     for _ in range(4):
@@ -215,7 +216,39 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
     rope_ms = min(e0.elapsed_time(e1) for e0, e1 in rope_ev[1:])
     rope_bytes = algorithmic_bytes(w, Wk, Wv, n_rec)["attn_call"]
 
+    # ---- per-layer cross-head latent (outside the step): the keys of one layer as one
+    # d_kv = 8 x 128 stream, groups of 64, fitted on its first 8192 tokens ----
+    dl = H * d
+    pl = S.Params(head_dim=dl, group_size=64, ratio=w.ratio)
+    xl = synth.device_layer_stream(w, 0, 0, 0, n_rec, dev)
+    cl = S.Codec(pl, 1)
+    S.spectra_fit_basis(cl, xl[:, :8192])
+    pkl = cl.empty_packed(t_cap)
+    outl = torch.empty((1, n_rec, dl), dtype=torch.float32, device=dev)
+    lay_ev = []
+    for _ in range(4):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record()
+        S.spectra_encode(cl, xl, 0, pkl, t_cap)
+        e[1].record()
+        S.spectra_decode(cl, pkl, t_cap, 0, n_rec, out=outl)
+        e[2].record()
+        lay_ev.append(e)
+    torch.cuda.synchronize()
+    lenc_ms = min(e[0].elapsed_time(e[1]) for e in lay_ev[1:])
+    ldec_ms = min(e[1].elapsed_time(e[2]) for e in lay_ev[1:])
+    Wl = cl.record_words
+    lenc_bytes = n_rec * dl * 2 + n_rec * Wl * 4 + dl * dl * 4 + dl * 4
+    ldec_bytes = n_rec * Wl * 4 + n_rec * dl * 4 + dl * dl * 4 + dl * 4
+    kept = int((cl.bits[0] > 0).sum().item())
+    del xl, pkl, outl, cl
+
     return {
+        "layer_latent": {"d": dl, "group_size": 64, "record_words": Wl, "kept_groups": kept, "tokens": n_rec,
+                         "encode_ms": round(lenc_ms, 4), "encode_GBps": round(lenc_bytes / (lenc_ms * 1e-3) / 1e9, 1),
+                         "decode_ms": round(ldec_ms, 4), "decode_GBps": round(ldec_bytes / (ldec_ms * 1e-3) / 1e9, 1),
+                         "what": "per-layer cross-head latent: spectra_encode and spectra_decode of one layer's keys "
+                                 "as one d_kv stream, outside the step"},
         "mode_a_rope_attention": {"us_per_layer_call": round(rope_ms * 1e3, 1),
                                   "GBps": round(rope_bytes / (rope_ms * 1e-3) / 1e9, 1),
                                   "what": "spectra_decode_attention_rope (keys reconstructed and rotated) over one "

@@ -227,3 +227,29 @@ def numpy_layer_stream(w: Workload, seq: int, layer: int, tensor: int, n_tokens:
     z = rng.standard_normal((n_tokens, shared_rank))
     x = (x + z @ u.T).astype(np.float32)
     return x if w.dtype == "f32" else f32_to_bf16_bits(x)
+
+
+def device_layer_stream(w: Workload, seq: int, layer: int, tensor: int, n_tokens: int, device, seed: int = 0,
+                        shared_rank: int = 16, shared_frac: float = 0.3):
+    """Per-layer stream of ``numpy_layer_stream``'s distribution drawn on the GPU:
+    [1, T, n_kv_heads * 128] in the workload dtype. The heads come from
+    ``device_streams`` (sequence ``seq``), U from the same numpy rng as the numpy
+    backend, Z from a torch generator; values differ from the numpy backend's."""
+    import torch
+    heads = device_streams(w, tensor, layer, n_tokens, device, seed=seed)[seq * w.n_kv_heads:(seq + 1) * w.n_kv_heads]
+    x = heads.permute(1, 0, 2).reshape(n_tokens, -1).float()
+    del heads
+    d_kv = x.shape[1]
+    rng = np.random.default_rng([seed, w.wid, seq, layer, 1000 + tensor])
+    u = rng.standard_normal((d_kv, shared_rank))
+    energy = float((x[: min(n_tokens, 8192)] ** 2).mean())
+    u_t = torch.from_numpy((u * math.sqrt(shared_frac * energy / shared_rank)).astype(np.float32)).to(device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(((seed * 1000003 + w.wid) * 1000003 + layer) * 4 + tensor + 7919)
+    step = 16384
+    for t0 in range(0, n_tokens, step):
+        t1 = min(n_tokens, t0 + step)
+        z = torch.randn((t1 - t0, shared_rank), generator=gen, device=device, dtype=torch.float32)
+        x[t0:t1] += z @ u_t.T
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    return x.to(dt).unsqueeze(0)
