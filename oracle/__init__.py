@@ -11,7 +11,7 @@ mathematics fixes (closed forms, identities, brute force, hand-built records).
 """
 from .codec import (  # noqa: F401
     Params, FitResult, record_budget_bits, record_words, split_budget,
-    fit, fit_from_weights, allocate_bits, allocate_bits_bruteforce,
+    fit, fit_from_weights, latent_scale_factors, allocate_bits, allocate_bits_bruteforce,
     quantize, quantize_given_meta, dequantize, pack, unpack, physical_index, encode, decode,
     attention_mode_a, attention_mode_a_rope, rope, attention_mode_b, softmax_f64, fp16_rne_sat, fp16_bits,
     f16_bits_to_f64,

@@ -23,7 +23,7 @@ from __future__ import annotations
 import math
 from dataclasses import dataclass, replace
 from itertools import product
-from typing import List, Sequence, Tuple
+from typing import Optional, List, Sequence, Tuple
 
 import numpy as np
 
@@ -116,9 +116,10 @@ class FitResult:
     second_moment: np.ndarray  # [d, d] float64, the matrix that was diagonalised
     mu: np.ndarray        # [d] float64 token mean
     cov: np.ndarray       # [d, d] float64 centered covariance
+    scale: Optional[np.ndarray] = None  # [d] float32 square-root split factors f_j (None: orthonormal latent)
 
 
-def fit(x: np.ndarray, p: Params) -> FitResult:
+def fit(x: np.ndarray, p: Params, latent_scale: bool = False) -> FitResult:
     """Per-stream spectral basis.
 
     Sec. 3.1 builds the latent from the G-weighted SVD M = G^{1/2} W = U S V^T.
@@ -143,10 +144,10 @@ def fit(x: np.ndarray, p: Params) -> FitResult:
     assert d == p.head_dim and T > 0
     mu = x.sum(axis=0) / T
     S = (x.T @ x) / T
-    return _fit_from_moments(S, mu, p)
+    return _fit_from_moments(S, mu, p, latent_scale)
 
 
-def fit_from_weights(W: np.ndarray, G: np.ndarray, hbar, p: Params) -> FitResult:
+def fit_from_weights(W: np.ndarray, G: np.ndarray, hbar, p: Params, latent_scale: bool = False) -> FitResult:
     """Calibrate-once basis from a head's projection and its layer's input statistics
     (Sec. 3.1, Eqs. gweighted and gsvd; App. B).
 
@@ -162,11 +163,20 @@ def fit_from_weights(W: np.ndarray, G: np.ndarray, hbar, p: Params) -> FitResult
     assert W.shape[1] == p.head_dim and G.shape == (W.shape[0], W.shape[0])
     S = W.T @ G @ W
     mu = np.zeros(p.head_dim) if hbar is None else np.asarray(hbar, dtype=np.float64) @ W
-    return _fit_from_moments(S, mu, p)
+    return _fit_from_moments(S, mu, p, latent_scale)
 
 
-def _fit_from_moments(S: np.ndarray, mu: np.ndarray, p: Params) -> FitResult:
-    """Steps of ``fit`` after the moments: second moment S and mean mu, fp64."""
+def _fit_from_moments(S: np.ndarray, mu: np.ndarray, p: Params, latent_scale: bool = False) -> FitResult:
+    """Steps of ``fit`` after the moments: second moment S and mean mu, fp64.
+
+    latent_scale: the square-root split of Eq. gsvd. With M = G^{1/2} W = U Sig V^T the
+    cached latent is h G^{-1/2} U Sig^{1/2} = (k V) Sig^{-1/2}, and Sig = diag(sqrt(lambda))
+    for the eigenvalues lambda of E[k^T k]; so coordinate j of the orthonormal latent is
+    multiplied by f_j = lambda_j^{-1/4}, which makes E[c^T c] = diag(sqrt(lambda)) (Eq.
+    second-moment-latent). Reading: lambda_j is floored at lambda_0 2^-40 (a rank-deficient
+    fit would otherwise scale noise without bound); the allocation receives the centered
+    variances of the scaled coordinates, the quantities that are cached.
+    """
     d = p.head_dim
     C = S - np.outer(mu, mu)
     M = C if p.centered else S
@@ -183,7 +193,19 @@ def _fit_from_moments(S: np.ndarray, mu: np.ndarray, p: Params) -> FitResult:
     V64 = V32.astype(np.float64)
     m = (mu @ V64).astype(np.float32)
     var = np.einsum("ij,ik,kj->j", V64, C, V64)
-    return FitResult(V32, m, var, lam, M, mu, C)
+    if not latent_scale:
+        return FitResult(V32, m, var, lam, M, mu, C)
+    f = latent_scale_factors(lam)
+    f64 = f.astype(np.float64)
+    return FitResult(V32, m, var * f64 * f64, lam, M, mu, C, f)
+
+
+def latent_scale_factors(lam: np.ndarray) -> np.ndarray:
+    """f_j = max(lambda_j, lambda_0 2^-40)^(-1/4) as fp32 (1 where lambda_0 <= 0)."""
+    lam = np.asarray(lam, dtype=np.float64)
+    if lam[0] <= 0:
+        return np.ones(lam.shape, np.float32)
+    return (np.maximum(lam, lam[0] * 2.0 ** -40) ** -0.25).astype(np.float32)
 
 
 # ----------------------------------------------------------------------------
@@ -441,18 +463,25 @@ def physical_index(stream: int, t: np.ndarray, w: int, t_capacity: int, W: int) 
 # ----------------------------------------------------------------------------
 # Encode / decode (Sec. 3.1-3.3, Mode A)
 # ----------------------------------------------------------------------------
-def encode(x: np.ndarray, basis32: np.ndarray, mean32: np.ndarray, bits: Sequence[int], p: Params):
-    """Project (c = x V32 - m, fp64), quantize and pack: returns (records, codes, meta, coef)."""
+def encode(x: np.ndarray, basis32: np.ndarray, mean32: np.ndarray, bits: Sequence[int], p: Params, scale32=None):
+    """Project (c = x V32 - m, fp64; times f_j under the square-root split), quantize and
+    pack: returns (records, codes, meta, coef)."""
     x = np.asarray(x, dtype=np.float64)
     coef = x @ np.asarray(basis32, dtype=np.float64) - np.asarray(mean32, dtype=np.float64)[None, :]
+    if scale32 is not None:
+        coef = coef * np.asarray(scale32, dtype=np.float64)[None, :]
     codes, meta = quantize(coef, bits, p)
     return pack(codes, meta, bits, p), codes, meta, coef
 
 
-def decode(rec: np.ndarray, basis32: np.ndarray, mean32: np.ndarray, bits: Sequence[int], p: Params) -> np.ndarray:
-    """Mode A reconstruction x_hat = (c_hat + m) V32^T in fp64 (Sec. 3.3)."""
+def decode(rec: np.ndarray, basis32: np.ndarray, mean32: np.ndarray, bits: Sequence[int], p: Params,
+           scale32=None) -> np.ndarray:
+    """Mode A reconstruction x_hat = (c_hat + m) V32^T in fp64 (Sec. 3.3); under the
+    square-root split c_hat / f_j takes the place of c_hat."""
     codes, meta = unpack(rec, bits, p)
     c_hat = dequantize(codes, meta, bits, p)
+    if scale32 is not None:
+        c_hat = c_hat / np.asarray(scale32, dtype=np.float64)[None, :]
     return (c_hat + np.asarray(mean32, np.float64)[None, :]) @ np.asarray(basis32, np.float64).T
 
 

@@ -105,3 +105,69 @@ def test_layer_capacity_at_8x():
     used = sum(1 + 2 * b for b in bits if b > 0)
     assert used <= 64
     assert bits == sorted(bits, reverse=True)
+
+
+# ---------------------------------------------------------------------------
+# Square-root latent scaling (Eqs. gsvd and second-moment-latent)
+# ---------------------------------------------------------------------------
+def test_square_root_split_matches_the_whitened_weight_svd():
+    # The paper's latent c = h W_down with W_down = G^{-1/2} U_r S_r^{1/2} and
+    # M = G^{1/2} W = U S V^T, formed here with numpy's SVD and eigh; the oracle's
+    # scaled latent (h W V) * f must equal it up to the sign of each column.
+    rng = np.random.default_rng(5)
+    dm, d, T = 96, 64, 4000
+    A = rng.standard_normal((dm, dm)) * (np.arange(1, dm + 1) ** -0.7)[None, :]
+    G = A @ A.T / dm + 1e-3 * np.eye(dm)
+    W = rng.standard_normal((dm, d)) / np.sqrt(dm)
+    gw, gv = np.linalg.eigh(G)
+    Gh = (gv * np.sqrt(gw)) @ gv.T
+    Gmh = (gv / np.sqrt(gw)) @ gv.T
+    U, Sg, Vt = np.linalg.svd(Gh @ W, full_matrices=False)
+    W_down = Gmh @ U * np.sqrt(Sg)[None, :]
+    h = rng.standard_normal((T, dm)) @ Gh            # E[h^T h] = G
+    c_paper = h @ W_down
+    p = O.Params(head_dim=d, group_size=16)
+    f = O.fit_from_weights(W, G, None, p, latent_scale=True)
+    c_or = (h @ W @ f.basis.astype(np.float64)) * f.scale.astype(np.float64)[None, :]
+    sign = np.sign(np.sum(c_or * c_paper, axis=0))
+    assert np.all(sign != 0)
+    assert np.abs(c_or * sign[None, :] - c_paper).max() <= 1e-5 * np.abs(c_paper).max()
+    # and the split's energies are the singular values of M
+    assert np.allclose(f.scale.astype(np.float64) ** -2, Sg, rtol=1e-6)
+
+
+def test_scaled_latent_second_moment_is_the_singular_values():
+    # Eq. second-moment-latent: E[c^T c] = S (diagonal, descending) for the scaled latent,
+    # S the singular values of the data matrix / sqrt(T) taken from numpy's SVD.
+    w = synth.WORKLOADS["qwen_layer_8x"]
+    x = synth.bf16_bits_to_f32(synth.numpy_layer_stream(w, 0, 0, 1, 3000)).astype(np.float64)
+    d = x.shape[1]
+    p = O.Params(head_dim=d, group_size=64)
+    f = O.fit(x, p, latent_scale=True)
+    sv = np.linalg.svd(x / np.sqrt(x.shape[0]), compute_uv=False)
+    c = (x @ f.basis.astype(np.float64)) * f.scale.astype(np.float64)[None, :]
+    Mc = c.T @ c / x.shape[0]
+    keep = sv > sv[0] * 1e-3
+    assert np.allclose(np.diag(Mc)[keep], sv[keep], rtol=1e-4)
+    off = Mc - np.diag(np.diag(Mc))
+    assert np.abs(off).max() <= 1e-5 * sv[0]
+
+
+def test_scaled_fit_same_reconstruction_flatter_allocation():
+    # Any split gives the same reconstruction (Sec. 3.1): at 8 bits per group the scaled
+    # and orthonormal codecs both reconstruct to quantization accuracy; the scaled latent's
+    # variances are sqrt(lambda)-like, so its allocation spreads bits over more groups.
+    w = synth.WORKLOADS["qwen_layer_8x"]
+    x = synth.bf16_bits_to_f32(synth.numpy_layer_stream(w, 0, 0, 0, 2048)).astype(np.float64)
+    d = x.shape[1]
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    fo, fs = O.fit(x, p), O.fit(x, p, latent_scale=True)
+    assert np.array_equal(fo.basis, fs.basis) and np.array_equal(fo.mean, fs.mean)
+    bo, bs = O.allocate_bits(fo.var, p), O.allocate_bits(fs.var, p)
+    assert sum(b > 0 for b in bs) >= sum(b > 0 for b in bo)
+    p8 = O.Params(head_dim=d, group_size=64, budget_bits=d * 8 + 32 * (d // 64))
+    full = [8] * (d // 64)
+    for f in (fo, fs):
+        rec, *_ = O.encode(x[:256], f.basis, f.mean, full, p8, f.scale)
+        xr = O.decode(rec, f.basis, f.mean, full, p8, f.scale)
+        assert np.linalg.norm(xr - x[:256]) <= 2e-2 * np.linalg.norm(x[:256])
