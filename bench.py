@@ -45,7 +45,7 @@ DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "enco
                        "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "dfce811c5237b2c556736516433317251562ec403fd53a11520edf9d65fdd320": {
+    "b9f6b8d34df74539f80ce511cdfd029384db6b10edf384cc3c7ffe5576ae1b9b": {
         "fetch_bytes": 74540646, "write_bytes": 1674240,
         "per_kernel": {"attn_kernel<1,8,8,true>": [70700646, 1657856], "combine_kernel": [3840000, 16384]}},
 }

@@ -101,6 +101,12 @@ typedef struct {
   float* mean;          /* device [n_streams][d] fp32: coefficient-space mean m = mean_t(x_t) V */
   float* var;           /* device [n_streams][d] fp32: centered marginal variance of coefficient j */
   uint8_t* bits;        /* device [n_streams][d/g]: group code widths (0 = dropped) */
+  float* lscale;        /* device [n_streams][d] fp32, or NULL: square-root split of the latent
+                           (Eq. gsvd; per-layer geometry only). When set, the fit writes
+                           f_j = max(lambda_j, lambda_0 2^-40)^(-1/4) (lambda the descending
+                           eigenvalues), var holds the scaled coordinates' variances v_j f_j^2
+                           and the widths are allocated on them; encode caches (x V - m)_j f_j
+                           and decode reconstructs (c_hat / f + m) V^T. */
 } spectra_codec;
 
 /* Validates p, fills c->p, c->n_streams and c->record_words. Host only. */

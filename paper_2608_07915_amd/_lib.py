@@ -30,7 +30,7 @@ class spectra_params(ctypes.Structure):
 class spectra_codec(ctypes.Structure):
     _fields_ = [("p", spectra_params), ("n_streams", ctypes.c_int64), ("record_words", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("basis", ctypes.c_void_p), ("mean", ctypes.c_void_p),
-                ("var", ctypes.c_void_p), ("bits", ctypes.c_void_p)]
+                ("var", ctypes.c_void_p), ("bits", ctypes.c_void_p), ("lscale", ctypes.c_void_p)]
 
 
 _P = ctypes.c_void_p

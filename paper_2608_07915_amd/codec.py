@@ -97,7 +97,9 @@ def _stream(stream=None):
 class Codec:
     """Per-stream codec state (basis, mean, variances, group widths) in device memory."""
 
-    def __init__(self, params: Params, n_streams: int, device="cuda", _views=None):
+    def __init__(self, params: Params, n_streams: int, device="cuda", _views=None, latent_scale: bool = False):
+        """latent_scale: cache the square-root split of the latent (Eq. gsvd; per-layer
+        geometry only): the fit then also writes ``lscale`` [n_streams, d]."""
         import torch
         self.params = params
         self.n_streams = int(n_streams)
@@ -107,14 +109,16 @@ class Codec:
             self.mean = torch.zeros((n_streams, d), dtype=torch.float32, device=device)
             self.var = torch.zeros((n_streams, d), dtype=torch.float32, device=device)
             self.bits = torch.zeros((n_streams, nG), dtype=torch.uint8, device=device)
+            self.lscale = torch.ones((n_streams, d), dtype=torch.float32, device=device) if latent_scale else None
         else:
-            self.basis, self.mean, self.var, self.bits = _views
+            self.basis, self.mean, self.var, self.bits, self.lscale = _views
         self.struct = spectra_codec()
         check(_lib.get().spectra_codec_init(ctypes.byref(self.struct), ctypes.byref(params.c()), self.n_streams))
         self.struct.basis = self.basis.data_ptr()
         self.struct.mean = self.mean.data_ptr()
         self.struct.var = self.var.data_ptr()
         self.struct.bits = self.bits.data_ptr()
+        self.struct.lscale = self.lscale.data_ptr() if self.lscale is not None else None
 
     @property
     def record_words(self) -> int:
@@ -123,7 +127,8 @@ class Codec:
     def view(self, start: int, count: int) -> "Codec":
         """Codec over streams [start, start + count) sharing this codec's memory."""
         sl = slice(start, start + count)
-        return Codec(self.params, count, _views=(self.basis[sl], self.mean[sl], self.var[sl], self.bits[sl]))
+        return Codec(self.params, count, _views=(self.basis[sl], self.mean[sl], self.var[sl], self.bits[sl],
+                                                 self.lscale[sl] if self.lscale is not None else None))
 
     def packed_words(self, t_capacity: int) -> int:
         return int(_lib.get().spectra_packed_words(ctypes.byref(self.struct), int(t_capacity)))

@@ -9,6 +9,7 @@
 
 #include "host_common.hpp"
 #include "kernels.hpp"
+#include "layer.hpp"
 
 using namespace spectra;
 using spectra_dev::AttnArgs;
@@ -41,6 +42,9 @@ spectra_status check_codec(const spectra_codec* c, const char* name, bool layer_
   if (c->n_streams <= 0 || c->n_streams > 65535)
     return fail(SPECTRA_EINVAL, "%s: n_streams=%lld out of range [1, 65535]", name, (long long)c->n_streams);
   if (!c->basis || !c->mean || !c->var || !c->bits) return fail(SPECTRA_EINVAL, "%s: null codec array", name);
+  if (c->lscale && !layer_geometry(c->p))
+    return fail(SPECTRA_EUNSUPPORTED, "%s: the square-root latent split (lscale) runs in the per-layer geometry only", name);
+  if (c->lscale && !aligned(c->lscale, 4)) return fail(SPECTRA_EINVAL, "%s: lscale must be 4-byte aligned", name);
   if (!aligned(c->basis, 16) || !aligned(c->mean, 4) || !aligned(c->var, 4) || !aligned(c->bits, 4))
     return fail(SPECTRA_EINVAL, "%s: basis must be 16-byte aligned, the other codec arrays 4-byte aligned", name);
   return SPECTRA_OK;
@@ -104,6 +108,7 @@ spectra_status finish_fit(spectra_codec* c, const std::vector<double>& mom, int6
   hipError_t e = hipSuccess;
   std::vector<float> basis((size_t)S * d * d), mean((size_t)S * d), var32((size_t)S * d);
   std::vector<double> var((size_t)S * d);
+  std::vector<float> scale(c->lscale ? (size_t)S * d : 0);
   const int nG = d / c->p.group_size;
   std::vector<uint8_t> bits((size_t)S * nG);
   std::vector<spectra_status> res((size_t)S, SPECTRA_OK);
@@ -115,7 +120,8 @@ spectra_status finish_fit(spectra_codec* c, const std::vector<double>& mom, int6
       for (int64_t s = w; s < S; s += nthreads) {
         const double* m = &mom[(size_t)(s * mstride)];
         res[(size_t)s] = fit_from_moments(c->p, n_tokens, m, m + (size_t)d * d, &basis[(size_t)s * d * d], &mean[(size_t)s * d],
-                                          &var[(size_t)s * d], &bits[(size_t)s * nG]);
+                                          &var[(size_t)s * d], &bits[(size_t)s * nG],
+                                          c->lscale ? &scale[(size_t)s * d] : nullptr);
         if (res[(size_t)s] != SPECTRA_OK) msgs[(size_t)s] = spectra_last_error();
       }
     });
@@ -128,6 +134,8 @@ spectra_status finish_fit(spectra_codec* c, const std::vector<double>& mom, int6
   if (e == hipSuccess) e = hipMemcpyAsync(c->mean, mean.data(), mean.size() * sizeof(float), hipMemcpyHostToDevice, hs);
   if (e == hipSuccess) e = hipMemcpyAsync(c->var, var32.data(), var32.size() * sizeof(float), hipMemcpyHostToDevice, hs);
   if (e == hipSuccess) e = hipMemcpyAsync(c->bits, bits.data(), bits.size(), hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && c->lscale)
+    e = hipMemcpyAsync(c->lscale, scale.data(), scale.size() * sizeof(float), hipMemcpyHostToDevice, hs);
   if (e == hipSuccess) e = hipStreamSynchronize(hs);
   if (e != hipSuccess) return hip_fail(e, "fit result copy");
   return SPECTRA_OK;
@@ -265,6 +273,7 @@ spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dty
     a.W = c->record_words;
     a.d = c->p.head_dim;
     a.n_streams = (int32_t)c->n_streams;
+    a.lscale = c->lscale;
     hipError_t e = launch_layer_encode(a, (hipStream_t)stream);
     return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "encode launch");
   }
@@ -309,6 +318,7 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
     a.W = c->record_words;
     a.d = c->p.head_dim;
     a.n_streams = (int32_t)c->n_streams;
+    a.lscale = c->lscale;
     hipError_t e = launch_layer_decode(a, (hipStream_t)stream);
     return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "decode launch");
   }

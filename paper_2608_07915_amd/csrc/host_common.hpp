@@ -31,8 +31,9 @@ spectra_status allocate_bits(const double* var, const spectra_params& p, uint8_t
 spectra_status eigh_sym(const double* a, int n, double* w, double* v);
 
 // Fit of one stream from its moments.
+// scale: NULL, or the square-root split factors f_j to write (var then holds v_j f_j^2).
 spectra_status fit_from_moments(const spectra_params& p, int64_t n_tokens, const double* gram,
                                 const double* colsum, float* basis, float* mean, double* var,
-                                uint8_t* bits);
+                                uint8_t* bits, float* scale = nullptr);
 
 }  // namespace spectra

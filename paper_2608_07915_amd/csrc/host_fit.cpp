@@ -1,5 +1,6 @@
 // Fit of one stream from its first and second moments (Sec. 3.1), plus the
 // parameter checks, error reporting and the C entry points that need no GPU.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -67,7 +68,7 @@ spectra_status check_params_gpu(const spectra_params& p) {
 
 spectra_status fit_from_moments(const spectra_params& p, int64_t n_tokens, const double* gram,
                                 const double* colsum, float* basis, float* mean, double* var,
-                                uint8_t* bits) {
+                                uint8_t* bits, float* scale) {
   const int d = p.head_dim;
   if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "fit needs at least one token");
   const double invT = 1.0 / (double)n_tokens;
@@ -105,6 +106,16 @@ spectra_status fit_from_moments(const spectra_params& p, int64_t n_tokens, const
     double vj = 0.0;
     for (int i = 0; i < d; ++i) vj += V32[(size_t)i * d + j] * Cv[i];
     var[j] = vj;
+  }
+  if (scale) {
+    // Eq. gsvd, square-root split: coordinate j of the orthonormal latent times
+    // lambda_j^(-1/4) (lambda floored at lambda_0 2^-40); widths from the scaled variances
+    const double floor_l = w[0] > 0.0 ? w[0] * std::ldexp(1.0, -40) : 0.0;
+    for (int j = 0; j < d; ++j) {
+      scale[j] = w[0] > 0.0 ? (float)std::pow(std::max(w[j], floor_l), -0.25) : 1.0f;
+      const double f = (double)scale[j];
+      var[j] *= f * f;
+    }
   }
   return allocate_bits(var, p, bits);
 }

@@ -52,40 +52,6 @@ struct GramArgs {
   double* moments;  // [n_streams][128*128 + 128]
 };
 
-// Per-layer geometry (d = n_kv_heads x 128 in [256, 1024], groups of 64)
-struct LayerGramArgs {
-  const void* x;
-  int64_t stream_stride, token_stride, n;
-  int64_t chunk_tokens;
-  int32_t k_split;
-  int32_t n_streams;
-  int32_t d;
-  double* partial;  // [n_streams][k_split][d*d]
-  double* moments;  // [n_streams][d*d + d]
-};
-
-struct LayerEncodeArgs {
-  const void* x;  // bf16
-  int64_t stream_stride, token_stride;
-  int64_t t0, n;
-  const float* basis;
-  const float* mean;
-  const uint8_t* bits;
-  uint32_t* packed;
-  int64_t t_cap;
-  int32_t W, d, n_streams;
-};
-
-struct LayerDecodeArgs {
-  const uint32_t* packed;
-  int64_t t_cap, t0, n;
-  const float* basis;
-  const float* mean;
-  const uint8_t* bits;
-  float* out;  // [n_streams][n][d]
-  int32_t W, d, n_streams;
-};
-
 struct AttnArgs {
   const uint32_t* packed_k;
   const uint32_t* packed_v;
@@ -151,11 +117,6 @@ int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_token
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
-// Per-layer geometry
-void layer_gram_layout(int32_t d, int64_t n_streams, int64_t n_tokens, int32_t* k_split, int64_t* chunk_tokens);
-hipError_t launch_layer_moments(const spectra_dev::LayerGramArgs& g, bool f32_in, hipStream_t st);
-hipError_t launch_layer_encode(const spectra_dev::LayerEncodeArgs& a, hipStream_t st);
-hipError_t launch_layer_decode(const spectra_dev::LayerDecodeArgs& a, hipStream_t st);
 // moments[s] = [W_s^T G W_s, hbar W_s] for W [n_streams][d_model][128] fp32 and per-layer
 // G [layers][d_model][d_model], hbar [layers][d_model] fp64 (layer = s / streams_per_layer);
 // scratch: n_streams * d_model * 128 doubles.

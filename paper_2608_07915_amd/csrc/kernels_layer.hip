@@ -19,6 +19,7 @@
 //                         (128 tokens, 128 channels, stream).
 #include "device_common.hpp"
 #include "kernels.hpp"
+#include "layer.hpp"
 
 namespace spectra_dev {
 
@@ -246,6 +247,14 @@ __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
     c[i] = (acc0[i] + sm0[i]) - mg[16 * h + i];
     c[16 + i] = (acc1[i] + sm1[i]) - mg[32 + 16 * h + i];
   }
+  if (a.lscale) {  // square-root split: the cached coordinate is (x V - m)_j f_j
+    const float* fg = a.lscale + (int64_t)s * d + LG * ks.grp;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      c[i] *= fg[16 * h + i];
+      c[16 + i] *= fg[32 + 16 * h + i];
+    }
+  }
   float lo = c[0], hi = c[0];
 #pragma unroll
   for (int i = 1; i < 32; ++i) {
@@ -310,12 +319,17 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
     const int u = (tid + 512 * r) & (LD_TOK - 1);
     tbase[r] = rec_word(sbase, a.t0 + (tok0 + u < a.n ? tok0 + u : a.n - 1), a.W, 0);
   }
-  float vpre[16];
+  float vpre[16], upre[16];
   uint32_t wpre[2][3], mpre[2];
   auto prefetch = [&](const LayerSlot& ks, int slot) {
     const float* vr = Vs + (int64_t)(ch0 + vc) * d + LG * ks.grp + 16 * vq;
 #pragma unroll
     for (int i = 0; i < 16; ++i) vpre[i] = vr[i];
+    if (a.lscale) {
+      const float* fr = a.lscale + (int64_t)s * d + LG * ks.grp + 16 * vq;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) upre[i] = fr[i];
+    }
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int k8 = (tid + 512 * r) >> 7;
@@ -377,6 +391,10 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
       }
     }
     {
+      if (a.lscale) {  // square-root split: c_hat_j / f_j, folded into the basis columns
+#pragma unroll
+        for (int i = 0; i < 16; ++i) vpre[i] = vpre[i] * (1.0f / upre[i]);
+      }
       float sum = 0.0f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) sum += vpre[i];

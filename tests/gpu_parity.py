@@ -83,15 +83,18 @@ def _fp16_boundary_ok(pre: np.ndarray, got_bits: np.ndarray, want_bits: np.ndarr
 
 
 def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gpu: np.ndarray,
-                         dot_bound: bool = False) -> EncodeReport:
+                         dot_bound: bool = False, scale=None) -> EncodeReport:
     """P3-P5 for one stream: x64 [n, d] input values, rec_gpu [n, W] GPU records.
 
     dot_bound (long projections, d > 128): a code may differ only where the oracle's
     u = (c - z)/s lies within the forward error bound of the GPU's fp32 projection of
     a half-integer: |dc| <= n_r 2^-24 sum_k |x_k V_kj| + 2^-23 |c| (n_r = d/16 + 16
-    sequential roundings: 16-term MFMA steps chained over d, then the chunk adds)."""
+    sequential roundings: 16-term MFMA steps chained over d, then the chunk adds).
+    scale: the square-root split factors f_j (the cached coordinate is (x V - m)_j f_j)."""
     W = O.record_words(p)
     coef = x64 @ basis.astype(np.float64) - mean.astype(np.float64)[None, :]
+    fs = np.ones(coef.shape[1]) if scale is None else np.asarray(scale, np.float64)
+    coef = coef * fs[None, :]
     codes_o, meta_o = O.quantize(coef, bits, p)
     codes_g, meta_g = O.unpack(rec_gpu, bits, p)
     # P5: re-packing the GPU's codes and metadata reproduces its words exactly
@@ -132,7 +135,7 @@ def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gp
             for G, b in enumerate(bits):
                 if b:
                     s_tok[:, G * g:(G + 1) * g] = O.f16_bits_to_f64(meta_g[:, G] & 0xFFFF)[:, None]
-            dc = (d / 16 + 16) * 2.0 ** -24 * A + 2.0 ** -23 * np.abs(coef)
+            dc = (d / 16 + 16) * 2.0 ** -24 * A * fs[None, :] + 2.0 ** -22 * np.abs(coef)
             bound = (dc[:, kept] / np.where(s_tok[:, kept] > 0, s_tok[:, kept], np.inf))[mism] + 1e-6
             assert np.all(np.abs(uu - np.floor(uu) - 0.5) <= bound), "code mismatch outside the fp32 projection bound"
         else:

@@ -144,3 +144,37 @@ def test_layer_rejects_what_it_does_not_run():
     q = torch.zeros((1, 28, d), dtype=torch.float32, device="cuda")
     with pytest.raises((S.SpectraError, ValueError)):
         S.spectra_decode_attention(codec, codec, packed, packed, t_cap, 128, q, 1)
+
+
+@pytest.mark.parametrize("name,ratio", [("qwen_layer_8x", 8.0), ("llama_layer_4x", 12.0)])
+def test_layer_square_root_split(name, ratio):
+    # Eq. gsvd's square-root split of the latent: factors, widths, records and
+    # reconstruction against the oracle's scaled codec
+    w, xf = _layers(name, 1, T_FIT)
+    T = 500
+    x = np.ascontiguousarray(xf[:, :T])
+    d = x.shape[2]
+    p = O.Params(head_dim=d, group_size=64, ratio=ratio)
+    codec = S.Codec(sparams(p), 1, latent_scale=True)
+    S.spectra_fit_basis(codec, to_device(xf, w.dtype))
+    basis, mean, bits = codec_state(codec, 0)
+    f_gpu = codec.lscale[0].cpu().numpy()
+    fo = O.fit(values_f64(xf[0], w.dtype), p, latent_scale=True)
+    assert np.allclose(f_gpu, fo.scale, rtol=2e-5)
+    assert bits == O.allocate_bits(fo.var, p)
+    t_cap = 576
+    packed = codec.empty_packed(t_cap)
+    x_dev = to_device(x, w.dtype)
+    S.spectra_encode(codec, x_dev, 0, packed, t_cap)
+    dec = S.spectra_decode(codec, packed, t_cap, 0, T).cpu().numpy()[0]
+    rec = records_of(packed, 0, 0, T, t_cap, O.record_words(p))
+    xs = values_f64(x[0], w.dtype)
+    check_encoded_stream(xs, basis, mean, bits, p, rec, dot_bound=True, scale=f_gpu)
+    assert rel_l2(dec, O.decode(rec, basis, mean, bits, p, f_gpu)) <= 1e-6
+    rec_o, *_ = O.encode(xs, basis, mean, bits, p, f_gpu)
+    assert rel_l2(dec, O.decode(rec_o, basis, mean, bits, p, f_gpu)) <= 1e-3
+    # the per-head geometry refuses the split
+    ph = O.Params(ratio=8.0)
+    with pytest.raises(S.SpectraError):
+        ch = S.Codec(sparams(ph), 1, latent_scale=True)
+        S.spectra_fit_basis(ch, to_device(np.ascontiguousarray(x[:, :, :128]), w.dtype))
