@@ -51,8 +51,9 @@
  * transform over a layer's whole KV vector, a stream being one (sequence, layer,
  * tensor) matrix with head_dim = d_kv = n_kv_heads x 128): head_dim a multiple
  * of 128 in [256, 1024] with group_size = 64 and records of at most 128 words,
- * for spectra_fit_basis, spectra_encode (bf16 tokens) and spectra_decode; the
- * other GPU entry points return SPECTRA_EUNSUPPORTED for it.
+ * for spectra_fit_basis, spectra_encode (bf16 tokens), spectra_decode and
+ * spectra_layer_decode_attention; the other GPU entry points return
+ * SPECTRA_EUNSUPPORTED for it.
  * The host-only functions (allocation, eigensolver, fit from moments) accept
  * any head_dim <= 1024 that group_size divides.
  */
@@ -186,6 +187,29 @@ spectra_status spectra_encode(const spectra_codec* c, const void* x, spectra_dty
  * ------------------------------------------------------------------------- */
 spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, int64_t t_capacity,
                               int64_t t0, int64_t n_tokens, float* out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Decode-step attention over per-layer latents (App. E Mode B with the latent of
+ * Sec. 3.1 spanning all KV heads of a layer; the per-layer geometry, d = n_kv_heads x
+ * 128). Stream b of both codecs is sequence b < batch (record slots [0, n_tokens));
+ * q[b][h][c] (device, q_dt, contiguous, 128 channels per head), query head h reads KV
+ * head kv = h / (n_q_heads / n_kv_heads), whose keys and values are channels
+ * [128 kv, 128 kv + 128) of the reconstructed layer vectors. out[b][h][c] (fp32) =
+ * sum_t softmax_t(scale q_h . k_hat_t[kv]) v_hat_t[kv], computed as q~_h = scale q_h
+ * V_K[kv rows] (a d-wide latent query), scores over the kept key coefficients (the
+ * constant q~_h . m_K cancels), softmax, value sums over the kept value coefficients,
+ * then (a / sum + m_V) V_V[kv rows]^T. n_q_heads <= 32, records of at most 64 words, no
+ * square-root split. softmax_scale <= 0 selects 1/sqrt(128). Workspace: device,
+ * spectra_layer_attention_workspace_bytes bytes, 256-byte aligned. Asynchronous.
+ * ------------------------------------------------------------------------- */
+size_t spectra_layer_attention_workspace_bytes(const spectra_codec* ck, int32_t batch, int32_t n_q_heads,
+                                               int64_t n_tokens);
+spectra_status spectra_layer_decode_attention(const spectra_codec* ck, const spectra_codec* cv,
+                                              const uint32_t* packed_k, const uint32_t* packed_v,
+                                              int64_t t_capacity, int64_t n_tokens, const void* q,
+                                              spectra_dtype q_dt, int32_t batch, int32_t n_q_heads,
+                                              int32_t n_kv_heads, float softmax_scale, float* out,
+                                              void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Decode-step attention read straight from the packed caches (App. E, Mode B).

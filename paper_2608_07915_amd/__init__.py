@@ -12,5 +12,6 @@ from .codec import (  # noqa: F401
     spectra_decode_attention_rope, spectra_decode_step,
     spectra_eigh_host, spectra_encode, spectra_fit_basis, spectra_fit_from_moments_host,
     spectra_fit_weights, spectra_fit_weights_workspace_bytes, spectra_fit_workspace_bytes, spectra_pack_codes, spectra_record_budget_bits, spectra_record_words,
-    spectra_split_budget, spectra_unpack_codes,
+    spectra_split_budget, spectra_unpack_codes, spectra_layer_attention_workspace_bytes,
+    spectra_layer_decode_attention,
 )

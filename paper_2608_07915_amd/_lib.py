@@ -40,6 +40,9 @@ _PC = ctypes.POINTER(spectra_codec)
 
 _SIGNATURES = {
     "spectra_codec_init": (_I32, [_PC, _PP, _I64]),
+    "spectra_layer_attention_workspace_bytes": (_SZ, [_PC, _I32, _I32, _I64]),
+    "spectra_layer_decode_attention": (_I32, [_PC, _PC, _P, _P, _I64, _I64, _P, _I32, _I32, _I32, _I32, _F32, _P, _P,
+                                              _SZ, _P]),
     "spectra_record_budget_bits": (_I32, [_PP]),
     "spectra_record_words": (_I32, [_PP]),
     "spectra_split_budget": (_I32, [_PP, ctypes.c_double, _PP, _PP]),

@@ -246,6 +246,40 @@ def spectra_decode_attention(ck: Codec, cv: Codec, packed_k, packed_v, t_capacit
     return out
 
 
+def spectra_layer_attention_workspace_bytes(ck: Codec, batch: int, n_q_heads: int, n_tokens: int) -> int:
+    return int(_lib.get().spectra_layer_attention_workspace_bytes(ctypes.byref(ck.struct), int(batch), int(n_q_heads),
+                                                                   int(n_tokens)))
+
+
+def spectra_layer_decode_attention(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, n_tokens: int, q,
+                                   n_kv_heads: int, softmax_scale: float = 0.0, out=None, workspace=None, stream=None):
+    """Decode-step attention over per-layer latents: codecs of the per-layer geometry
+    (stream b = sequence b), q [batch, n_q_heads, 128] -> float32 [batch, n_q_heads, 128]."""
+    import torch
+    _need(q.is_cuda and q.dim() == 3 and q.is_contiguous() and q.shape[2] == 128,
+          "q must be a contiguous device tensor [batch, n_q_heads, 128]")
+    batch, n_q_heads, _ = q.shape
+    _need(ck.params.head_dim == cv.params.head_dim == 128 * int(n_kv_heads),
+          f"the codecs' latent width must be n_kv_heads x 128 = {128 * int(n_kv_heads)}")
+    _need(n_q_heads % n_kv_heads == 0, f"n_q_heads={n_q_heads} is not a multiple of n_kv_heads={n_kv_heads}")
+    _need(ck.n_streams >= batch and cv.n_streams >= batch, "the codecs hold fewer streams than sequences")
+    _packed_words(ck, packed_k, t_capacity, "packed_k")
+    _packed_words(cv, packed_v, t_capacity, "packed_v")
+    if out is None:
+        out = torch.empty((batch, n_q_heads, 128), dtype=torch.float32, device=q.device)
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and tuple(out.shape) == (batch, n_q_heads, 128),
+          f"out must be a contiguous float32 device tensor {(batch, n_q_heads, 128)}")
+    if workspace is None:
+        need = spectra_layer_attention_workspace_bytes(ck, batch, n_q_heads, n_tokens)
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    check(_lib.get().spectra_layer_decode_attention(ctypes.byref(ck.struct), ctypes.byref(cv.struct), packed_k.data_ptr(),
+                                                    packed_v.data_ptr(), int(t_capacity), int(n_tokens), q.data_ptr(),
+                                                    _dtype_code(q), batch, n_q_heads, int(n_kv_heads),
+                                                    float(softmax_scale), out.data_ptr(), workspace.data_ptr(),
+                                                    workspace.numel(), _stream(stream)))
+    return out
+
+
 def spectra_decode_attention_rope(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, n_tokens: int, q,
                                   n_kv_heads: int, inv_freq, q_position: Optional[int] = None, softmax_scale: float = 0.0,
                                   out=None, workspace=None, stream=None):

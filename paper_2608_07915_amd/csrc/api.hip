@@ -337,6 +337,78 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
   return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "decode launch");
 }
 
+size_t spectra_layer_attention_workspace_bytes(const spectra_codec* ck, int32_t batch, int32_t n_q_heads,
+                                               int64_t n_tokens) {
+  if (!ck || batch <= 0 || n_q_heads <= 0 || n_tokens <= 0) return 0;
+  return layer_attention_ws_floats(batch, n_q_heads, ck->p.head_dim, n_tokens) * sizeof(float);
+}
+
+spectra_status spectra_layer_decode_attention(const spectra_codec* ck, const spectra_codec* cv, const uint32_t* packed_k,
+                                              const uint32_t* packed_v, int64_t t_capacity, int64_t n_tokens,
+                                              const void* q, spectra_dtype q_dt, int32_t batch, int32_t n_q_heads,
+                                              int32_t n_kv_heads, float softmax_scale, float* out, void* workspace,
+                                              size_t ws_bytes, void* stream) {
+  const char* name = "layer_decode_attention";
+  spectra_status st = check_codec(ck, name, true);
+  if (st != SPECTRA_OK) return st;
+  st = check_codec(cv, name, true);
+  if (st != SPECTRA_OK) return st;
+  if (!layer_geometry(ck->p) || !layer_geometry(cv->p) || ck->p.head_dim != cv->p.head_dim)
+    return fail(SPECTRA_EINVAL, "%s: both codecs must use the same per-layer geometry", name);
+  if (ck->lscale || cv->lscale) return fail(SPECTRA_EUNSUPPORTED, "%s: codecs with the square-root split are not supported", name);
+  const int d = ck->p.head_dim;
+  if (n_kv_heads <= 0 || n_kv_heads * 128 != d)
+    return fail(SPECTRA_EINVAL, "%s: n_kv_heads * 128 must equal the latent width %d", name, d);
+  if (n_q_heads <= 0 || n_q_heads % n_kv_heads != 0 || n_q_heads > 32)
+    return fail(SPECTRA_EINVAL, "%s: n_q_heads must be a multiple of n_kv_heads, at most 32", name);
+  if (batch <= 0 || batch > 65535 || batch > ck->n_streams || batch > cv->n_streams)
+    return fail(SPECTRA_EINVAL, "%s: batch must be in [1, codec streams]", name);
+  if (ck->record_words > 64 || cv->record_words > 64)
+    return fail(SPECTRA_EUNSUPPORTED, "%s: records of at most 64 words", name);
+  if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "%s: attention needs n_tokens >= 1", name);
+  st = check_slots(0, n_tokens, t_capacity);
+  if (st != SPECTRA_OK) return st;
+  if (q_dt != SPECTRA_F32 && q_dt != SPECTRA_BF16) return fail(SPECTRA_EINVAL, "%s: q dtype %d not supported", name, (int)q_dt);
+  if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return fail(SPECTRA_EINVAL, "%s: q/out must be non-null and aligned", name);
+  if ((ck->record_words > 0 && (!packed_k || !aligned(packed_k, 4))) ||
+      (cv->record_words > 0 && (!packed_v || !aligned(packed_v, 4))))
+    return fail(SPECTRA_EINVAL, "%s: packed_k / packed_v must be non-null and 4-byte aligned", name);
+  if (!(softmax_scale == softmax_scale) || std::isinf(softmax_scale)) return fail(SPECTRA_EINVAL, "%s: softmax_scale not finite", name);
+  const size_t need = spectra_layer_attention_workspace_bytes(ck, batch, n_q_heads, n_tokens);
+  if (!workspace || !aligned(workspace, 256)) return fail(SPECTRA_EINVAL, "%s: workspace must be 256-byte aligned", name);
+  if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "%s: workspace %zu < %zu bytes", name, ws_bytes, need);
+  int dev = 0, lds = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  if ((size_t)lds < layer_scores_lds_bytes(d, ck->record_words))
+    return fail(SPECTRA_EUNSUPPORTED, "%s: needs %zu bytes of LDS per workgroup", name, layer_scores_lds_bytes(d, ck->record_words));
+  spectra_dev::LayerAttnArgs a{};
+  a.packed_k = packed_k;
+  a.packed_v = packed_v;
+  a.t_cap = t_capacity;
+  a.n_tokens = n_tokens;
+  a.basis_k = ck->basis;
+  a.basis_v = cv->basis;
+  a.mean_v = cv->mean;
+  a.bits_k = ck->bits;
+  a.bits_v = cv->bits;
+  a.q = q;
+  a.q_f32 = q_dt == SPECTRA_F32;
+  a.batch = batch;
+  a.n_q_heads = n_q_heads;
+  a.n_kv_heads = n_kv_heads;
+  a.d = d;
+  a.Wk = ck->record_words;
+  a.Wv = cv->record_words;
+  const float sc = softmax_scale > 0.0f ? softmax_scale : 1.0f / std::sqrt(128.0f);
+  a.scale_log2 = sc * 1.4426950408889634f;
+  a.out = out;
+  layer_attention_ws_layout(a, reinterpret_cast<float*>(workspace));
+  e = launch_layer_attention(a, (hipStream_t)stream);
+  return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "layer attention launch");
+}
+
 size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, int64_t n_tokens) {
   if (batch <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_tokens <= 0) return 0;
   int32_t tpc;

@@ -49,3 +49,39 @@ hipError_t launch_layer_moments(const spectra_dev::LayerGramArgs& g, bool f32_in
 hipError_t launch_layer_encode(const spectra_dev::LayerEncodeArgs& a, hipStream_t st);
 hipError_t launch_layer_decode(const spectra_dev::LayerDecodeArgs& a, hipStream_t st);
 }  // namespace spectra
+
+namespace spectra_dev {
+
+// Decode-step attention over per-layer latents (App. E, Mode B, with the latent spanning
+// all KV heads of the layer): stream b of both codecs is sequence b.
+struct LayerAttnArgs {
+  const uint32_t* packed_k;
+  const uint32_t* packed_v;
+  int64_t t_cap, n_tokens;
+  const float* basis_k;
+  const float* basis_v;
+  const float* mean_v;
+  const uint8_t* bits_k;
+  const uint8_t* bits_v;
+  const void* q;
+  int32_t q_f32;
+  int32_t batch, n_q_heads, n_kv_heads, d, Wk, Wv;
+  float scale_log2;
+  int32_t n_chunks, tiles_per_chunk;
+  float* qt;      // [batch][Hq][d]: scale log2(e) q_h V_K[kv rows], 0 on dropped groups
+  float* qsum;    // [batch][Hq][16]: per group sums of qt
+  float* scores;  // [batch][Hq][n_tokens] (log2 domain)
+  float* stats;   // [batch][n_chunks][Hq][2]: chunk max, chunk sum of exp2(s - max)
+  float* part;    // [batch][n_chunks][Hq][d + 16]: value sums per coefficient, zero-point sums per group
+  float* out;     // [batch][Hq][128]
+};
+
+}  // namespace spectra_dev
+
+namespace spectra {
+int32_t layer_attention_chunks(int32_t batch, int64_t n_tokens, int32_t* tiles_per_chunk);
+size_t layer_attention_ws_floats(int32_t batch, int32_t n_q_heads, int32_t d, int64_t n_tokens);
+void layer_attention_ws_layout(spectra_dev::LayerAttnArgs& a, float* ws);
+size_t layer_scores_lds_bytes(int32_t d, int32_t Wk);
+hipError_t launch_layer_attention(const spectra_dev::LayerAttnArgs& a, hipStream_t st);
+}  // namespace spectra

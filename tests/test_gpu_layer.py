@@ -178,3 +178,47 @@ def test_layer_square_root_split(name, ratio):
     with pytest.raises(S.SpectraError):
         ch = S.Codec(sparams(ph), 1, latent_scale=True)
         S.spectra_fit_basis(ch, to_device(np.ascontiguousarray(x[:, :, :128]), w.dtype))
+
+
+def _oracle_layer_attention(q64, kh, vh, n_kv):
+    """Mode A over reconstructed layer vectors: kh, vh [T, n_kv * 128] -> heads of 128."""
+    T = kh.shape[0]
+    k = kh.reshape(T, n_kv, 128).transpose(1, 0, 2)
+    v = vh.reshape(T, n_kv, 128).transpose(1, 0, 2)
+    return O.attention_mode_a(q64, k, v)
+
+
+@pytest.mark.parametrize("name,T,ratio,batch", [("qwen_layer_8x", 1000, 8.0, 1), ("llama_layer_4x", 777, 8.0, 2),
+                                                 ("qwen_layer_8x", 300, 16.0, 2)])
+def test_layer_decode_attention(name, T, ratio, batch):
+    # Mode B over the per-layer latent against Mode A over the oracle's reconstruction of
+    # the same bytes (arithmetic only) and of the oracle's own encoding
+    w = synth.WORKLOADS[name]
+    xk = np.stack([synth.numpy_layer_stream(w, b, 0, 0, max(T_FIT, T)) for b in range(batch)])
+    xv = np.stack([synth.numpy_layer_stream(w, b, 0, 1, max(T_FIT, T)) for b in range(batch)])
+    d = xk.shape[2]
+    n_kv = d // 128
+    p = O.Params(head_dim=d, group_size=64, ratio=ratio)
+    ck, cv = S.Codec(sparams(p), batch), S.Codec(sparams(p), batch)
+    S.spectra_fit_basis(ck, to_device(xk, w.dtype))
+    S.spectra_fit_basis(cv, to_device(xv, w.dtype))
+    t_cap = (T + 63) // 64 * 64 + 64
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
+    S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
+    qs = np.stack([synth.numpy_query(w, b, 0, 0) for b in range(batch)])   # [batch, n_q_heads, 128]
+    out = S.spectra_layer_decode_attention(ck, cv, pk, pv, t_cap, T, to_device(qs, w.dtype), n_kv).cpu().numpy()
+    W = O.record_words(p)
+    for b in range(batch):
+        q64 = values_f64(qs[b], w.dtype)
+        kb, km, kbits = codec_state(ck, b)
+        vb, vm, vbits = codec_state(cv, b)
+        rk, rv = records_of(pk, b, 0, T, t_cap, W), records_of(pv, b, 0, T, t_cap, W)
+        ref = _oracle_layer_attention(q64, O.decode(rk, kb, km, kbits, p), O.decode(rv, vb, vm, vbits, p), n_kv)
+        for h in range(q64.shape[0]):
+            assert rel_l2(out[b, h], ref[h]) <= 2e-5, (b, h, rel_l2(out[b, h], ref[h]))
+        rko, *_ = O.encode(values_f64(xk[b, :T], w.dtype), kb, km, kbits, p)
+        rvo, *_ = O.encode(values_f64(xv[b, :T], w.dtype), vb, vm, vbits, p)
+        ref_o = _oracle_layer_attention(q64, O.decode(rko, kb, km, kbits, p), O.decode(rvo, vb, vm, vbits, p), n_kv)
+        for h in range(q64.shape[0]):
+            assert rel_l2(out[b, h], ref_o[h]) <= 2e-3
