@@ -216,8 +216,8 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
     rope_ms = min(e0.elapsed_time(e1) for e0, e1 in rope_ev[1:])
     rope_bytes = algorithmic_bytes(w, Wk, Wv, n_rec)["attn_call"]
 
-    # ---- per-layer cross-head latent (outside the step): the keys of one layer as one
-    # d_kv = 8 x 128 stream, groups of 64, fitted on its first 8192 tokens ----
+    # ---- per-layer cross-head latent (outside the step): the keys (and values) of one
+    # layer as one d_kv = 8 x 128 stream each, groups of 64, fitted on the first 8192 tokens ----
     dl = H * d
     pl = S.Params(head_dim=dl, group_size=64, ratio=w.ratio)
     xl = synth.device_layer_stream(w, 0, 0, 0, n_rec, dev)
@@ -225,6 +225,12 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
     S.spectra_fit_basis(cl, xl[:, :8192])
     pkl = cl.empty_packed(t_cap)
     outl = torch.empty((1, n_rec, dl), dtype=torch.float32, device=dev)
+    xlv = synth.device_layer_stream(w, 0, 0, 1, n_rec, dev)
+    clv = S.Codec(pl, 1)
+    S.spectra_fit_basis(clv, xlv[:, :8192])
+    pklv = clv.empty_packed(t_cap)
+    S.spectra_encode(clv, xlv, 0, pklv, t_cap)
+    del xlv
     lay_ev = []
     for _ in range(4):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -237,18 +243,35 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
     torch.cuda.synchronize()
     lenc_ms = min(e[0].elapsed_time(e[1]) for e in lay_ev[1:])
     ldec_ms = min(e[1].elapsed_time(e[2]) for e in lay_ev[1:])
+    # Mode B attention of the 32 query heads over both per-layer caches
+    lq = qs[0, 0].contiguous()  # [1, Hq, 128]
+    lws = torch.empty(S.spectra_layer_attention_workspace_bytes(cl, 1, Hq, n_rec), dtype=torch.uint8, device=dev)
+    lout = torch.empty((1, Hq, d), dtype=torch.float32, device=dev)
+    latt_ev = []
+    for _ in range(4):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        S.spectra_layer_decode_attention(cl, clv, pkl, pklv, t_cap, n_rec, lq, H, out=lout, workspace=lws)
+        e[1].record()
+        latt_ev.append(e)
+    torch.cuda.synchronize()
+    latt_ms = min(e[0].elapsed_time(e[1]) for e in latt_ev[1:])
     Wl = cl.record_words
     lenc_bytes = n_rec * dl * 2 + n_rec * Wl * 4 + dl * dl * 4 + dl * 4
     ldec_bytes = n_rec * Wl * 4 + n_rec * dl * 4 + dl * dl * 4 + dl * 4
     kept = int((cl.bits[0] > 0).sum().item())
-    del xl, pkl, outl, cl
+    latt_bytes = 2 * n_rec * Wl * 4 + 2 * (dl * dl * 4 + dl * 4) + Hq * d * 2 + Hq * d * 4
+    del xl, pkl, outl, cl, clv, pklv, lws
 
     return {
         "layer_latent": {"d": dl, "group_size": 64, "record_words": Wl, "kept_groups": kept, "tokens": n_rec,
                          "encode_ms": round(lenc_ms, 4), "encode_GBps": round(lenc_bytes / (lenc_ms * 1e-3) / 1e9, 1),
                          "decode_ms": round(ldec_ms, 4), "decode_GBps": round(ldec_bytes / (ldec_ms * 1e-3) / 1e9, 1),
+                         "attention_us": round(latt_ms * 1e3, 1),
+                         "attention_GBps": round(latt_bytes / (latt_ms * 1e-3) / 1e9, 1),
                          "what": "per-layer cross-head latent: spectra_encode and spectra_decode of one layer's keys "
-                                 "as one d_kv stream, outside the step"},
+                                 "as one d_kv stream, and spectra_layer_decode_attention of the 32 query heads "
+                                 "over that layer's keys and values, outside the step"},
         "mode_a_rope_attention": {"us_per_layer_call": round(rope_ms * 1e3, 1),
                                   "GBps": round(rope_bytes / (rope_ms * 1e-3) / 1e9, 1),
                                   "what": "spectra_decode_attention_rope (keys reconstructed and rotated) over one "

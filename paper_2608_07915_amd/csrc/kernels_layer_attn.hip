@@ -11,12 +11,13 @@
 //                         (exact in fp16) times q~ as two fp16 parts on
 //                         v_mfma_f32_16x16x32_f16, one kept group at a time, the
 //                         token's scale and zero point applied after; chunk max and sum;
+//   layer_stats_kernel    softmax max and sum of every head over the chunks;
 //   layer_values_kernel   p = exp2(s - max over all chunks), then per kept value group
-//                         sum_t p_t s_t q_t on v_mfma_f32_16x16x32_f16 (weights as two
-//                         fp16 parts, codes of eight consecutive tokens read from the
+//                         sum_t p_t s_t q_t on v_mfma_f32_16x16x32_bf16 (weights as three
+//                         bf16 parts, codes of eight consecutive tokens read from the
 //                         word-major tile) and sum_t p_t z_t;
-//   layer_combine_kernel  sums the chunk partials, divides by the softmax sum, adds m_V
-//                         and applies V_V[kv rows]^T.
+//   layer_combine_kernel  sums the chunk partials, divides by the softmax sum, adds m_V;
+//   layer_rotate_kernel   applies V_V[kv rows]^T.
 #include "device_common.hpp"
 #include "kernels.hpp"
 #include "layer.hpp"
@@ -62,11 +63,13 @@ __device__ __forceinline__ bool layer_bits_ok(const uint8_t* __restrict__ bits_s
 // ---------------------------------------------------------------------------
 // q~[b][h][j] = scale log2(e) sum_i q[b][h][i] V_K[b][kv 128 + i][j] on kept groups
 // ---------------------------------------------------------------------------
+// grid (heads, sequences, d / 256): thread -> one coefficient j, four groups per workgroup
 __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
   __shared__ float qv[128];
-  __shared__ float qtl[1024];
+  __shared__ float qtl[256];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int d = a.d, ng = d / 64;
+  const int j = 256 * blockIdx.z + tid;
   const int kv = h / (a.n_q_heads / a.n_kv_heads);
   const uint8_t* bits_s = a.bits_k + (int64_t)b * ng;
   if (tid < 128) {
@@ -75,20 +78,24 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
               a.scale_log2;
   }
   __syncthreads();
-  const float* V = a.basis_k + (int64_t)b * d * d + (int64_t)kv * 128 * d;
-  for (int j = tid; j < d; j += 256) {
-    float acc = 0.0f;
-    if (bits_s[j >> 6] > 0)
-      for (int i = 0; i < 128; ++i) acc = __builtin_fmaf(qv[i], V[(int64_t)i * d + j], acc);
-    qtl[j] = acc;
-    a.qt[((int64_t)b * a.n_q_heads + h) * d + j] = acc;
+  const float* V = a.basis_k + (int64_t)b * d * d + (int64_t)kv * 128 * d + j;
+  float acc = 0.0f;
+  if (j < d && bits_s[j >> 6] > 0) {
+    float part[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int i = 0; i < 128; i += 8)
+#pragma unroll
+      for (int r = 0; r < 8; ++r) part[r] = __builtin_fmaf(qv[i + r], V[(int64_t)(i + r) * d], part[r]);
+    acc = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
   }
+  qtl[tid] = acc;
+  if (j < d) a.qt[((int64_t)b * a.n_q_heads + h) * d + j] = acc;
   __syncthreads();
-  if (tid < 16) {
+  // group sums (only the groups of this workgroup's coefficients; the score pass reads kept groups only)
+  if (tid < 4 && 4 * (int)blockIdx.z + tid < ng) {
     float s = 0.0f;
-    if (tid < ng)
-      for (int j = 0; j < 64; ++j) s += qtl[64 * tid + j];
-    a.qsum[((int64_t)b * a.n_q_heads + h) * 16 + tid] = s;
+    for (int jj = 0; jj < 64; ++jj) s += qtl[64 * tid + jj];
+    a.qsum[((int64_t)b * a.n_q_heads + h) * 16 + 4 * blockIdx.z + tid] = s;
   }
 }
 
@@ -97,7 +104,9 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
 // ---------------------------------------------------------------------------
 __host__ __device__ constexpr int la_qp(int d) { return d + 8; }  // fp16 per staged query row
 __host__ __device__ constexpr int la_off_rec(int d) { return 2 * LA_H * la_qp(d) * 2; }
-__host__ __device__ constexpr int la_off_qs(int d, int Wk) { return la_off_rec(d) + Wk * LA_ROW * 4; }
+// the record rows also hold the slot halves' scores of a tile ([4][64][8] floats) once read
+__host__ __device__ constexpr int la_rec_bytes(int Wk) { return Wk * LA_ROW * 4 > 4 * 64 * 8 * 4 ? Wk * LA_ROW * 4 : 4 * 64 * 8 * 4; }
+__host__ __device__ constexpr int la_off_qs(int d, int Wk) { return la_off_rec(d) + la_rec_bytes(Wk); }
 __host__ __device__ constexpr int la_scores_lds(int d, int Wk) { return la_off_qs(d, Wk) + LA_H * 16 * 4 + 4 * LA_H * 2 * 4; }
 
 __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
@@ -117,8 +126,9 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   __syncthreads();
   const int nk = snk;
   // kept coefficients of q~ as two fp16 parts, compacted by slot; group sums
-  for (int e = tid; e < LA_H * nk * 64; e += 512) {
-    const int h = e / (nk * 64), jj = e - h * (nk * 64);
+  for (int e = tid; e < LA_H * 16 * 64; e += 512) {
+    const int h = e >> 10, jj = e & 1023;
+    if ((jj >> 6) >= nk) continue;
     const float v = h < Hq ? a.qt[((int64_t)b * Hq + h) * d + 64 * sgrp[jj >> 6] + (jj & 63)] : 0.0f;
     const _Float16 hi = (_Float16)v;
     const _Float16 lo = (_Float16)(v - (float)hi);
@@ -134,24 +144,41 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   const int64_t t_begin = (int64_t)chunk * a.tiles_per_chunk;
   const int64_t t_end = t_begin + a.tiles_per_chunk < n_tiles ? t_begin + a.tiles_per_chunk : n_tiles;
   const uint32_t* kp = a.packed_k + (int64_t)b * a.t_cap * Wk;
-  const int hb = wave & 1, tb = wave >> 1;  // head block (16 heads), token block (16 tokens)
-  float mloc[4], lloc[4];
+  // wavefront: token block tb (16 tokens), both head blocks, kept slots sh, sh + 2, ...
+  const int tb = wave & 3, sh = wave >> 2;
+  float mloc[8], lloc[8];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 8; ++j) {
     mloc[j] = -__builtin_inff();
     lloc[j] = 0.0f;
   }
+  constexpr int PF = 64 * LA_WMAX / 512;  // record words per thread and tile
+  uint32_t pre[PF];
+  auto load_tile = [&](int64_t tt) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + 512 * i;
+      pre[i] = k < 64 * Wk ? kp[tt * 64 * Wk + k] : 0u;
+    }
+  };
+  float* sred = reinterpret_cast<float*>(rec);  // [4 token blocks][64 lanes][8], after the tile's products
+  if (t_begin < t_end) load_tile(t_begin);
   for (int64_t tt = t_begin; tt < t_end; ++tt) {
     __syncthreads();  // previous tile's reads done (and the prologue's writes visible)
-    for (int k = tid; k < 64 * Wk; k += 512) rec[(k >> 6) * LA_ROW + (k & 63)] = kp[tt * 64 * Wk + k];
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + 512 * i;
+      if (k < 64 * Wk) rec[(k >> 6) * LA_ROW + (k & 63)] = pre[i];
+    }
     __syncthreads();
+    if (tt + 1 < t_end) load_tile(tt + 1);
     const int u = 16 * tb + c16;
-    f32x4 S = {0.f, 0.f, 0.f, 0.f};
-    for (int sl = 0; sl < nk; ++sl) {
+    f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    for (int sl = sh; sl < nk; sl += 2) {
       const int pay = spay[sl];
       const uint32_t m = rec[sl * LA_ROW + u];
       const float st = h2f(m), zt = h2f(m >> 16);
-      f32x4 g = {0.f, 0.f, 0.f, 0.f};
+      f32x4 g[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         f16x8v bop;
@@ -163,36 +190,54 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
           for (int i = 0; i < 8; ++i) bop[i] = (_Float16)(float)cd[i];
         });
         const int col = sl * 64 + 32 * ks + 8 * kg;
-        const f16x8v a0 = __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (16 * hb + c16) * QP + col));
-        const f16x8v a1 = __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (LA_H + 16 * hb + c16) * QP + col));
-        g = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bop, g, 0, 0, 0);
-        g = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bop, g, 0, 0, 0);
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+          const f16x8v a0 = __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (16 * hb + c16) * QP + col));
+          const f16x8v a1 =
+              __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (LA_H + 16 * hb + c16) * QP + col));
+          g[hb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bop, g[hb], 0, 0, 0);
+          g[hb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bop, g[hb], 0, 0, 0);
+        }
       }
       // lane: heads 16 hb + 4 kg + j, token u
 #pragma unroll
-      for (int j = 0; j < 4; ++j) S[j] += st * g[j] + zt * qs[(16 * hb + 4 * kg + j) * 16 + sl];
-    }
-    const int64_t t = tt * 64 + u;
-    if (t < a.n_tokens) {
+      for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int h = 16 * hb + 4 * kg + j;
-        if (h < Hq) {
-          a.scores[((int64_t)b * Hq + h) * a.n_tokens + t] = S[j];
-          const float x = S[j];
-          if (x > mloc[j]) {
-            lloc[j] = lloc[j] * __builtin_amdgcn_exp2f(mloc[j] - x) + 1.0f;
-            mloc[j] = x;
-          } else {
-            lloc[j] += __builtin_amdgcn_exp2f(x - mloc[j]);
+        for (int j = 0; j < 4; ++j) S[hb][j] += st * g[hb][j] + zt * qs[(16 * hb + 4 * kg + j) * 16 + sl];
+    }
+    // the two slot halves meet in LDS (over the record rows, whose reads are done)
+    __syncthreads();
+    if (sh == 1) {
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sred[(tb * 64 + lane) * 8 + 4 * hb + j] = S[hb][j];
+    }
+    __syncthreads();
+    if (sh == 0) {
+      const int64_t t = tt * 64 + u;
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int h = 16 * hb + 4 * kg + j;
+          const float x = S[hb][j] + sred[(tb * 64 + lane) * 8 + 4 * hb + j];
+          if (t < a.n_tokens && h < Hq) {
+            a.scores[((int64_t)b * Hq + h) * a.n_tokens + t] = x;
+            const int q = 4 * hb + j;
+            if (x > mloc[q]) {
+              lloc[q] = lloc[q] * __builtin_amdgcn_exp2f(mloc[q] - x) + 1.0f;
+              mloc[q] = x;
+            } else {
+              lloc[q] += __builtin_amdgcn_exp2f(x - mloc[q]);
+            }
           }
         }
-      }
     }
   }
   // chunk statistics: merge the 16 token lanes, then the four token-block wavefronts
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 8; ++j) {
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) {
       const float mo = __shfl_xor(mloc[j], o), lo = __shfl_xor(lloc[j], o);
@@ -204,12 +249,12 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
     }
   }
   __syncthreads();
-  if (c16 == 0) {
+  if (c16 == 0 && sh == 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int h = 16 * hb + 4 * kg + j;
-      red[(tb * LA_H + h) * 2] = mloc[j];
-      red[(tb * LA_H + h) * 2 + 1] = lloc[j];
+    for (int q = 0; q < 8; ++q) {
+      const int h = 16 * (q >> 2) + 4 * kg + (q & 3);
+      red[(tb * LA_H + h) * 2] = mloc[q];
+      red[(tb * LA_H + h) * 2 + 1] = lloc[q];
     }
   }
   __syncthreads();
@@ -228,80 +273,138 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Values
+// Softmax max and sum of every head over all chunks (one workgroup per head)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void layer_stats_kernel(LayerAttnArgs a) {
+  __shared__ float rm[4], rl[4];
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Hq = a.n_q_heads;
+  float m = -__builtin_inff(), l = 0.0f;
+  for (int c = tid; c < a.n_chunks; c += 256) {
+    const float* st = a.stats + (((int64_t)b * a.n_chunks + c) * Hq + h) * 2;
+    const float mc = st[0], lc = st[1];
+    if (mc != -__builtin_inff()) {
+      const float mn = __builtin_fmaxf(m, mc);
+      l = (m == -__builtin_inff() ? 0.0f : l * __builtin_amdgcn_exp2f(m - mn)) + lc * __builtin_amdgcn_exp2f(mc - mn);
+      m = mn;
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float mo = __shfl_xor(m, o), lo = __shfl_xor(l, o);
+    const float mn = __builtin_fmaxf(m, mo);
+    l = (m == -__builtin_inff() ? 0.0f : l * __builtin_amdgcn_exp2f(m - mn)) +
+        (mo == -__builtin_inff() ? 0.0f : lo * __builtin_amdgcn_exp2f(mo - mn));
+    m = mn;
+  }
+  if (lane == 0) {
+    rm[wave] = m;
+    rl[wave] = l;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float mm = -__builtin_inff();
+    for (int w = 0; w < 4; ++w) mm = __builtin_fmaxf(mm, rm[w]);
+    float ll = 0.0f;
+    for (int w = 0; w < 4; ++w)
+      if (rm[w] != -__builtin_inff()) ll += rl[w] * __builtin_amdgcn_exp2f(rm[w] - mm);
+    a.ml[((int64_t)b * Hq + h) * 2] = mm;
+    a.ml[((int64_t)b * Hq + h) * 2 + 1] = ll;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Values: one workgroup per (token chunk, quarter of the kept slots, sequence)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t rec[LA_WMAX * LA_ROW];
   __shared__ __attribute__((aligned(16))) float pl[LA_H * LA_ROW];
   __shared__ float mh[LA_H];
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
-  const int chunk = blockIdx.x, b = blockIdx.y;
+  const int chunk = blockIdx.x, quarter = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
   const int d = a.d, ng = d / 64, Wv = a.Wv, Hq = a.n_q_heads;
   const uint8_t* bits_s = a.bits_v + (int64_t)b * ng;
   const bool ok = layer_bits_ok(bits_s, ng, Wv) && layer_bits_ok(a.bits_k + (int64_t)b * ng, ng, a.Wk);
   if (tid == 0) snk = ok ? layer_slots(bits_s, ng, sgrp, sbw, spay) : 0;
-  if (tid < LA_H) {
-    float m = -__builtin_inff();
-    if (tid < Hq)
-      for (int c = 0; c < a.n_chunks; ++c) m = __builtin_fmaxf(m, a.stats[(((int64_t)b * a.n_chunks + c) * Hq + tid) * 2]);
-    mh[tid] = m;
-  }
+  if (tid < LA_H) mh[tid] = tid < Hq ? a.ml[((int64_t)b * Hq + tid) * 2] : -__builtin_inff();
   __syncthreads();
   const int nk = snk;
-  const int hb = wave & 1, q4 = wave >> 1;  // head block; value slots q4, q4 + 4, q4 + 8, q4 + 12
-  f32x4 acc[4][4];
+  // wavefront: head block hb, kept slot quarter + 4 si (its four 16-coefficient column blocks)
+  const int hb = wave & 1, si = wave >> 1;
+  f32x4 acc[1][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int zh = tid & 31, zsl = tid >> 5;  // zero-point sums: thread -> (head, slot)
+  for (int c = 0; c < 4; ++c) acc[0][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int zh = tid & 31, zsl = quarter + 4 * (tid >> 5);  // zero-point sums: threads < 128 -> (head, slot)
+  const bool zthr = tid < 128;
   float zacc = 0.0f;
 
   const int64_t n_tiles = (a.n_tokens + 63) >> 6;
-  const int64_t t_begin = (int64_t)chunk * a.tiles_per_chunk;
-  const int64_t t_end = t_begin + a.tiles_per_chunk < n_tiles ? t_begin + a.tiles_per_chunk : n_tiles;
+  const int64_t t_begin = (int64_t)chunk * a.v_tiles_per_chunk;
+  const int64_t t_end = t_begin + a.v_tiles_per_chunk < n_tiles ? t_begin + a.v_tiles_per_chunk : n_tiles;
   const uint32_t* vp = a.packed_v + (int64_t)b * a.t_cap * Wv;
+  constexpr int PF = 64 * LA_WMAX / 512;       // record words per thread and tile
+  constexpr int PS = LA_H * 64 / 512;          // scores per thread and tile
+  uint32_t pre[PF];
+  float spre[PS];
+  auto load_tile = [&](int64_t tt) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + 512 * i;
+      pre[i] = k < 64 * Wv ? vp[tt * 64 * Wv + k] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < PS; ++i) {
+      const int e = tid + 512 * i, h = e >> 6;
+      const int64_t tok = tt * 64 + (e & 63);
+      spre[i] = (h < Hq && tok < a.n_tokens) ? a.scores[((int64_t)b * Hq + h) * a.n_tokens + tok] : -__builtin_inff();
+    }
+  };
+  if (ok && t_begin < t_end) load_tile(t_begin);
   for (int64_t tt = (ok ? t_begin : t_end); tt < t_end; ++tt) {
     __syncthreads();
-    for (int k = tid; k < 64 * Wv; k += 512) rec[(k >> 6) * LA_ROW + (k & 63)] = vp[tt * 64 * Wv + k];
-    for (int e = tid; e < LA_H * 64; e += 512) {
-      const int h = e >> 6, t = e & 63;
-      const int64_t tok = tt * 64 + t;
-      float p = 0.0f;
-      if (h < Hq && tok < a.n_tokens && mh[h] != -__builtin_inff())
-        p = __builtin_amdgcn_exp2f(a.scores[((int64_t)b * Hq + h) * a.n_tokens + tok] - mh[h]);
-      pl[h * LA_ROW + t] = p;
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + 512 * i;
+      if (k < 64 * Wv) rec[(k >> 6) * LA_ROW + (k & 63)] = pre[i];
+    }
+#pragma unroll
+    for (int i = 0; i < PS; ++i) {
+      const int e = tid + 512 * i, h = e >> 6;
+      const float x = spre[i];
+      pl[h * LA_ROW + (e & 63)] = (x != -__builtin_inff() && mh[h] != -__builtin_inff()) ? __builtin_amdgcn_exp2f(x - mh[h]) : 0.0f;
     }
     __syncthreads();
-    if (zsl < nk && zh < Hq) {
+    if (tt + 1 < t_end) load_tile(tt + 1);
+    if (zthr && zsl < nk && zh < Hq) {
       float z = 0.0f;
       for (int t = 0; t < 64; ++t) z = __builtin_fmaf(pl[zh * LA_ROW + t], h2f(rec[zsl * LA_ROW + t] >> 16), z);
       zacc += z;
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int sl = q4 + 4 * i;
+    for (int i = 0; i < 1; ++i) {
+      const int sl = quarter + 4 * si;
       if (sl < nk) {
         const int B = sbw[sl], pay = spay[sl];
         const uint32_t M = (1u << B) - 1u;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           const int tk0 = 32 * ks + 8 * kg;
-          // weights p_t s_t of head 16 hb + c16 for tokens tk0 .. tk0 + 7, two fp16 parts
-          f16x8v whi, wlo;
+          // weights p_t s_t of head 16 hb + c16 for tokens tk0 .. tk0 + 7 as three bf16
+          // parts (the fp32 exponent range: p_t s_t spans many decades below 1)
+          bf16x8 wp[3];
           {
             const float* pr = pl + (16 * hb + c16) * LA_ROW + tk0;
             const f32x4 p0 = *reinterpret_cast<const f32x4*>(pr), p1 = *reinterpret_cast<const f32x4*>(pr + 4);
             const u32x4 m0 = *reinterpret_cast<const u32x4*>(rec + sl * LA_ROW + tk0);
             const u32x4 m1 = *reinterpret_cast<const u32x4*>(rec + sl * LA_ROW + tk0 + 4);
+            uint32_t q0[8], q1[8], q2[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float w = (e < 4 ? p0[e] : p1[e - 4]) * h2f(e < 4 ? m0[e] : m1[e - 4]);
-              const _Float16 hi = (_Float16)w;
-              whi[e] = hi;
-              wlo[e] = (_Float16)(w - (float)hi);
-            }
+            for (int e = 0; e < 8; ++e)
+              split3((e < 4 ? p0[e] : p1[e - 4]) * h2f(e < 4 ? m0[e] : m1[e - 4]), q0[e], q1[e], q2[e]);
+            wp[0] = as_bf16x8(u32x4{pack2(q0[0], q0[1]), pack2(q0[2], q0[3]), pack2(q0[4], q0[5]), pack2(q0[6], q0[7])});
+            wp[1] = as_bf16x8(u32x4{pack2(q1[0], q1[1]), pack2(q1[2], q1[3]), pack2(q1[4], q1[5]), pack2(q1[6], q1[7])});
+            wp[2] = as_bf16x8(u32x4{pack2(q2[0], q2[1]), pack2(q2[2], q2[3]), pack2(q2[4], q2[5]), pack2(q2[6], q2[7])});
           }
 #pragma unroll
           for (int cb = 0; cb < 4; ++cb) {
@@ -315,24 +418,27 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
               h0 = *reinterpret_cast<const u32x4*>(rec + (w + 1) * LA_ROW + tk0);
               h1 = *reinterpret_cast<const u32x4*>(rec + (w + 1) * LA_ROW + tk0 + 4);
             }
-            f16x8v cv;
+            uint32_t cd[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              cv[e] = (_Float16)(float)(__builtin_amdgcn_alignbit(h0[e], l0[e], sh) & M);
-              cv[4 + e] = (_Float16)(float)(__builtin_amdgcn_alignbit(h1[e], l1[e], sh) & M);
+              cd[e] = __builtin_amdgcn_alignbit(h0[e], l0[e], sh) & M;
+              cd[4 + e] = __builtin_amdgcn_alignbit(h1[e], l1[e], sh) & M;
             }
-            acc[i][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(whi, cv, acc[i][cb], 0, 0, 0);
-            acc[i][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wlo, cv, acc[i][cb], 0, 0, 0);
+            const bf16x8 cv = as_bf16x8(u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]),
+                                              int_to_bf16_pair(cd[4], cd[5]), int_to_bf16_pair(cd[6], cd[7])});
+#pragma unroll
+            for (int q = 0; q < 3; ++q)
+              acc[i][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wp[q], cv, acc[i][cb], 0, 0, 0);
           }
         }
       }
     }
   }
   // partials: lane holds rows (heads 16 hb + 4 kg + j) of column (coefficient 16 cb + c16)
-  float* pb = a.part + ((int64_t)b * a.n_chunks + chunk) * Hq * (d + 16);
+  float* pb = a.part + ((int64_t)b * a.nv_chunks + chunk) * Hq * (d + 16);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int sl = q4 + 4 * i;
+  for (int i = 0; i < 1; ++i) {
+    const int sl = quarter + 4 * si;
     if (sl < nk) {
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb)
@@ -343,57 +449,70 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
         }
     }
   }
-  if (zsl < nk && zh < Hq) pb[(int64_t)zh * (d + 16) + d + sgrp[zsl]] = zacc;
+  if (zthr && zsl < nk && zh < Hq) pb[(int64_t)zh * (d + 16) + d + sgrp[zsl]] = zacc;
 }
 
 // ---------------------------------------------------------------------------
-// Combine and inverse rotation
+// Combine: c[j] = (sum over value chunks of the coefficient sums + zero-point sums)
+// / softmax sum + m_V[j], written over q~ (no longer needed); grid (heads, sequences,
+// d / 256), one coefficient per thread
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void layer_combine_kernel(LayerAttnArgs a) {
-  __shared__ float cf[1024];
-  __shared__ float part_o[2][128];
-  __shared__ float ml[2];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int d = a.d, ng = d / 64, Hq = a.n_q_heads;
-  const int kv = h / (Hq / a.n_kv_heads);
+  const int j = 256 * blockIdx.z + tid;
+  if (j >= d) return;
   const uint8_t* bv = a.bits_v + (int64_t)b * ng;
   const bool ok = layer_bits_ok(bv, ng, a.Wv) && layer_bits_ok(a.bits_k + (int64_t)b * ng, ng, a.Wk);
-  if (tid == 0) {
-    float m = -__builtin_inff();
-    for (int c = 0; c < a.n_chunks; ++c) m = __builtin_fmaxf(m, a.stats[(((int64_t)b * a.n_chunks + c) * Hq + h) * 2]);
-    float l = 0.0f;
-    for (int c = 0; c < a.n_chunks; ++c) {
-      const float* st = a.stats + (((int64_t)b * a.n_chunks + c) * Hq + h) * 2;
-      if (st[0] != -__builtin_inff()) l += st[1] * __builtin_amdgcn_exp2f(st[0] - m);
-    }
-    ml[0] = m;
-    ml[1] = l;
-  }
-  __syncthreads();
-  const float inv_l = ml[1] > 0.0f ? 1.0f / ml[1] : 0.0f;
-  const float* mv = a.mean_v + (int64_t)b * d;
-  for (int j = tid; j < d; j += 256) {
-    const int g = j >> 6;
-    float c = 0.0f;
-    if (ok && bv[g] > 0) {
-      float s = 0.0f, z = 0.0f;
-      for (int ch = 0; ch < a.n_chunks; ++ch) {
-        const float* pb = a.part + (((int64_t)b * a.n_chunks + ch) * Hq + h) * (d + 16);
-        s += pb[j];
-        z += pb[d + g];
+  const float l = a.ml[((int64_t)b * Hq + h) * 2 + 1];
+  const float inv_l = l > 0.0f ? 1.0f / l : 0.0f;
+  const int g = j >> 6;
+  float c = 0.0f;
+  if (ok && bv[g] > 0) {
+    float s[4] = {0.f, 0.f, 0.f, 0.f}, z[4] = {0.f, 0.f, 0.f, 0.f};
+    const float* pb = a.part + ((int64_t)b * a.nv_chunks * Hq + h) * (d + 16);
+    const int64_t cstride = (int64_t)Hq * (d + 16);
+    int ch = 0;
+    for (; ch + 4 <= a.nv_chunks; ch += 4)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s[r] += pb[(ch + r) * cstride + j];
+        z[r] += pb[(ch + r) * cstride + d + g];
       }
-      c = (s + z) * inv_l;
+    for (; ch < a.nv_chunks; ++ch) {
+      s[0] += pb[ch * cstride + j];
+      z[0] += pb[ch * cstride + d + g];
     }
-    cf[j] = c + mv[j];
+    c = (((s[0] + s[1]) + (s[2] + s[3])) + ((z[0] + z[1]) + (z[2] + z[3]))) * inv_l;
   }
-  __syncthreads();
-  const int i = tid & 127, half = tid >> 7;
-  const float* vr = a.basis_v + (int64_t)b * d * d + (int64_t)(kv * 128 + i) * d;
-  float acc = 0.0f;
-  for (int j = half * (d / 2); j < (half + 1) * (d / 2); ++j) acc = __builtin_fmaf(cf[j], vr[j], acc);
-  part_o[half][i] = acc;
-  __syncthreads();
-  if (tid < 128) a.out[((int64_t)b * Hq + h) * 128 + tid] = part_o[0][tid] + part_o[1][tid];
+  a.qt[((int64_t)b * Hq + h) * d + j] = c + a.mean_v[(int64_t)b * d + j];
+}
+
+// ---------------------------------------------------------------------------
+// Inverse rotation: out[i] = sum_j c[j] V_V[kv 128 + i][j]; grid (heads, sequences, 16):
+// workgroup z takes rows 8 z .. 8 z + 7, two per wavefront, each row read by the whole
+// wavefront (d / 64 values per lane), then a wavefront sum
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void layer_rotate_kernel(LayerAttnArgs a) {
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, Hq = a.n_q_heads;
+  const int kv = h / (Hq / a.n_kv_heads);
+  const float* cfv = a.qt + ((int64_t)b * Hq + h) * d;
+  float cl[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) cl[k] = (64 * k + lane < d) ? cfv[64 * k + lane] : 0.0f;
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int i = 8 * blockIdx.z + 2 * wave + r;
+    const float* vr = a.basis_v + (int64_t)b * d * d + (int64_t)(kv * 128 + i) * d;
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (64 * k + lane < d) acc = __builtin_fmaf(cl[k], vr[64 * k + lane], acc);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+    if (lane == 0) a.out[((int64_t)b * Hq + h) * 128 + i] = acc;
+  }
 }
 
 }  // namespace spectra_dev
@@ -411,22 +530,35 @@ int32_t layer_attention_chunks(int32_t batch, int64_t n_tokens, int32_t* tiles_p
   return (int32_t)((n_tiles + tpc - 1) / tpc);
 }
 
+// Value pass: about 256 workgroups over (chunk, slot quarter, sequence), at least 8 tiles each.
+int32_t layer_value_chunks(int32_t batch, int64_t n_tokens, int32_t* tiles_per_chunk) {
+  const int64_t n_tiles = (n_tokens + 63) / 64;
+  const int64_t want = (64 + batch - 1) / batch;
+  int64_t tpc = (n_tiles + want - 1) / want;
+  if (tpc < 8) tpc = 8;
+  *tiles_per_chunk = (int32_t)tpc;
+  return (int32_t)((n_tiles + tpc - 1) / tpc);
+}
+
 size_t layer_attention_ws_floats(int32_t batch, int32_t n_q_heads, int32_t d, int64_t n_tokens) {
   int32_t tpc;
   const int64_t nch = layer_attention_chunks(batch, n_tokens, &tpc);
+  const int64_t nv = layer_value_chunks(batch, n_tokens, &tpc);
   const int64_t B = batch, H = n_q_heads;
   auto r64 = [](int64_t n) { return (n + 63) / 64 * 64; };  // 256-byte aligned sections
-  return (size_t)(r64(B * H * d) + r64(B * H * 16) + r64(B * H * n_tokens) + r64(B * nch * H * 2) +
-                  r64(B * nch * H * (d + 16)));
+  return (size_t)(r64(B * H * d) + r64(B * H * 16) + r64(B * H * 2) + r64(B * H * n_tokens) + r64(B * nch * H * 2) +
+                  r64(B * nv * H * (d + 16)));
 }
 
 void layer_attention_ws_layout(LayerAttnArgs& a, float* ws) {
   a.n_chunks = layer_attention_chunks(a.batch, a.n_tokens, &a.tiles_per_chunk);
+  a.nv_chunks = layer_value_chunks(a.batch, a.n_tokens, &a.v_tiles_per_chunk);
   const int64_t B = a.batch, H = a.n_q_heads;
   auto r64 = [](int64_t n) { return (n + 63) / 64 * 64; };
   a.qt = ws;
   a.qsum = a.qt + r64(B * H * a.d);
-  a.scores = a.qsum + r64(B * H * 16);
+  a.ml = a.qsum + r64(B * H * 16);
+  a.scores = a.ml + r64(B * H * 2);
   a.stats = a.scores + r64(B * H * a.n_tokens);
   a.part = a.stats + r64(B * a.n_chunks * H * 2);
 }
@@ -434,16 +566,22 @@ void layer_attention_ws_layout(LayerAttnArgs& a, float* ws) {
 size_t layer_scores_lds_bytes(int32_t d, int32_t Wk) { return (size_t)la_scores_lds(d, Wk); }
 
 hipError_t launch_layer_attention(const LayerAttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(layer_qprep_kernel, dim3(a.n_q_heads, a.batch), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(layer_qprep_kernel, dim3(a.n_q_heads, a.batch, (a.d + 255) / 256), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(layer_scores_kernel, dim3(a.n_chunks, a.batch), dim3(512), la_scores_lds(a.d, a.Wk), st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layer_values_kernel, dim3(a.n_chunks, a.batch), dim3(512), 0, st, a);
+  hipLaunchKernelGGL(layer_stats_kernel, dim3(a.n_q_heads, a.batch), dim3(256), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layer_combine_kernel, dim3(a.n_q_heads, a.batch), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(layer_values_kernel, dim3(a.nv_chunks, 4, a.batch), dim3(512), 0, st, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(layer_combine_kernel, dim3(a.n_q_heads, a.batch, (a.d + 255) / 256), dim3(256), 0, st, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(layer_rotate_kernel, dim3(a.n_q_heads, a.batch, 16), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -67,12 +67,14 @@ struct LayerAttnArgs {
   int32_t q_f32;
   int32_t batch, n_q_heads, n_kv_heads, d, Wk, Wv;
   float scale_log2;
-  int32_t n_chunks, tiles_per_chunk;
+  int32_t n_chunks, tiles_per_chunk;     // score pass: token chunks
+  int32_t nv_chunks, v_tiles_per_chunk;  // value pass: token chunks (x 4 kept-slot quarters)
   float* qt;      // [batch][Hq][d]: scale log2(e) q_h V_K[kv rows], 0 on dropped groups
+  float* ml;      // [batch][Hq][2]: softmax max and sum over all tokens
   float* qsum;    // [batch][Hq][16]: per group sums of qt
   float* scores;  // [batch][Hq][n_tokens] (log2 domain)
   float* stats;   // [batch][n_chunks][Hq][2]: chunk max, chunk sum of exp2(s - max)
-  float* part;    // [batch][n_chunks][Hq][d + 16]: value sums per coefficient, zero-point sums per group
+  float* part;    // [batch][nv_chunks][Hq][d + 16]: value sums per coefficient, zero-point sums per group
   float* out;     // [batch][Hq][128]
 };
 

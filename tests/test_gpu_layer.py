@@ -189,7 +189,7 @@ def _oracle_layer_attention(q64, kh, vh, n_kv):
 
 
 @pytest.mark.parametrize("name,T,ratio,batch", [("qwen_layer_8x", 1000, 8.0, 1), ("llama_layer_4x", 777, 8.0, 2),
-                                                 ("qwen_layer_8x", 300, 16.0, 2)])
+                                                 ("qwen_layer_8x", 300, 16.0, 2), ("qwen_layer_8x", 2500, 8.0, 1)])
 def test_layer_decode_attention(name, T, ratio, batch):
     # Mode B over the per-layer latent against Mode A over the oracle's reconstruction of
     # the same bytes (arithmetic only) and of the oracle's own encoding
@@ -222,3 +222,29 @@ def test_layer_decode_attention(name, T, ratio, batch):
         ref_o = _oracle_layer_attention(q64, O.decode(rko, kb, km, kbits, p), O.decode(rvo, vb, vm, vbits, p), n_kv)
         for h in range(q64.shape[0]):
             assert rel_l2(out[b, h], ref_o[h]) <= 2e-3
+
+
+def test_layer_attention_three_heads_d384():
+    # a latent width that is not a multiple of 256 (three KV heads side by side)
+    w = synth.WORKLOADS["qwen_layer_8x"]
+    T = 700
+    xk = np.ascontiguousarray(synth.numpy_layer_stream(w, 0, 0, 0, T_FIT)[None, :, :384])
+    xv = np.ascontiguousarray(synth.numpy_layer_stream(w, 0, 0, 1, T_FIT)[None, :, :384])
+    p = O.Params(head_dim=384, group_size=64, ratio=8.0)
+    ck, cv = S.Codec(sparams(p), 1), S.Codec(sparams(p), 1)
+    S.spectra_fit_basis(ck, to_device(xk, w.dtype))
+    S.spectra_fit_basis(cv, to_device(xv, w.dtype))
+    t_cap = 768
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
+    S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
+    qs = np.ascontiguousarray(synth.numpy_query(w, 0, 0, 0)[None, :24])
+    out = S.spectra_layer_decode_attention(ck, cv, pk, pv, t_cap, T, to_device(qs, w.dtype), 3).cpu().numpy()
+    W = O.record_words(p)
+    kb, km, kbits = codec_state(ck, 0)
+    vb, vm, vbits = codec_state(cv, 0)
+    ref = _oracle_layer_attention(values_f64(qs[0], w.dtype),
+                                  O.decode(records_of(pk, 0, 0, T, t_cap, W), kb, km, kbits, p),
+                                  O.decode(records_of(pv, 0, 0, T, t_cap, W), vb, vm, vbits, p), 3)
+    for h in range(24):
+        assert rel_l2(out[0, h], ref[h]) <= 2e-5
