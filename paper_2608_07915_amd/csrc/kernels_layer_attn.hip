@@ -126,14 +126,24 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   __syncthreads();
   const int nk = snk;
   // kept coefficients of q~ as two fp16 parts, compacted by slot; group sums
-  for (int e = tid; e < LA_H * 16 * 64; e += 512) {
-    const int h = e >> 10, jj = e & 1023;
-    if ((jj >> 6) >= nk) continue;
-    const float v = h < Hq ? a.qt[((int64_t)b * Hq + h) * d + 64 * sgrp[jj >> 6] + (jj & 63)] : 0.0f;
-    const _Float16 hi = (_Float16)v;
-    const _Float16 lo = (_Float16)(v - (float)hi);
-    qa[h * QP + jj] = __builtin_bit_cast(uint16_t, hi);
-    qa[(LA_H + h) * QP + jj] = __builtin_bit_cast(uint16_t, lo);
+  // (eight loads in flight per thread: the staging is latency-bound otherwise)
+  for (int i0 = 0; i0 < (LA_H * 16 * 64) / 512; i0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int e = tid + 512 * (i0 + r), h = e >> 10, jj = e & 1023;
+      v[r] = (h < Hq && (jj >> 6) < nk) ? a.qt[((int64_t)b * Hq + h) * d + 64 * sgrp[jj >> 6] + (jj & 63)] : 0.0f;
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int e = tid + 512 * (i0 + r), h = e >> 10, jj = e & 1023;
+      if ((jj >> 6) < nk) {
+        const _Float16 hi = (_Float16)v[r];
+        const _Float16 lo = (_Float16)(v[r] - (float)hi);
+        qa[h * QP + jj] = __builtin_bit_cast(uint16_t, hi);
+        qa[(LA_H + h) * QP + jj] = __builtin_bit_cast(uint16_t, lo);
+      }
+    }
   }
   for (int e = tid; e < LA_H * 16; e += 512) {
     const int h = e >> 4, sl = e & 15;
@@ -335,8 +345,9 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   f32x4 acc[1][4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) acc[0][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int zh = tid & 31, zsl = quarter + 4 * (tid >> 5);  // zero-point sums: threads < 128 -> (head, slot)
-  const bool zthr = tid < 128;
+  // zero-point sums: thread -> (head tid & 31, slot quarter + 4 ((tid >> 5) & 3), tokens 16 (tid >> 7) ..)
+  const int zh = tid & 31, zsl = quarter + 4 * ((tid >> 5) & 3), zq = tid >> 7;
+  __shared__ float zred[4][128];
   float zacc = 0.0f;
 
   const int64_t n_tiles = (a.n_tokens + 63) >> 6;
@@ -376,9 +387,17 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
     }
     __syncthreads();
     if (tt + 1 < t_end) load_tile(tt + 1);
-    if (zthr && zsl < nk && zh < Hq) {
+    if (zsl < nk && zh < Hq) {
+      const float* pr = pl + zh * LA_ROW + 16 * zq;
+      const uint32_t* mr = rec + zsl * LA_ROW + 16 * zq;
       float z = 0.0f;
-      for (int t = 0; t < 64; ++t) z = __builtin_fmaf(pl[zh * LA_ROW + t], h2f(rec[zsl * LA_ROW + t] >> 16), z);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(pr + 4 * q);
+        const u32x4 mv = *reinterpret_cast<const u32x4*>(mr + 4 * q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) z = __builtin_fmaf(pv[e], h2f(mv[e] >> 16), z);
+      }
       zacc += z;
     }
 #pragma unroll
@@ -449,7 +468,10 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
         }
     }
   }
-  if (zthr && zsl < nk && zh < Hq) pb[(int64_t)zh * (d + 16) + d + sgrp[zsl]] = zacc;
+  zred[zq][tid & 127] = zacc;
+  __syncthreads();
+  if (tid < 128 && zsl < nk && zh < Hq)
+    pb[(int64_t)zh * (d + 16) + d + sgrp[zsl]] = (zred[0][tid] + zred[1][tid]) + (zred[2][tid] + zred[3][tid]);
 }
 
 // ---------------------------------------------------------------------------
