@@ -182,3 +182,41 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(_lib, "LIB_PATH", "/nonexistent/libspectra.so")
     with pytest.raises(_lib.LibraryMissing):
         S.spectra_allocate_bits(np.ones(128), S.Params())
+
+
+def test_layer_geometry_argument_errors(lib):
+    # the per-layer geometry (d = heads x 128, groups of 64): accepted by fit / encode /
+    # decode / layer attention only, checked on the host before anything is launched
+    cl = _lib.spectra_codec()
+    pl = S.Params(head_dim=1024, group_size=64, ratio=8.0).c()
+    assert lib.spectra_codec_init(ctypes.byref(cl), ctypes.byref(pl), 2) == 0
+    assert cl.record_words == 64
+    cl.basis = cl.mean = cl.var = cl.bits = 256
+    # the per-head entry points refuse it
+    assert lib.spectra_decode_attention(ctypes.byref(cl), ctypes.byref(cl), 256, 256, 64, 8, 256, 1, 1, 8, 8, 0.0,
+                                        256, 256, 1 << 20, None) == -2
+    assert b"per-layer geometry" in lib.spectra_last_error()
+    # 1024-wide records beyond 128 words are not run on the GPU
+    c4 = _lib.spectra_codec()
+    p4 = S.Params(head_dim=1024, group_size=64, ratio=2.0).c()
+    assert lib.spectra_codec_init(ctypes.byref(c4), ctypes.byref(p4), 1) == 0
+    c4.basis = c4.mean = c4.var = c4.bits = 256
+    assert lib.spectra_decode(ctypes.byref(c4), 256, 64, 0, 8, 256, None) == -2
+    # encode takes bf16 tokens only in this geometry; fp32 is refused
+    assert lib.spectra_encode(ctypes.byref(cl), 256, 0, 8192, 1024, 0, 8, 256, 64, None) == -2
+    # layer attention: kv heads x 128 must equal the width, at most 32 query heads, workspace
+    ws = lib.spectra_layer_attention_workspace_bytes(ctypes.byref(cl), 1, 32, 100)
+    assert ws > 0
+    args = lambda n_q, n_kv, wsb: (ctypes.byref(cl), ctypes.byref(cl), 256, 256, 128, 100, 256, 1, 1, n_q, n_kv, 0.0,
+                                   256, 256, wsb, None)
+    assert lib.spectra_layer_decode_attention(*args(32, 4, ws)) == -1
+    assert lib.spectra_layer_decode_attention(*args(48, 8, ws)) == -1
+    assert lib.spectra_layer_decode_attention(*args(32, 8, 1024)) == -4
+    # the square-root split belongs to the per-layer geometry
+    ch = _lib.spectra_codec()
+    assert lib.spectra_codec_init(ctypes.byref(ch), ctypes.byref(S.Params().c()), 1) == 0
+    ch.basis = ch.mean = ch.var = ch.bits = ch.lscale = 256
+    assert lib.spectra_decode(ctypes.byref(ch), 256, 64, 0, 8, 256, None) == -2
+    assert b"square-root" in lib.spectra_last_error()
+    cl.lscale = 256
+    assert lib.spectra_layer_decode_attention(*args(32, 8, ws)) == -2
