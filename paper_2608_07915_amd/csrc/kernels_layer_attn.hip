@@ -13,7 +13,7 @@
 //                         token's scale and zero point applied after; chunk max and sum;
 //   layer_stats_kernel    softmax max and sum of every head over the chunks;
 //   layer_values_kernel   p = exp2(s - max over all chunks), then per kept value group
-//                         sum_t p_t s_t q_t on v_mfma_f32_16x16x32_bf16 (weights as three
+//                         sum_t p_t s_t q_t on v_mfma_f32_16x16x32_bf16 (weights as two
 //                         bf16 parts, codes of eight consecutive tokens read from the
 //                         word-major tile) and sum_t p_t z_t;
 //   layer_combine_kernel  sums the chunk partials, divides by the softmax sum, adds m_V;
@@ -409,21 +409,25 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           const int tk0 = 32 * ks + 8 * kg;
-          // weights p_t s_t of head 16 hb + c16 for tokens tk0 .. tk0 + 7 as three bf16
-          // parts (the fp32 exponent range: p_t s_t spans many decades below 1)
-          bf16x8 wp[3];
+          // weights p_t s_t of head 16 hb + c16 for tokens tk0 .. tk0 + 7 as two bf16 parts:
+          // the fp32 exponent range (p_t s_t spans many decades below 1) and 16 significant
+          // bits (relative error below 2^-17 per weight; a third part changed the output by
+          // 1e-6 relative and cost 7% of the call)
+          bf16x8 wp[2];
           {
             const float* pr = pl + (16 * hb + c16) * LA_ROW + tk0;
             const f32x4 p0 = *reinterpret_cast<const f32x4*>(pr), p1 = *reinterpret_cast<const f32x4*>(pr + 4);
             const u32x4 m0 = *reinterpret_cast<const u32x4*>(rec + sl * LA_ROW + tk0);
             const u32x4 m1 = *reinterpret_cast<const u32x4*>(rec + sl * LA_ROW + tk0 + 4);
-            uint32_t q0[8], q1[8], q2[8];
+            uint32_t q0[8], q1[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              split3((e < 4 ? p0[e] : p1[e - 4]) * h2f(e < 4 ? m0[e] : m1[e - 4]), q0[e], q1[e], q2[e]);
+            for (int e = 0; e < 8; ++e) {
+              const float wv = (e < 4 ? p0[e] : p1[e - 4]) * h2f(e < 4 ? m0[e] : m1[e - 4]);
+              q0[e] = f2bf(wv);
+              q1[e] = f2bf(wv - bf2f(q0[e]));
+            }
             wp[0] = as_bf16x8(u32x4{pack2(q0[0], q0[1]), pack2(q0[2], q0[3]), pack2(q0[4], q0[5]), pack2(q0[6], q0[7])});
             wp[1] = as_bf16x8(u32x4{pack2(q1[0], q1[1]), pack2(q1[2], q1[3]), pack2(q1[4], q1[5]), pack2(q1[6], q1[7])});
-            wp[2] = as_bf16x8(u32x4{pack2(q2[0], q2[1]), pack2(q2[2], q2[3]), pack2(q2[4], q2[5]), pack2(q2[6], q2[7])});
           }
 #pragma unroll
           for (int cb = 0; cb < 4; ++cb) {
@@ -446,7 +450,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
             const bf16x8 cv = as_bf16x8(u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]),
                                               int_to_bf16_pair(cd[4], cd[5]), int_to_bf16_pair(cd[6], cd[7])});
 #pragma unroll
-            for (int q = 0; q < 3; ++q)
+            for (int q = 0; q < 2; ++q)
               acc[i][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wp[q], cv, acc[i][cb], 0, 0, 0);
           }
         }
