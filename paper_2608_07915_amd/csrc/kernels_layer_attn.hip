@@ -89,7 +89,19 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
     acc = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
   }
   qtl[tid] = acc;
-  if (j < d) a.qt[((int64_t)b * a.n_q_heads + h) * d + j] = acc;
+  if (j < d) {
+    a.qt[((int64_t)b * a.n_q_heads + h) * d + j] = acc;
+    const int g = j >> 6;
+    if (bits_s[g] > 0) {  // fp16 parts for the score pass, at the group's kept slot
+      int slot = 0;
+      for (int gg = 0; gg < g; ++gg) slot += bits_s[gg] > 0 ? 1 : 0;
+      const _Float16 hi = (_Float16)acc;
+      const _Float16 lo = (_Float16)(acc - (float)hi);
+      uint16_t* qh = a.qh + (int64_t)b * 2 * LA_H * d;
+      qh[(int64_t)h * d + 64 * slot + (j & 63)] = __builtin_bit_cast(uint16_t, hi);
+      qh[(int64_t)(LA_H + h) * d + 64 * slot + (j & 63)] = __builtin_bit_cast(uint16_t, lo);
+    }
+  }
   __syncthreads();
   // group sums (only the groups of this workgroup's coefficients; the score pass reads kept groups only)
   if (tid < 4 && 4 * (int)blockIdx.z + tid < ng) {
@@ -126,22 +138,24 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   __syncthreads();
   const int nk = snk;
   // kept coefficients of q~ as two fp16 parts, compacted by slot; group sums
-  // (eight loads in flight per thread: the staging is latency-bound otherwise)
-  for (int i0 = 0; i0 < (LA_H * 16 * 64) / 512; i0 += 8) {
-    float v[8];
+  // copied as written by the query pass (16-byte pieces, eight in flight per thread);
+  // rows of heads past n_q_heads are zero
+  {
+    const uint16_t* qh = a.qh + (int64_t)b * 2 * LA_H * d;
+    const int pieces = nk * 8;  // 16-byte pieces per row
+    for (int i0 = 0; i0 < (2 * LA_H * 16 * 8) / 512; i0 += 8) {
+      u32x4 v[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int e = tid + 512 * (i0 + r), h = e >> 10, jj = e & 1023;
-      v[r] = (h < Hq && (jj >> 6) < nk) ? a.qt[((int64_t)b * Hq + h) * d + 64 * sgrp[jj >> 6] + (jj & 63)] : 0.0f;
-    }
+      for (int r = 0; r < 8; ++r) {
+        const int e = tid + 512 * (i0 + r), row = e >> 7, pc = e & 127;
+        const int h = row & (LA_H - 1);
+        v[r] = (h < Hq && pc < pieces) ? *reinterpret_cast<const u32x4*>(qh + (int64_t)row * d + 8 * pc)
+                                       : u32x4{0u, 0u, 0u, 0u};
+      }
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int e = tid + 512 * (i0 + r), h = e >> 10, jj = e & 1023;
-      if ((jj >> 6) < nk) {
-        const _Float16 hi = (_Float16)v[r];
-        const _Float16 lo = (_Float16)(v[r] - (float)hi);
-        qa[h * QP + jj] = __builtin_bit_cast(uint16_t, hi);
-        qa[(LA_H + h) * QP + jj] = __builtin_bit_cast(uint16_t, lo);
+      for (int r = 0; r < 8; ++r) {
+        const int e = tid + 512 * (i0 + r), row = e >> 7, pc = e & 127;
+        if (pc < pieces) *reinterpret_cast<u32x4*>(qa + row * QP + 8 * pc) = v[r];
       }
     }
   }
@@ -573,8 +587,8 @@ size_t layer_attention_ws_floats(int32_t batch, int32_t n_q_heads, int32_t d, in
   const int64_t nv = layer_value_chunks(batch, n_tokens, &tpc);
   const int64_t B = batch, H = n_q_heads;
   auto r64 = [](int64_t n) { return (n + 63) / 64 * 64; };  // 256-byte aligned sections
-  return (size_t)(r64(B * H * d) + r64(B * H * 16) + r64(B * H * 2) + r64(B * H * n_tokens) + r64(B * nch * H * 2) +
-                  r64(B * nv * H * (d + 16)));
+  return (size_t)(r64(B * H * d) + r64(B * LA_H * d) + r64(B * H * 16) + r64(B * H * 2) + r64(B * H * n_tokens) +
+                  r64(B * nch * H * 2) + r64(B * nv * H * (d + 16)));
 }
 
 void layer_attention_ws_layout(LayerAttnArgs& a, float* ws) {
@@ -583,7 +597,8 @@ void layer_attention_ws_layout(LayerAttnArgs& a, float* ws) {
   const int64_t B = a.batch, H = a.n_q_heads;
   auto r64 = [](int64_t n) { return (n + 63) / 64 * 64; };
   a.qt = ws;
-  a.qsum = a.qt + r64(B * H * a.d);
+  a.qh = reinterpret_cast<uint16_t*>(a.qt + r64(B * H * a.d));  // 2 x 32 x d halves = 32 x d floats
+  a.qsum = a.qt + r64(B * H * a.d) + r64(B * LA_H * a.d);
   a.ml = a.qsum + r64(B * H * 16);
   a.scores = a.ml + r64(B * H * 2);
   a.stats = a.scores + r64(B * H * a.n_tokens);

@@ -71,6 +71,7 @@ struct LayerAttnArgs {
   int32_t nv_chunks, v_tiles_per_chunk;  // value pass: token chunks (x 4 kept-slot quarters)
   float* qt;      // [batch][Hq][d]: scale log2(e) q_h V_K[kv rows], 0 on dropped groups
   float* ml;      // [batch][Hq][2]: softmax max and sum over all tokens
+  uint16_t* qh;   // [batch][2][32][d] fp16: qt as high and low parts, kept groups in slot order
   float* qsum;    // [batch][Hq][16]: per group sums of qt
   float* scores;  // [batch][Hq][n_tokens] (log2 domain)
   float* stats;   // [batch][n_chunks][Hq][2]: chunk max, chunk sum of exp2(s - max)
