@@ -67,11 +67,19 @@ __device__ __forceinline__ bool layer_bits_ok(const uint8_t* __restrict__ bits_s
 __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
   __shared__ float qv[128];
   __shared__ float qtl[256];
+  __shared__ int slot_of[16];  // kept rank of each group
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int d = a.d, ng = d / 64;
   const int j = 256 * blockIdx.z + tid;
   const int kv = h / (a.n_q_heads / a.n_kv_heads);
   const uint8_t* bits_s = a.bits_k + (int64_t)b * ng;
+  if (tid == 0) {
+    int n = 0;
+    for (int g = 0; g < ng; ++g) {
+      slot_of[g] = n;
+      n += bits_s[g] > 0 ? 1 : 0;
+    }
+  }
   if (tid < 128) {
     const int64_t qi = ((int64_t)b * a.n_q_heads + h) * 128 + tid;
     qv[tid] = (a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi])) *
@@ -93,8 +101,7 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
     a.qt[((int64_t)b * a.n_q_heads + h) * d + j] = acc;
     const int g = j >> 6;
     if (bits_s[g] > 0) {  // fp16 parts for the score pass, at the group's kept slot
-      int slot = 0;
-      for (int gg = 0; gg < g; ++gg) slot += bits_s[gg] > 0 ? 1 : 0;
+      const int slot = slot_of[g];
       const _Float16 hi = (_Float16)acc;
       const _Float16 lo = (_Float16)(acc - (float)hi);
       uint16_t* qh = a.qh + (int64_t)b * 2 * LA_H * d;
@@ -136,7 +143,7 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   const bool ok = layer_bits_ok(bits_s, ng, Wk);
   if (tid == 0) snk = ok ? layer_slots(bits_s, ng, sgrp, sbw, spay) : 0;
   __syncthreads();
-  const int nk = snk;
+  const int nk = __builtin_amdgcn_readfirstlane(snk);
   // kept coefficients of q~ as two fp16 parts, compacted by slot; group sums
   // copied as written by the query pass (16-byte pieces, eight in flight per thread);
   // rows of heads past n_q_heads are zero
@@ -199,14 +206,16 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
     const int u = 16 * tb + c16;
     f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
     for (int sl = sh; sl < nk; sl += 2) {
-      const int pay = spay[sl];
+      // slot tables are uniform: scalar registers, scalar branches on the width
+      const int pay = __builtin_amdgcn_readfirstlane(spay[sl]);
+      const int bw = __builtin_amdgcn_readfirstlane(sbw[sl]);
       const uint32_t m = rec[sl * LA_ROW + u];
       const float st = h2f(m), zt = h2f(m >> 16);
       f32x4 g[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         f16x8v bop;
-        with_bits(sbw[sl], [&](auto bc) {
+        with_bits(bw, [&](auto bc) {
           constexpr int B = decltype(bc)::value;
           uint32_t cd[8];
           extract8<B>([&](int i) { return rec[(pay + i) * LA_ROW + u]; }, 32 * ks + 8 * kg, cd);
@@ -353,7 +362,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   if (tid == 0) snk = ok ? layer_slots(bits_s, ng, sgrp, sbw, spay) : 0;
   if (tid < LA_H) mh[tid] = tid < Hq ? a.ml[((int64_t)b * Hq + tid) * 2] : -__builtin_inff();
   __syncthreads();
-  const int nk = snk;
+  const int nk = __builtin_amdgcn_readfirstlane(snk);
   // wavefront: head block hb, kept slot quarter + 4 si (its four 16-coefficient column blocks)
   const int hb = wave & 1, si = wave >> 1;
   f32x4 acc[1][4];
@@ -418,7 +427,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
     for (int i = 0; i < 1; ++i) {
       const int sl = quarter + 4 * si;
       if (sl < nk) {
-        const int B = sbw[sl], pay = spay[sl];
+        const int B = __builtin_amdgcn_readfirstlane(sbw[sl]), pay = __builtin_amdgcn_readfirstlane(spay[sl]);
         const uint32_t M = (1u << B) - 1u;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
