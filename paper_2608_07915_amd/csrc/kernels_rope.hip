@@ -109,7 +109,8 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   __shared__ float mst[NH], lst[NH], zst[NH][NG];
 
   const int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar slot and role selection
   const int s = b * a.n_kv_heads + kv;
   const int nqh = a.n_qh;
   const int Wk = a.Wk, Wv = a.Wv;
