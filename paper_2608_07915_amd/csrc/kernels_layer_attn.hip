@@ -137,7 +137,7 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   float* red = qs + LA_H * 16;                                           // [4][LA_H][2]
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
   const int chunk = blockIdx.x, b = blockIdx.y;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
   const int Hq = a.n_q_heads;
   const uint8_t* bits_s = a.bits_k + (int64_t)b * ng;
   const bool ok = layer_bits_ok(bits_s, ng, Wk);
@@ -310,7 +310,7 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void layer_stats_kernel(LayerAttnArgs a) {
   __shared__ float rm[4], rl[4];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int Hq = a.n_q_heads;
   float m = -__builtin_inff(), l = 0.0f;
   for (int c = tid; c < a.n_chunks; c += 256) {
@@ -355,7 +355,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   __shared__ float mh[LA_H];
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
   const int chunk = blockIdx.x, quarter = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
   const int d = a.d, ng = d / 64, Wv = a.Wv, Hq = a.n_q_heads;
   const uint8_t* bits_s = a.bits_v + (int64_t)b * ng;
   const bool ok = layer_bits_ok(bits_s, ng, Wv) && layer_bits_ok(a.bits_k + (int64_t)b * ng, ng, a.Wk);
@@ -543,7 +543,7 @@ __global__ __launch_bounds__(256) void layer_combine_kernel(LayerAttnArgs a) {
 // wavefront (d / 64 values per lane), then a wavefront sum
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void layer_rotate_kernel(LayerAttnArgs a) {
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int d = a.d, Hq = a.n_q_heads;
   const int kv = h / (Hq / a.n_kv_heads);
   const float* cfv = a.qt + ((int64_t)b * Hq + h) * d;
