@@ -248,3 +248,36 @@ def test_layer_attention_three_heads_d384():
                                   O.decode(records_of(pv, 0, 0, T, t_cap, W), vb, vm, vbits, p), 3)
     for h in range(24):
         assert rel_l2(out[0, h], ref[h]) <= 2e-5
+
+
+def test_layer_attention_fp32_queries_and_softmax_scale():
+    # fp32 queries and an explicit softmax scale take the same path as bf16 ones
+    w = synth.WORKLOADS["qwen_layer_8x"]
+    T = 640
+    xk = synth.numpy_layer_stream(w, 0, 0, 0, T_FIT)[None]
+    xv = synth.numpy_layer_stream(w, 0, 0, 1, T_FIT)[None]
+    d = xk.shape[2]
+    n_kv = d // 128
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    ck, cv = S.Codec(sparams(p), 1), S.Codec(sparams(p), 1)
+    S.spectra_fit_basis(ck, to_device(xk, w.dtype))
+    S.spectra_fit_basis(cv, to_device(xv, w.dtype))
+    t_cap = 704
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
+    S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
+    rng = np.random.default_rng(9)
+    q32 = rng.standard_normal((1, w.n_q_heads, 128)).astype(np.float32) * 2.0
+    scale = 0.05
+    out = S.spectra_layer_decode_attention(ck, cv, pk, pv, t_cap, T, torch.from_numpy(q32).cuda(), n_kv,
+                                           softmax_scale=scale).cpu().numpy()
+    W = O.record_words(p)
+    kb, km, kbits = codec_state(ck, 0)
+    vb, vm, vbits = codec_state(cv, 0)
+    kh = O.decode(records_of(pk, 0, 0, T, t_cap, W), kb, km, kbits, p)
+    vh = O.decode(records_of(pv, 0, 0, T, t_cap, W), vb, vm, vbits, p)
+    k = kh.reshape(T, n_kv, 128).transpose(1, 0, 2)
+    v = vh.reshape(T, n_kv, 128).transpose(1, 0, 2)
+    ref = O.attention_mode_a(q32[0].astype(np.float64), k, v, scale)
+    for h in range(w.n_q_heads):
+        assert rel_l2(out[0, h], ref[h]) <= 2e-5
