@@ -347,14 +347,15 @@ __global__ __launch_bounds__(256) void layer_stats_kernel(LayerAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Values: one workgroup per (token chunk, quarter of the kept slots, sequence)
+// Values: one workgroup per (token chunk, block of 16 query heads, sequence); wavefront w
+// takes kept value slots w and w + 8
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t rec[LA_WMAX * LA_ROW];
-  __shared__ __attribute__((aligned(16))) float pl[LA_H * LA_ROW];
+  __shared__ __attribute__((aligned(16))) float pl[16 * LA_ROW];
   __shared__ float mh[LA_H];
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
-  const int chunk = blockIdx.x, quarter = blockIdx.y, b = blockIdx.z;
+  const int chunk = blockIdx.x, hbk = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
   const int d = a.d, ng = d / 64, Wv = a.Wv, Hq = a.n_q_heads;
   const uint8_t* bits_s = a.bits_v + (int64_t)b * ng;
@@ -363,14 +364,16 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   if (tid < LA_H) mh[tid] = tid < Hq ? a.ml[((int64_t)b * Hq + tid) * 2] : -__builtin_inff();
   __syncthreads();
   const int nk = __builtin_amdgcn_readfirstlane(snk);
-  // wavefront: head block hb, kept slot quarter + 4 si (its four 16-coefficient column blocks)
-  const int hb = wave & 1, si = wave >> 1;
-  f32x4 acc[1][4];
+  // workgroup: heads 16 hbk .. 16 hbk + 15; wavefront: kept slots wave, wave + 8
+  const int hb = hbk;
+  f32x4 acc[2][4];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) acc[0][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // zero-point sums: thread -> (head tid & 31, slot quarter + 4 ((tid >> 5) & 3), tokens 16 (tid >> 7) ..)
-  const int zh = tid & 31, zsl = quarter + 4 * ((tid >> 5) & 3), zq = tid >> 7;
-  __shared__ float zred[4][128];
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // zero-point sums: thread -> (head 16 hbk + (tid & 15), slot (tid >> 4) & 15, tokens 32 (tid >> 8) ..)
+  const int zhl = tid & 15, zh = 16 * hbk + zhl, zsl = (tid >> 4) & 15, zq = tid >> 8;
+  __shared__ float zred[2][256];
   float zacc = 0.0f;
 
   const int64_t n_tiles = (a.n_tokens + 63) >> 6;
@@ -378,7 +381,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   const int64_t t_end = t_begin + a.v_tiles_per_chunk < n_tiles ? t_begin + a.v_tiles_per_chunk : n_tiles;
   const uint32_t* vp = a.packed_v + (int64_t)b * a.t_cap * Wv;
   constexpr int PF = 64 * LA_WMAX / 512;       // record words per thread and tile
-  constexpr int PS = LA_H * 64 / 512;          // scores per thread and tile
+  constexpr int PS = 16 * 64 / 512;            // scores per thread and tile
   uint32_t pre[PF];
   float spre[PS];
   auto load_tile = [&](int64_t tt) {
@@ -389,7 +392,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < PS; ++i) {
-      const int e = tid + 512 * i, h = e >> 6;
+      const int e = tid + 512 * i, h = 16 * hbk + (e >> 6);
       const int64_t tok = tt * 64 + (e & 63);
       spre[i] = (h < Hq && tok < a.n_tokens) ? a.scores[((int64_t)b * Hq + h) * a.n_tokens + tok] : -__builtin_inff();
     }
@@ -404,18 +407,18 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < PS; ++i) {
-      const int e = tid + 512 * i, h = e >> 6;
+      const int e = tid + 512 * i, hl = e >> 6, h = 16 * hbk + hl;
       const float x = spre[i];
-      pl[h * LA_ROW + (e & 63)] = (x != -__builtin_inff() && mh[h] != -__builtin_inff()) ? __builtin_amdgcn_exp2f(x - mh[h]) : 0.0f;
+      pl[hl * LA_ROW + (e & 63)] = (x != -__builtin_inff() && mh[h] != -__builtin_inff()) ? __builtin_amdgcn_exp2f(x - mh[h]) : 0.0f;
     }
     __syncthreads();
     if (tt + 1 < t_end) load_tile(tt + 1);
     if (zsl < nk && zh < Hq) {
-      const float* pr = pl + zh * LA_ROW + 16 * zq;
-      const uint32_t* mr = rec + zsl * LA_ROW + 16 * zq;
+      const float* pr = pl + zhl * LA_ROW + 32 * zq;
+      const uint32_t* mr = rec + zsl * LA_ROW + 32 * zq;
       float z = 0.0f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < 8; ++q) {
         const f32x4 pv = *reinterpret_cast<const f32x4*>(pr + 4 * q);
         const u32x4 mv = *reinterpret_cast<const u32x4*>(mr + 4 * q);
 #pragma unroll
@@ -424,8 +427,8 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
       zacc += z;
     }
 #pragma unroll
-    for (int i = 0; i < 1; ++i) {
-      const int sl = quarter + 4 * si;
+    for (int i = 0; i < 2; ++i) {
+      const int sl = wave + 8 * i;
       if (sl < nk) {
         const int B = __builtin_amdgcn_readfirstlane(sbw[sl]), pay = __builtin_amdgcn_readfirstlane(spay[sl]);
         const uint32_t M = (1u << B) - 1u;
@@ -438,7 +441,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
           // 1e-6 relative and cost 7% of the call)
           bf16x8 wp[2];
           {
-            const float* pr = pl + (16 * hb + c16) * LA_ROW + tk0;
+            const float* pr = pl + c16 * LA_ROW + tk0;
             const f32x4 p0 = *reinterpret_cast<const f32x4*>(pr), p1 = *reinterpret_cast<const f32x4*>(pr + 4);
             const u32x4 m0 = *reinterpret_cast<const u32x4*>(rec + sl * LA_ROW + tk0);
             const u32x4 m1 = *reinterpret_cast<const u32x4*>(rec + sl * LA_ROW + tk0 + 4);
@@ -483,8 +486,8 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   // partials: lane holds rows (heads 16 hb + 4 kg + j) of column (coefficient 16 cb + c16)
   float* pb = a.part + ((int64_t)b * a.nv_chunks + chunk) * Hq * (d + 16);
 #pragma unroll
-  for (int i = 0; i < 1; ++i) {
-    const int sl = quarter + 4 * si;
+  for (int i = 0; i < 2; ++i) {
+    const int sl = wave + 8 * i;
     if (sl < nk) {
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb)
@@ -495,10 +498,9 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
         }
     }
   }
-  zred[zq][tid & 127] = zacc;
+  zred[zq][tid & 255] = zacc;
   __syncthreads();
-  if (tid < 128 && zsl < nk && zh < Hq)
-    pb[(int64_t)zh * (d + 16) + d + sgrp[zsl]] = (zred[0][tid] + zred[1][tid]) + (zred[2][tid] + zred[3][tid]);
+  if (tid < 256 && zsl < nk && zh < Hq) pb[(int64_t)zh * (d + 16) + d + sgrp[zsl]] = zred[0][tid] + zred[1][tid];
 }
 
 // ---------------------------------------------------------------------------
@@ -579,11 +581,11 @@ int32_t layer_attention_chunks(int32_t batch, int64_t n_tokens, int32_t* tiles_p
   return (int32_t)((n_tiles + tpc - 1) / tpc);
 }
 
-// Value pass: about 256 workgroups over (chunk, slot quarter, sequence), at least 8 tiles
-// each (twice as many, two per CU, measured slower: more partials, no faster tiles).
+// Value pass: about 256 workgroups over (chunk, head block of 16, sequence), at least 8
+// tiles each.
 int32_t layer_value_chunks(int32_t batch, int64_t n_tokens, int32_t* tiles_per_chunk) {
   const int64_t n_tiles = (n_tokens + 63) / 64;
-  const int64_t want = (64 + batch - 1) / batch;
+  const int64_t want = (128 + batch - 1) / batch;
   int64_t tpc = (n_tiles + want - 1) / want;
   if (tpc < 8) tpc = 8;
   *tiles_per_chunk = (int32_t)tpc;
@@ -626,7 +628,7 @@ hipError_t launch_layer_attention(const LayerAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(layer_stats_kernel, dim3(a.n_q_heads, a.batch), dim3(256), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layer_values_kernel, dim3(a.nv_chunks, 4, a.batch), dim3(512), 0, st, a);
+  hipLaunchKernelGGL(layer_values_kernel, dim3(a.nv_chunks, 2, a.batch), dim3(512), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(layer_combine_kernel, dim3(a.n_q_heads, a.batch, (a.d + 255) / 256), dim3(256), 0, st, a);

@@ -68,7 +68,7 @@ struct LayerAttnArgs {
   int32_t batch, n_q_heads, n_kv_heads, d, Wk, Wv;
   float scale_log2;
   int32_t n_chunks, tiles_per_chunk;     // score pass: token chunks
-  int32_t nv_chunks, v_tiles_per_chunk;  // value pass: token chunks (x 4 kept-slot quarters)
+  int32_t nv_chunks, v_tiles_per_chunk;  // value pass: token chunks (x 2 head blocks)
   float* qt;      // [batch][Hq][d]: scale log2(e) q_h V_K[kv rows], 0 on dropped groups
   float* ml;      // [batch][Hq][2]: softmax max and sum over all tokens
   uint16_t* qh;   // [batch][2][32][d] fp16: qt as high and low parts, kept groups in slot order
