@@ -126,3 +126,50 @@ def test_largest_capacity_offsets():
         want = (e_end @ vh + e_0 * v0) / (e_end.sum() + e_0)
         # fp32 running sums over ~1400 tiles per lane: rounding up to ~1400 * 2^-24 relative
         assert rel_l2(out[h], want) <= 2e-4, h
+
+
+def test_full_size_per_layer_latent_sampled():
+    # the per-layer geometry at the benchmark's size, as the bench runs it: one Llama layer's
+    # keys and values as 1024-wide streams (131104 tokens), fitted on the first 8192 tokens,
+    # encoded, decoded and attended by the 32 query heads; checked against the oracle on a
+    # sample of tokens (records, reconstruction) and in full for the attention outputs
+    w = synth.WORKLOADS["llama_model_131k_8x"]
+    dev = torch.device("cuda:0")
+    H, Hq = w.n_kv_heads, w.n_q_heads
+    n = w.n_tokens + w.n_append
+    t_cap = (n + 63) // 64 * 64
+    d = H * 128
+    p = O.Params(head_dim=d, group_size=64, ratio=w.ratio)
+    xs_dev, codecs, packs = [], [], []
+    for tensor in (0, 1):
+        x = synth.device_layer_stream(w, 0, 0, tensor, n, dev)
+        c = S.Codec(sparams(p), 1)
+        S.spectra_fit_basis(c, x[:, :8192])
+        pk = c.empty_packed(t_cap)
+        S.spectra_encode(c, x, 0, pk, t_cap)
+        xs_dev.append(x)
+        codecs.append(c)
+        packs.append(pk)
+    q = synth.device_queries(w, 0, 0, dev)                                 # [1, Hq, 128]
+    out = S.spectra_layer_decode_attention(codecs[0], codecs[1], packs[0], packs[1], t_cap, n, q, H).cpu().numpy()
+    rng = np.random.default_rng(4)
+    sample = np.sort(rng.choice(n, size=1500, replace=False))
+    sample[-1] = n - 1
+    dec_full = []
+    for c, pk, x in zip(codecs, packs, xs_dev):
+        basis, mean, bits = codec_state(c, 0)
+        W = c.record_words
+        words = pk.cpu().numpy().view(np.uint32)
+        rec = np.stack([words[O.physical_index(0, np.arange(n), w_, t_cap, W)] for w_ in range(W)], axis=1)
+        xs = host_values(x[0, sample])
+        check_encoded_stream(xs, basis, mean, bits, p, rec[sample], dot_bound=True)
+        dec = S.spectra_decode(c, pk, t_cap, 0, n).cpu().numpy()[0]
+        dec_o = O.decode(rec, basis, mean, bits, p)
+        assert rel_l2(dec[sample], dec_o[sample]) <= 1e-6
+        dec_full.append(dec_o)
+    q64 = host_values(q)[0]
+    k = dec_full[0].reshape(n, H, 128).transpose(1, 0, 2)
+    v = dec_full[1].reshape(n, H, 128).transpose(1, 0, 2)
+    ref = O.attention_mode_a(q64, k, v)
+    for h in range(Hq):
+        assert rel_l2(out[0, h], ref[h]) <= 2e-5, (h, rel_l2(out[0, h], ref[h]))
