@@ -4,7 +4,8 @@ prefill tokens), fitted and encoded as the benchmark does, then two decode
 steps of spectra_decode_step. Sampled against the oracle: the records of two
 KV heads (K and V streams, every token, including the appended ones) and the
 attention outputs of their eight query heads, over the GPU's bytes and over the
-oracle's own encoding (App. E, Mode A)."""
+oracle's own encoding (App. E, Mode A). Also at that size: the per-layer geometry
+(1024-wide latents) and attention with rotary embeddings, as the benchmark runs them."""
 import numpy as np
 import pytest
 
@@ -171,5 +172,41 @@ def test_full_size_per_layer_latent_sampled():
     k = dec_full[0].reshape(n, H, 128).transpose(1, 0, 2)
     v = dec_full[1].reshape(n, H, 128).transpose(1, 0, 2)
     ref = O.attention_mode_a(q64, k, v)
+    for h in range(Hq):
+        assert rel_l2(out[0, h], ref[h]) <= 2e-5, (h, rel_l2(out[0, h], ref[h]))
+
+
+def test_full_size_rope_attention():
+    # Mode A with RoPE at the benchmark's size and launch shape (one layer, 8 KV heads, 32
+    # query heads, 131104 slots, rope base 500000): every output against the oracle's
+    # rotary attention over the reconstruction of the GPU's bytes
+    w = synth.WORKLOADS["llama_model_131k_8x"]
+    dev = torch.device("cuda:0")
+    H, Hq = w.n_kv_heads, w.n_q_heads
+    n = w.n_tokens + w.n_append
+    t_cap = (n + 63) // 64 * 64
+    p = O.Params(ratio=w.ratio)
+    inv_freq = (500000.0 ** (-np.arange(64, dtype=np.float64) / 64)).astype(np.float32)
+    codecs, packs = [], []
+    for tensor in (0, 1):
+        x = synth.device_streams(w, tensor, 0, n, dev)
+        c = S.Codec(sparams(p), H)
+        S.spectra_fit_basis(c, x)
+        pk = c.empty_packed(t_cap)
+        S.spectra_encode(c, x, 0, pk, t_cap)
+        codecs.append(c)
+        packs.append(pk)
+        del x
+    q = synth.device_queries(w, 0, 0, dev)
+    out = S.spectra_decode_attention_rope(codecs[0], codecs[1], packs[0], packs[1], t_cap, n, q, H,
+                                          torch.from_numpy(inv_freq).to(dev)).cpu().numpy()
+    hats = []
+    for c, pk in zip(codecs, packs):
+        rows = []
+        for s in range(H):
+            basis, mean, bits = codec_state(c, s)
+            rows.append(O.decode(records_of(pk, s, 0, n, t_cap, c.record_words), basis, mean, bits, p))
+        hats.append(np.stack(rows))
+    ref = O.attention_mode_a_rope(host_values(q)[0], hats[0], hats[1], inv_freq, n - 1)
     for h in range(Hq):
         assert rel_l2(out[0, h], ref[h]) <= 2e-5, (h, rel_l2(out[0, h], ref[h]))
