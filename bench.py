@@ -285,7 +285,7 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
 def main():
     args = _parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "bench.py runs on one GPU only: the codec streams shard without communication (see the sharding notes); multi-GPU runs are not implemented",
+        print(json.dumps({"error": "bench.py runs on one GPU only; multi-GPU runs are not implemented (codec streams are independent and shard without communication)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     if args.fit_weights:
