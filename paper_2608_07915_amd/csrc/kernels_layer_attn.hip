@@ -506,37 +506,48 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
 // ---------------------------------------------------------------------------
 // Combine: c[j] = (sum over value chunks of the coefficient sums + zero-point sums)
 // / softmax sum + m_V[j], written over q~ (no longer needed); grid (heads, sequences,
-// d / 256), one coefficient per thread
+// d / 64 groups)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void layer_combine_kernel(LayerAttnArgs a) {
+  // thread -> (coefficient 64 z + (tid & 63), every fourth chunk from tid >> 6): four short
+  // chains of loads instead of one long one, summed in LDS in a fixed order
+  __shared__ float ps[4][64], pz[4][64];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int d = a.d, ng = d / 64, Hq = a.n_q_heads;
-  const int j = 256 * blockIdx.z + tid;
-  if (j >= d) return;
+  const int j = 64 * blockIdx.z + (tid & 63), part = tid >> 6;
   const uint8_t* bv = a.bits_v + (int64_t)b * ng;
   const bool ok = layer_bits_ok(bv, ng, a.Wv) && layer_bits_ok(a.bits_k + (int64_t)b * ng, ng, a.Wk);
-  const float l = a.ml[((int64_t)b * Hq + h) * 2 + 1];
-  const float inv_l = l > 0.0f ? 1.0f / l : 0.0f;
-  const int g = j >> 6;
-  float c = 0.0f;
-  if (ok && bv[g] > 0) {
-    float s[4] = {0.f, 0.f, 0.f, 0.f}, z[4] = {0.f, 0.f, 0.f, 0.f};
+  const int g = j >> 6;  // one group per workgroup
+  const bool kept = ok && bv[g] > 0;
+  float s0 = 0.f, s1 = 0.f, z0 = 0.f, z1 = 0.f;
+  if (kept) {
     const float* pb = a.part + ((int64_t)b * a.nv_chunks * Hq + h) * (d + 16);
     const int64_t cstride = (int64_t)Hq * (d + 16);
-    int ch = 0;
-    for (; ch + 4 <= a.nv_chunks; ch += 4)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        s[r] += pb[(ch + r) * cstride + j];
-        z[r] += pb[(ch + r) * cstride + d + g];
-      }
-    for (; ch < a.nv_chunks; ++ch) {
-      s[0] += pb[ch * cstride + j];
-      z[0] += pb[ch * cstride + d + g];
+    int ch = part;
+#pragma unroll 2
+    for (; ch + 4 < a.nv_chunks; ch += 8) {
+      s0 += pb[ch * cstride + j];
+      z0 += pb[ch * cstride + d + g];
+      s1 += pb[(ch + 4) * cstride + j];
+      z1 += pb[(ch + 4) * cstride + d + g];
     }
-    c = (((s[0] + s[1]) + (s[2] + s[3])) + ((z[0] + z[1]) + (z[2] + z[3]))) * inv_l;
+    if (ch < a.nv_chunks) {
+      s0 += pb[ch * cstride + j];
+      z0 += pb[ch * cstride + d + g];
+    }
   }
-  a.qt[((int64_t)b * Hq + h) * d + j] = c + a.mean_v[(int64_t)b * d + j];
+  ps[part][tid & 63] = s0 + s1;
+  pz[part][tid & 63] = z0 + z1;
+  __syncthreads();
+  if (tid < 64) {
+    const float l = a.ml[((int64_t)b * Hq + h) * 2 + 1];
+    const float inv_l = l > 0.0f ? 1.0f / l : 0.0f;
+    float c = 0.0f;
+    if (kept)
+      c = (((ps[0][tid] + ps[1][tid]) + (ps[2][tid] + ps[3][tid])) + ((pz[0][tid] + pz[1][tid]) + (pz[2][tid] + pz[3][tid]))) *
+          inv_l;
+    a.qt[((int64_t)b * Hq + h) * d + j] = c + a.mean_v[(int64_t)b * d + j];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -631,7 +642,7 @@ hipError_t launch_layer_attention(const LayerAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(layer_values_kernel, dim3(a.nv_chunks, 2, a.batch), dim3(512), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layer_combine_kernel, dim3(a.n_q_heads, a.batch, (a.d + 255) / 256), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(layer_combine_kernel, dim3(a.n_q_heads, a.batch, a.d / 64), dim3(256), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(layer_rotate_kernel, dim3(a.n_q_heads, a.batch, 16), dim3(256), 0, st, a);
