@@ -281,3 +281,36 @@ def test_layer_attention_fp32_queries_and_softmax_scale():
     ref = O.attention_mode_a(q32[0].astype(np.float64), k, v, scale)
     for h in range(w.n_q_heads):
         assert rel_l2(out[0, h], ref[h]) <= 2e-5
+
+
+@pytest.mark.parametrize("T", [1, 65])
+def test_layer_attention_tiny_caches(T):
+    # one token (the softmax is 1: the output is that token's reconstructed value) and a
+    # ragged second tile
+    w = synth.WORKLOADS["qwen_layer_8x"]
+    xk = synth.numpy_layer_stream(w, 0, 0, 0, T_FIT)[None]
+    xv = synth.numpy_layer_stream(w, 0, 0, 1, T_FIT)[None]
+    d = xk.shape[2]
+    n_kv = d // 128
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    ck, cv = S.Codec(sparams(p), 1), S.Codec(sparams(p), 1)
+    S.spectra_fit_basis(ck, to_device(xk, w.dtype))
+    S.spectra_fit_basis(cv, to_device(xv, w.dtype))
+    t_cap = 128
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
+    S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
+    qs = synth.numpy_query(w, 0, 0, 0)[None]
+    out = S.spectra_layer_decode_attention(ck, cv, pk, pv, t_cap, T, to_device(qs, w.dtype), n_kv).cpu().numpy()
+    W = O.record_words(p)
+    kb, km, kbits = codec_state(ck, 0)
+    vb, vm, vbits = codec_state(cv, 0)
+    vh = O.decode(records_of(pv, 0, 0, T, t_cap, W), vb, vm, vbits, p)
+    ref = _oracle_layer_attention(values_f64(qs[0], w.dtype),
+                                  O.decode(records_of(pk, 0, 0, T, t_cap, W), kb, km, kbits, p), vh, n_kv)
+    for h in range(w.n_q_heads):
+        assert rel_l2(out[0, h], ref[h]) <= 2e-5
+    if T == 1:
+        kvh = np.arange(w.n_q_heads) // (w.n_q_heads // n_kv)
+        want = vh[0].reshape(n_kv, 128)[kvh]
+        assert rel_l2(out[0], want) <= 1e-5
