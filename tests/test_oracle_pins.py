@@ -8,6 +8,7 @@ values printed in the paper (``tests/golden``).
 import json
 import math
 import os
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -263,8 +264,138 @@ def test_capacity_table_from_record_accounting():
 
 
 # ---------------------------------------------------------------------------
+# fp16 metadata rounding (Sec. 3.2: one fp16 scale and zero-point per kept group
+# and token; reading: each rounded once from the exact value, to nearest with
+# ties to even, saturating at +-65504)
+# ---------------------------------------------------------------------------
+def _fp16_exact_bits(x: float) -> int:
+    """Binary16 bits of x by exact rational arithmetic (no floating-point format
+    conversion involved): sign, then the nearest multiple of the quantum of x's
+    binade (2^-24 below 2^-14), ties to the even multiple; magnitudes >= 65504
+    saturate to the largest finite value."""
+    sign = 0x8000 if math.copysign(1.0, x) < 0 else 0
+    a = Fraction(abs(x))
+    if a >= 65504:
+        return sign | 0x7BFF
+    if a < Fraction(1, 2 ** 14):
+        quantum = Fraction(1, 2 ** 24)
+    else:
+        e = a.numerator.bit_length() - a.denominator.bit_length()
+        if Fraction(2) ** e > a:
+            e -= 1
+        quantum = Fraction(2) ** (e - 10)
+    q = a / quantum
+    n = q.numerator // q.denominator
+    rem = q - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    v = n * quantum                      # exact value of the rounded magnitude
+    if v == 0:
+        return sign
+    if v < Fraction(1, 2 ** 14):         # subnormal: the multiple of 2^-24 is the field
+        return sign | int(v * 2 ** 24)
+    e = v.numerator.bit_length() - v.denominator.bit_length()
+    if Fraction(2) ** e > v:
+        e -= 1
+    mant = int(v / Fraction(2) ** (e - 10)) - 1024
+    return sign | ((e + 15) << 10) | mant
+
+
+# (value, expected bits, why)
+_FP16_HAND = [
+    (1.0 + 2.0 ** -11, 0x3C00, "midpoint of 1 and 1+2^-10: even mantissa 0"),
+    (1.0 + 3 * 2.0 ** -11, 0x3C02, "midpoint of mantissas 1 and 2: even 2"),
+    (1.0 + 2.0 ** -11 + 2.0 ** -40, 0x3C01, "just above a midpoint (through fp32 it would become the midpoint)"),
+    (1.0 + 2.0 ** -11 - 2.0 ** -40, 0x3C00, "just below a midpoint"),
+    (-(1.0 + 3 * 2.0 ** -11), 0xBC02, "negative midpoint, even mantissa 2"),
+    (0.1, 0x2E66, "0.1 = 1638.4 quanta of 2^-14 -> 1638 = 0x400 + 0x266, exponent -4"),
+    (2.0 ** -24, 0x0001, "smallest subnormal"),
+    (2.0 ** -25, 0x0000, "half the smallest subnormal: tie to even zero"),
+    (3 * 2.0 ** -25, 0x0002, "midpoint of subnormals 1 and 2: even 2"),
+    (2.0 ** -25 + 2.0 ** -60, 0x0001, "just above the half-quantum"),
+    (1023 * 2.0 ** -24, 0x03FF, "largest subnormal"),
+    (2.0 ** -14 - 2.0 ** -25, 0x0400, "midpoint of the largest subnormal and 2^-14: even 0x400"),
+    (-(2.0 ** -25), 0x8000, "negative tie to zero keeps the sign"),
+    (65504.0, 0x7BFF, "largest finite"),
+    (65519.99, 0x7BFF, "below the overflow midpoint"),
+    (65520.0, 0x7BFF, "overflow midpoint: saturates (IEEE would give infinity)"),
+    (1.0e6, 0x7BFF, "saturates"),
+    (-1.0e6, 0xFBFF, "saturates negative"),
+    (-65520.0, 0xFBFF, "negative overflow midpoint saturates"),
+]
+
+
+@pytest.mark.parametrize("x,bits,why", _FP16_HAND)
+def test_fp16_rounding_hand_values(x, bits, why):
+    assert _fp16_exact_bits(x) == bits, why
+    assert int(O.fp16_bits(O.fp16_rne_sat(x))) == bits, why
+
+
+def test_fp16_rounding_is_single_not_through_fp32():
+    # rounding through fp32 first would collapse these onto fp16 midpoints
+    differs = 0
+    for k in range(0, 200):
+        base = 1.0 + (2 * k + 1) * 2.0 ** -11          # midpoint of mantissas k and k + 1
+        for off in (2.0 ** -40, -(2.0 ** -40)):
+            x = base + off
+            assert float(np.float32(x)) == base        # fp32 cannot hold the offset
+            want = 0x3C00 + k + (1 if off > 0 else 0)  # the nearer neighbour
+            assert _fp16_exact_bits(x) == want
+            assert int(O.fp16_bits(O.fp16_rne_sat(x))) == want
+            differs += _fp16_exact_bits(base) != want  # the tie through fp32 goes to the even one
+    assert differs == 200
+
+
+def test_fp16_rounding_matches_exact_reference():
+    rng = np.random.default_rng(31)
+    xs = list(rng.standard_normal(3000) * np.exp(rng.uniform(-25, 12, 3000)))
+    # exact midpoints and their fp64 neighbours in normal and subnormal binades
+    for e in range(-24, 16):
+        quantum = 2.0 ** (max(e, -14) - 10) if e >= -14 else 2.0 ** -24
+        for n in rng.integers(0, 1024, 8):
+            lo = (1024 + int(n)) * quantum if e >= -14 else int(n) * quantum
+            mid = lo + quantum / 2
+            if abs(mid) > 65504:
+                continue
+            xs += [mid, np.nextafter(mid, np.inf), np.nextafter(mid, -np.inf), -mid]
+    xs += [0.0, -0.0, 65504.0, 65520.0, 7e4, -7e4, np.nextafter(65520.0, 0.0)]
+    got = O.fp16_bits(O.fp16_rne_sat(np.array(xs, dtype=np.float64)))
+    want = np.array([_fp16_exact_bits(float(x)) for x in xs], dtype=np.uint32)
+    assert np.array_equal(got, want)
+
+
+# ---------------------------------------------------------------------------
 # O-3 quantize (Sec. 3.2)
 # ---------------------------------------------------------------------------
+def test_quantize_hand_case_zero_point_not_representable():
+    """Worked by hand: the zero-point is the fp16 rounding of the group minimum, so
+    z != lo, and s is rounded from (hi - z)/(2^b - 1) with that z.
+
+    [0.1, 0.3, 0.5, 0.7] at b = 2: z = fp16(0.1) = 1638 * 2^-14 = 0.0999755859375
+    (0x2E66); (0.7 - z)/3 = 0.200008138... = 1638.47 quanta of 2^-13 -> s =
+    1638 * 2^-13 = 0.199951171875 (0x3266); u = (c - z)/s = 1.2e-4, 1.00037,
+    2.00061, 3.00085 -> q = [0, 1, 2, 3]; decoded z + s q = 0.0999755859375,
+    0.2999267578125, 0.4998779296875, 0.6998291015625.
+
+    [0.10003, 0.25, 0.6, 0.9] at b = 3: z = fp16(0.10003) = 1639 * 2^-14 =
+    0.10003662109375 (0x2E67) lies above the minimum, so u_0 = -5.8e-5 clamps to 0;
+    (0.9 - z)/7 = 0.1142805 = 1872.40 quanta of 2^-14 -> s = 1872 * 2^-14 =
+    0.1142578125 (0x2F50); u = -5.8e-5, 1.3125, 4.37575, 7.00139 -> q = [0, 1, 4, 7].
+    """
+    p = O.Params(head_dim=4, group_size=4)
+    codes, meta = O.quantize(np.array([[0.1, 0.3, 0.5, 0.7]]), [2], p)
+    assert codes.tolist() == [[0, 1, 2, 3]]
+    assert int(meta[0, 0]) == 0x2E663266
+    rec = O.dequantize(codes, meta, [2], p)
+    assert rec[0].tolist() == [0.0999755859375, 0.2999267578125, 0.4998779296875, 0.6998291015625]
+    codes, meta = O.quantize(np.array([[0.10003, 0.25, 0.6, 0.9]]), [3], p)
+    assert codes.tolist() == [[0, 1, 4, 7]]
+    assert int(meta[0, 0]) == (0x2E67 << 16) | 0x2F50
+    rec = O.dequantize(codes, meta, [3], p)
+    assert rec[0].tolist() == [0.10003662109375, 0.10003662109375 + 0.1142578125,
+                               0.10003662109375 + 4 * 0.1142578125, 0.10003662109375 + 7 * 0.1142578125]
+
+
 def test_quantize_hand_vectors():
     p = O.Params(head_dim=4, group_size=4)
     codes, meta = O.quantize(np.array([[0.0, 1.0, 2.0, 3.0]]), [2], p)
