@@ -384,11 +384,15 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   constexpr int PS = 16 * 64 / 512;            // scores per thread and tile
   uint32_t pre[PF];
   float spre[PS];
+  // Slots past n_tokens in the last tile get weight 0; their metadata words are
+  // staged as 0 so that whatever the cache holds there (a NaN scale or zero-point)
+  // never enters the products (0 * NaN would reach every head through the MFMA).
   auto load_tile = [&](int64_t tt) {
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
       const int k = tid + 512 * i;
-      pre[i] = k < 64 * Wv ? vp[tt * 64 * Wv + k] : 0u;
+      const bool meta_past_end = (k >> 6) < nk && tt * 64 + (k & 63) >= a.n_tokens;
+      pre[i] = (k < 64 * Wv && !meta_past_end) ? vp[tt * 64 * Wv + k] : 0u;
     }
 #pragma unroll
     for (int i = 0; i < PS; ++i) {

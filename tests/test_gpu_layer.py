@@ -9,7 +9,7 @@ import pytest
 import oracle as O
 import paper_2608_07915_amd as S
 import synth
-from gpu_parity import check_encoded_stream, codec_state, records_of, rel_l2, sparams, to_device, values_f64
+from gpu_parity import ATTN_SAME_TOL, check_encoded_stream, codec_state, records_of, rel_l2, sparams, to_device, values_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -204,6 +204,8 @@ def test_layer_decode_attention(name, T, ratio, batch):
     S.spectra_fit_basis(cv, to_device(xv, w.dtype))
     t_cap = (T + 63) // 64 * 64 + 64
     pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    pk.fill_(-1)  # slots past the tokens hold NaN metadata: they must not reach the output
+    pv.fill_(-1)
     S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
     S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
     qs = np.stack([synth.numpy_query(w, b, 0, 0) for b in range(batch)])   # [batch, n_q_heads, 128]
@@ -216,7 +218,7 @@ def test_layer_decode_attention(name, T, ratio, batch):
         rk, rv = records_of(pk, b, 0, T, t_cap, W), records_of(pv, b, 0, T, t_cap, W)
         ref = _oracle_layer_attention(q64, O.decode(rk, kb, km, kbits, p), O.decode(rv, vb, vm, vbits, p), n_kv)
         for h in range(q64.shape[0]):
-            assert rel_l2(out[b, h], ref[h]) <= 2e-5, (b, h, rel_l2(out[b, h], ref[h]))
+            assert rel_l2(out[b, h], ref[h]) <= ATTN_SAME_TOL, (b, h, rel_l2(out[b, h], ref[h]))
         rko, *_ = O.encode(values_f64(xk[b, :T], w.dtype), kb, km, kbits, p)
         rvo, *_ = O.encode(values_f64(xv[b, :T], w.dtype), vb, vm, vbits, p)
         ref_o = _oracle_layer_attention(q64, O.decode(rko, kb, km, kbits, p), O.decode(rvo, vb, vm, vbits, p), n_kv)
@@ -247,7 +249,7 @@ def test_layer_attention_three_heads_d384():
                                   O.decode(records_of(pk, 0, 0, T, t_cap, W), kb, km, kbits, p),
                                   O.decode(records_of(pv, 0, 0, T, t_cap, W), vb, vm, vbits, p), 3)
     for h in range(24):
-        assert rel_l2(out[0, h], ref[h]) <= 2e-5
+        assert rel_l2(out[0, h], ref[h]) <= ATTN_SAME_TOL, (h, rel_l2(out[0, h], ref[h]))
 
 
 def test_layer_attention_fp32_queries_and_softmax_scale():
@@ -280,7 +282,7 @@ def test_layer_attention_fp32_queries_and_softmax_scale():
     v = vh.reshape(T, n_kv, 128).transpose(1, 0, 2)
     ref = O.attention_mode_a(q32[0].astype(np.float64), k, v, scale)
     for h in range(w.n_q_heads):
-        assert rel_l2(out[0, h], ref[h]) <= 2e-5
+        assert rel_l2(out[0, h], ref[h]) <= ATTN_SAME_TOL, (h, rel_l2(out[0, h], ref[h]))
 
 
 @pytest.mark.parametrize("T", [1, 65])
@@ -298,6 +300,8 @@ def test_layer_attention_tiny_caches(T):
     S.spectra_fit_basis(cv, to_device(xv, w.dtype))
     t_cap = 128
     pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    pk.fill_(-1)  # slots past the tokens hold NaN metadata: they must not reach the output
+    pv.fill_(-1)
     S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
     S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
     qs = synth.numpy_query(w, 0, 0, 0)[None]
@@ -309,7 +313,7 @@ def test_layer_attention_tiny_caches(T):
     ref = _oracle_layer_attention(values_f64(qs[0], w.dtype),
                                   O.decode(records_of(pk, 0, 0, T, t_cap, W), kb, km, kbits, p), vh, n_kv)
     for h in range(w.n_q_heads):
-        assert rel_l2(out[0, h], ref[h]) <= 2e-5
+        assert rel_l2(out[0, h], ref[h]) <= ATTN_SAME_TOL, (h, rel_l2(out[0, h], ref[h]))
     if T == 1:
         kvh = np.arange(w.n_q_heads) // (w.n_q_heads // n_kv)
         want = vh[0].reshape(n_kv, 128)[kvh]
