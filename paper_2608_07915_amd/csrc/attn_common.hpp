@@ -55,10 +55,14 @@ __device__ __forceinline__ float wave_max_all(float v) {
 // offsets off = n*b and off + b in the group payload at record word `pay`) for
 // 8 consecutive tokens, as bf16 pairs. CLS 0: b in {1,2,4} (both codes in one
 // byte: one byte gather per token pair); CLS 1: b in {3,5,6,7} (one 32-bit
-// funnel-shift window per token holds both); both give 128 + c, the OR with the
-// exponent of 128 (`magic`, held in a VGPR) fused into the mask. CLS 2: b = 8,
-// exact c.
+// funnel-shift window per token holds both). Both give 1 + c 2^-b: the code in
+// the top b bits of the 7-bit mantissa under the exponent of 1.0 (`magic`,
+// 0x3F80 in both halves, held in a VGPR), so the offset 1 removed afterwards (a
+// product against -1) is at most 2^b times the code's weight and costs no
+// precision; the caller scales the sums by 2^b. CLS 2: b = 8, exact c.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t rotr32(uint32_t x, uint32_t s) { return __builtin_amdgcn_alignbit(x, x, s); }
+
 template <int CLS>
 __device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, int pay, int used, int b, int off,
                                              int tok0, uint32_t magic, u32x4& r0, u32x4& r1) {
@@ -67,13 +71,15 @@ __device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, in
   const uint32_t* row = vt + __umul24(w, TROW) + tok0;
   const u32x4 a0 = *reinterpret_cast<const u32x4*>(row);
   const u32x4 a1 = *reinterpret_cast<const u32x4*>(row + 4);
-  const uint32_t M = (1u << b) - 1u;
+  const uint32_t M = ((1u << b) - 1u) << (7 - b);  // the code's bits at the top of the mantissa
   const uint32_t MM = M | (M << 16);
   if constexpr (CLS == 0) {
-    // byte k of two tokens' words in both halves of one register, then shift and mask
+    // byte k of two tokens' words in both bytes of each half (bytes k, k, 4 + k, 4 + k,
+    // a byte broadcast, not a 32-bit multiply); the copy in the upper byte of a half,
+    // shifted right, puts a code at mantissa bits 7 - b .. 6 of that half
     const uint32_t k = (uint32_t)o >> 3, sh = (uint32_t)o & 7u;
-    // bytes k, k, 4 + k, 4 + k (a byte broadcast, not a 32-bit multiply)
     const uint32_t sel = __builtin_amdgcn_perm(k, k, 0u) | 0x04040000u;
+    const uint32_t s0 = sh + 1 + b, s1 = s0 + b;
     uint32_t y[4];
     y[0] = __builtin_amdgcn_perm(a0[1], a0[0], sel);
     y[1] = __builtin_amdgcn_perm(a0[3], a0[2], sel);
@@ -81,8 +87,8 @@ __device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, in
     y[3] = __builtin_amdgcn_perm(a1[3], a1[2], sel);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      r0[i] = ((y[i] >> sh) & MM) | magic;
-      r1[i] = ((y[i] >> (sh + b)) & MM) | magic;
+      r0[i] = ((y[i] >> s0) & MM) | magic;
+      r1[i] = ((y[i] >> s1) & MM) | magic;
     }
   } else {
     const int wn = (w + 1 < used) ? w + 1 : w;  // the next word only matters when a code straddles
@@ -102,11 +108,14 @@ __device__ __forceinline__ void value_codes2(const uint32_t* __restrict__ vt, in
         r1[i] = int_to_bf16_pair((c[2 * i] >> 8) & 0xFFu, (c[2 * i + 1] >> 8) & 0xFFu);
       }
     } else {
+      // codes at bits 0.. and b.. of each half; rotations (either direction, bits that
+      // wrap land outside the mask) move them to bits 7 - b .. 6
+      const uint32_t s0 = (uint32_t)(32 - (7 - b)) & 31u, s1 = (uint32_t)(32 + 2 * b - 7) & 31u;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const uint32_t y = __builtin_amdgcn_perm(c[2 * i + 1], c[2 * i], 0x05040100u);
-        r0[i] = (y & MM) | magic;
-        r1[i] = ((y >> b) & MM) | magic;
+        r0[i] = (rotr32(y, s0) & MM) | magic;
+        r1[i] = (rotr32(y, s1) & MM) | magic;
       }
     }
   }

@@ -533,10 +533,10 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     __builtin_amdgcn_wave_barrier();
 
     // ---- value accumulation over the kept value coefficients ----
-    const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
+    const bf16x8 negone = as_bf16x8(u32x4{0xBF80BF80u, 0xBF80BF80u, 0xBF80BF80u, 0xBF80BF80u});
     constexpr int AR = STACK ? 2 * NH : NH;  // weight rows of one MFMA (8, 12 or 16)
     static_assert(AR >= 8 && AR <= 16, "rows past AR re-read row col - AR");
-    uint32_t vmagic = 0x43004300u;  // exponent of 128 in both halves, in a VGPR (see value_codes2)
+    uint32_t vmagic = 0x3F803F80u;  // exponent of 1.0 in both halves, in a VGPR (see value_codes2)
     asm volatile("" : "+v"(vmagic));
 #pragma unroll
     for (int sl = 0; sl < NG; ++sl) {
@@ -563,10 +563,10 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
             const bf16x8 bop = as_bf16x8(vc[c2]);
             f32x4 acc = vacc[sl][c2];
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, bop, acc, 0, 0, 0);
-            if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
+            if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, negone, acc, 0, 0, 0);
             if constexpr (!STACK) {
               acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(awl, bop, acc, 0, 0, 0);
-              if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(awl, neg128, acc, 0, 0, 0);
+              if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(awl, negone, acc, 0, 0, 0);
             }
             vacc[sl][c2] = acc;
           }
@@ -609,12 +609,14 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int sl = 0; sl < NG; ++sl) {
     if (sl >= Kv.n) continue;
+    // codes below 8 bits entered as 1 + c 2^-b (see value_codes2)
+    const float vscale = Kv.bits[sl] < 8 ? (float)(1u << Kv.bits[sl]) : 1.0f;
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = 4 * kq + j;
-        if (row < ACC_ROWS) accw[row * AROW + G * Kv.grp[sl] + 2 * col + c2] = vacc[sl][c2][j];
+        if (row < ACC_ROWS) accw[row * AROW + G * Kv.grp[sl] + 2 * col + c2] = vacc[sl][c2][j] * vscale;
       }
   }
   uint32_t kept_groups = 0u;  // groups with no kept value coefficients have no sums

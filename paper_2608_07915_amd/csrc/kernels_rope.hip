@@ -408,8 +408,8 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
       // rows 0..NH-1: hi weights of the heads, NH..2NH-1: lo; MFMA rows past them
       // re-read a weight row and are never read back
       const int arow = col16 < 2 * NH ? col16 : col16 - 2 * NH;
-      const bf16x8 neg128 = as_bf16x8(u32x4{0xC300C300u, 0xC300C300u, 0xC300C300u, 0xC300C300u});
-      uint32_t vmagic = 0x43004300u;
+      const bf16x8 negone = as_bf16x8(u32x4{0xBF80BF80u, 0xBF80BF80u, 0xBF80BF80u, 0xBF80BF80u});
+      uint32_t vmagic = 0x3F803F80u;  // exponent of 1.0 in both halves (see value_codes2)
       asm volatile("" : "+v"(vmagic));
       const int tok0 = 32 * vhalf + 8 * kq;
       auto body = [&](auto cls) {
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int c2 = 0; c2 < 2; ++c2) {
           f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, as_bf16x8(vc[c2]), vacc[c2], 0, 0, 0);
-          if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, neg128, acc, 0, 0, 0);
+          if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, negone, acc, 0, 0, 0);
           vacc[c2] = acc;
         }
       };
@@ -451,12 +451,14 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   __syncthreads();  // all tile buffers are free: the key rows hold the value sums of both token halves now
   float* accw = khat + vhalf * (2 * NH * AROW);
   if (vslot) {
+    // codes below 8 bits entered as 1 + c 2^-b (see value_codes2)
+    const float vscale = vB < 8 ? (float)(1u << vB) : 1.0f;
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = 4 * kq + j;
-        if (row < 2 * NH) accw[row * AROW + G * vgrp + 2 * col16 + c2] = vacc[c2][j];
+        if (row < 2 * NH) accw[row * AROW + G * vgrp + 2 * col16 + c2] = vacc[c2][j] * vscale;
       }
   }
   uint32_t kept_groups = 0u;

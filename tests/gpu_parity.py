@@ -5,14 +5,15 @@ Comparison rules (tolerances derived in the design doc):
   records   oracle.pack(GPU codes, GPU metadata) reproduces the GPU words exactly
             (padding included); oracle-packed records unpack on the GPU exactly;
   metadata  fp16 zero-point/scale bit-equal, except adjacent fp16 values whose
-            oracle pre-rounding value lies within 1e-4 (relative) of the midpoint,
-            on at most 1% of (token, group) pairs;
+            oracle pre-rounding value lies within META_TOL (relative) of the
+            midpoint, at a rate of at most META_FRAC of (token, group) pairs
+            (binomial bound on the sample, rate_allowance);
   codes     under the GPU's metadata, >= 99.99% equal; every mismatch is one level
             with the oracle's u within TIE_TOL of a half-integer;
   decode    relative L2 per stream <= 1e-3 vs the oracle's own encode/decode, and
             <= 1e-6 vs the oracle decode of the GPU's bytes;
   attention relative L2 per (sequence, query head) <= 2e-3 vs the oracle's own
-            cache, <= 2e-5 vs the oracle over the GPU's bytes.
+            cache, <= ATTN_SAME_TOL vs the oracle over the GPU's bytes.
 """
 from __future__ import annotations
 
@@ -26,6 +27,9 @@ import paper_2608_07915_amd as S
 import synth
 
 TIE_TOL = 1e-3
+META_TOL = 1e-5
+META_FRAC = 1e-3
+ATTN_SAME_TOL = 1e-5
 
 
 def sparams(p: O.Params) -> S.Params:
@@ -70,16 +74,26 @@ class EncodeReport:
     meta_mismatch: float
     code_mismatch: float
     n_codes: int
+    meta_dist: float = 0.0   # largest relative distance of a differing fp16 value's pre-rounding value to the midpoint
 
 
-def _fp16_boundary_ok(pre: np.ndarray, got_bits: np.ndarray, want_bits: np.ndarray) -> np.ndarray:
-    """True where two fp16 values are adjacent and `pre` sits near their rounding midpoint."""
+def rate_allowance(n: int, rate: float, p_false: float = 1e-6) -> int:
+    """Largest count of events that a rate of at most `rate` over n trials exceeds
+    with probability below p_false (one-sided binomial bound): the bar for a mismatch
+    rate measured on a finite sample."""
+    from scipy.stats import binom
+    return int(binom.isf(p_false, n, rate)) if n > 0 else 0
+
+
+def _fp16_boundary_dist(pre: np.ndarray, got_bits: np.ndarray, want_bits: np.ndarray) -> np.ndarray:
+    """Relative distance of `pre` to the rounding midpoint of two fp16 values; inf
+    unless the two are adjacent."""
     a = O.f16_bits_to_f64(got_bits)
     b = O.f16_bits_to_f64(want_bits)
     adjacent = np.abs(got_bits.astype(np.int64) - want_bits.astype(np.int64)) == 1
     mid = 0.5 * (a + b)
-    near = np.abs(pre - mid) <= 1e-4 * np.maximum(np.abs(mid), 2.0 ** -24)
-    return adjacent & near
+    dist = np.abs(pre - mid) / np.maximum(np.abs(mid), 2.0 ** -24)
+    return np.where(adjacent, dist, np.inf)
 
 
 def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gpu: np.ndarray,
@@ -88,7 +102,7 @@ def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gp
 
     dot_bound (long projections, d > 128): a code may differ only where the oracle's
     u = (c - z)/s lies within the forward error bound of the GPU's fp32 projection of
-    a half-integer: |dc| <= n_r 2^-24 sum_k |x_k V_kj| + 2^-23 |c| (n_r = d/16 + 16
+    a half-integer: |dc| <= n_r 2^-24 sum_k |x_k V_kj| + 2^-22 |c| (n_r = d/16 + 16
     sequential roundings: 16-term MFMA steps chained over d, then the chunk adds).
     scale: the square-root split factors f_j (the cached coordinate is (x V - m)_j f_j)."""
     W = O.record_words(p)
@@ -101,6 +115,7 @@ def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gp
     assert np.array_equal(O.pack(codes_g, meta_g, bits, p), rec_gpu), "GPU record words are not the packed codes"
     n_pairs = 0
     bad_meta = 0
+    meta_dist = 0.0
     g = p.group_size
     for G, b in enumerate(bits):
         if b == 0:
@@ -110,14 +125,18 @@ def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gp
         zg, zo = meta_g[:, G] >> 16, meta_o[:, G] >> 16
         sg, so = meta_g[:, G] & 0xFFFF, meta_o[:, G] & 0xFFFF
         dz = zg != zo
-        assert np.all(_fp16_boundary_ok(lo[dz], zg[dz], zo[dz])), "zero-point differs away from an fp16 boundary"
+        dist_z = _fp16_boundary_dist(lo[dz], zg[dz], zo[dz])
         ds = (sg != so) & ~dz
         pre_s = np.maximum(hi - O.f16_bits_to_f64(zo), 0.0) / float((1 << b) - 1)
-        assert np.all(_fp16_boundary_ok(pre_s[ds], sg[ds], so[ds])), "scale differs away from an fp16 boundary"
+        dist_s = _fp16_boundary_dist(pre_s[ds], sg[ds], so[ds])
+        for dist in (dist_z, dist_s):
+            if dist.size:
+                meta_dist = max(meta_dist, float(dist.max()))
         bad_meta += int(np.count_nonzero(dz | (sg != so)))
         n_pairs += c.shape[0]
     meta_frac = bad_meta / max(n_pairs, 1)
-    assert meta_frac <= 1e-2, f"metadata mismatch fraction {meta_frac}"
+    assert meta_dist <= META_TOL, f"fp16 metadata differs {meta_dist:.3g} (relative) away from a rounding midpoint"
+    assert bad_meta <= rate_allowance(n_pairs, META_FRAC), f"metadata mismatch fraction {meta_frac} of {n_pairs}"
     # P4: codes under the GPU's metadata
     codes_r, u = O.quantize_given_meta(coef, meta_g, bits, p)
     kept = np.repeat(np.array(bits) > 0, g)
@@ -142,7 +161,7 @@ def check_encoded_stream(x64: np.ndarray, basis, mean, bits, p: O.Params, rec_gp
             assert np.all(np.abs(uu - np.floor(uu) - 0.5) <= TIE_TOL), "code mismatch away from a rounding tie"
     assert frac <= 1e-4, f"code mismatch fraction {frac}"
     assert np.all(codes_g[:, ~kept] == 0)
-    return EncodeReport(meta_frac, frac, n_codes)
+    return EncodeReport(meta_frac, frac, n_codes, meta_dist)
 
 
 def rel_l2(a, b) -> float:
