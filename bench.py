@@ -79,6 +79,9 @@ def _parse():
                     help="key share of the combined K+V budget (asymmetric split; 0.5 = symmetric records)")
     ap.add_argument("--check", action="store_true", help="compare sampled outputs with the oracle after timing")
     ap.add_argument("--eager", action="store_true", help="launch decode steps from Python instead of HIP graphs")
+    ap.add_argument("--skip-configs", action="store_true",
+                    help="skip the encode + attention measurements of the other layer workloads "
+                         "(Llama 4x, Qwen 8x, Llama batch 16 at 12x)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device-to-device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -279,6 +282,90 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
         "mode_a_decode": {"ms_per_layer": round(dec_ms, 4), "GBps": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 1),
                           "frac": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                           "what": "spectra_decode of one layer's keys (8 streams) to fp32, outside the step"},
+    }
+
+
+# The model-shaped layer workloads measured beside the headline one: encode of the whole
+# layer, then decode-step attention read from the packed records (no appends).
+CONFIG_WORKLOADS = ("llama_layer_4x", "qwen_layer_8x", "llama_batch16_12x")
+MALL_BYTES = 256 << 20
+
+
+def config_bench(S, torch, w, dev, reps=4):
+    """Encode and decode-step attention of one layer workload. Attention steps cycle
+    through enough copies of the packed caches (>= 2x the 256 MB MALL in total) that
+    every step reads its records from HBM; the steps of one pass are replayed from a
+    HIP graph, and HIP events around the replays give the time per step."""
+    import synth
+    H, Hq, d, B, T = w.n_kv_heads, w.n_q_heads, 128, w.n_seq, w.n_tokens
+    Sn = B * H
+    t_cap = (T + 63) // 64 * 64
+    xk = synth.device_streams(w, 0, 0, T, dev)
+    xv = synth.device_streams(w, 1, 0, T, dev)
+    sp = S.Params(ratio=w.ratio)
+    ck, cv = S.Codec(sp, Sn), S.Codec(sp, Sn)
+    S.spectra_fit_basis(ck, xk)
+    S.spectra_fit_basis(cv, xv)
+    Wk, Wv = ck.record_words, cv.record_words
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    enc = []
+    for _ in range(reps):
+        e0, e1 = ev(), ev()
+        e0.record()
+        S.spectra_encode(ck, xk, 0, pk, t_cap)
+        S.spectra_encode(cv, xv, 0, pv, t_cap)
+        e1.record()
+        enc.append((e0, e1))
+    torch.cuda.synchronize()
+    enc_ms = sum(e0.elapsed_time(e1) for e0, e1 in enc[1:]) / (reps - 1)
+    in_b = 2 if w.dtype == "bf16" else 4
+    state = Sn * 2 * (d * d * 4 + d * 4)
+    enc_bytes = Sn * T * (2 * d * in_b + (Wk + Wv) * 4) + state
+    del xk, xv
+    rec_bytes = Sn * T * (Wk + Wv) * 4
+    att_bytes = rec_bytes + state + B * Hq * d * (in_b + 4)
+    copies = max(1, -(-2 * MALL_BYTES // rec_bytes))
+    caches = [(pk, pv)] + [(pk.clone(), pv.clone()) for _ in range(copies - 1)]
+    steps = max(w.attn_steps, copies)
+    qs = [synth.device_queries(w, 0, s % max(w.attn_steps, 1), dev) for s in range(steps)]
+    ws = torch.empty(S.spectra_attention_workspace_bytes(B, Hq, H, T), dtype=torch.uint8, device=dev)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+
+    def attend():
+        for s in range(steps):
+            kp, vp = caches[s % copies]
+            S.spectra_decode_attention(ck, cv, kp, vp, t_cap, T, qs[s], H, out=out, workspace=ws)
+
+    attend()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        attend()
+    g.replay()
+    torch.cuda.synchronize()
+    runs = []
+    for _ in range(reps):
+        e0, e1 = ev(), ev()
+        e0.record()
+        g.replay()
+        e1.record()
+        runs.append((e0, e1))
+    torch.cuda.synchronize()
+    att_ms = sum(e0.elapsed_time(e1) for e0, e1 in runs) / (reps * steps)
+    del caches, g
+    enc_gbps = enc_bytes / (enc_ms * 1e-3) / 1e9
+    att_gbps = att_bytes / (att_ms * 1e-3) / 1e9
+    return {
+        "description": w.description, "record_words": [Wk, Wv], "ratio_actual": round(16 * d / (32 * Wk), 2),
+        "encode": {"ms": round(enc_ms, 4), "GBps": round(enc_gbps, 1), "frac": round(enc_gbps / HBM_PEAK_GBPS, 4),
+                   "bytes": enc_bytes},
+        "attention": {"us_per_step": round(att_ms * 1e3, 2), "GBps": round(att_gbps, 1),
+                      "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "bytes_per_step": att_bytes,
+                      "cache_tokens_per_s": round(B * T / (att_ms * 1e-3), 1),
+                      "sequences_per_s": round(B / (att_ms * 1e-3), 1),
+                      "steps_timed": steps * reps, "distinct_cache_copies": copies},
+        "bits_k_first": ck.bits[0].cpu().numpy().tolist(), "bits_v_first": cv.bits[0].cpu().numpy().tolist(),
     }
 
 
@@ -485,6 +572,14 @@ def main():
     }
     if args.check:
         result["check"] = sampled_check(w, p, p_v, ck, cv, pk, pv, xk, xv, qs, outs, t_cap, T, n_dec, L, H)
+    if not args.skip_configs:
+        # the other layer workloads, after the headline one's buffers are released
+        del xk, xv, pk, pv, k_new, v_new, layer_pk, layer_pv, graphs
+        torch.cuda.empty_cache()
+        result["configs"] = {}
+        for name in CONFIG_WORKLOADS:
+            result["configs"][name] = config_bench(S, torch, synth.WORKLOADS[name], dev)
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, p, p_v=p_v)
     print(json.dumps(result))
