@@ -294,6 +294,91 @@ __device__ __forceinline__ void score_slot(const uint32_t* __restrict__ kt, int 
 // and value record words per tile (>= W_k, W_v; both 0: no prefetch); EXACT:
 // W_k = PK and W_v = PV.
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Merge of the four wavefronts' online-softmax states of one scan workgroup in LDS
+// and the chunk's partial (m, l, zero-point sums per group, value sums per
+// coefficient) for every query head of the KV head. smem: the tile buffers, free
+// once every wave has left its tile loop.
+// ---------------------------------------------------------------------------
+template <int NQ>
+__device__ __forceinline__ void write_chunk_partial(const AttnArgs& a, int b, int kv, int chunk, int tid, int wave,
+                                                    int lane, int kq, int col, bool ok, const Kept& Kv,
+                                                    const float (&m_run)[4 * NQ], const float (&l_run)[4 * NQ],
+                                                    const float (&zacc)[4 * NQ][NG], const f32x4 (&vacc)[NG][2],
+                                                    uint32_t* smem) {
+  constexpr int NH = 4 * NQ;
+  constexpr bool STACK = NQ <= 2;
+  __shared__ float mst[WAVES][NH], lst[WAVES][NH], zst[WAVES][NH][NG];
+  const int nqh = a.n_qh;
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    const float l = wave_sum_lane63(l_run[h]);
+    float z[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) z[g] = g < Kv.n ? wave_sum_lane63(zacc[h][g]) : 0.0f;
+    if (lane == 63) {
+      mst[wave][h] = ok ? m_run[h] : -__builtin_inff();
+      lst[wave][h] = l;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) zst[wave][h][g] = 0.0f;
+      // zero-point sums are kept per slot; the partial holds them per group
+#pragma unroll
+      for (int sl = 0; sl < NG; ++sl)
+        if (sl < Kv.n) zst[wave][h][Kv.grp[sl]] = z[sl];
+    }
+  }
+  __syncthreads();  // all waves done with their tile buffers: reuse smem for the value sums
+  // per wave, MFMA row r of the value accumulators lands in row r of [ACC_ROWS][AROW]
+  // (stacked: rows NH.. hold the lo-weight sums of the same heads); every kept
+  // column of a row is written exactly once, so no read-modify-write is needed
+  constexpr int ACC_ROWS = STACK ? 2 * NH : NH;
+  float* accw = reinterpret_cast<float*>(smem) + wave * ACC_ROWS * AROW;
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl) {
+    if (sl >= Kv.n) continue;
+    // codes below 8 bits entered as 1 + c 2^-b (see value_codes2)
+    const float vscale = Kv.bits[sl] < 8 ? (float)(1u << Kv.bits[sl]) : 1.0f;
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = 4 * kq + j;
+        if (row < ACC_ROWS) accw[row * AROW + G * Kv.grp[sl] + 2 * col + c2] = vacc[sl][c2][j] * vscale;
+      }
+  }
+  uint32_t kept_groups = 0u;  // groups with no kept value coefficients have no sums
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl)
+    if (sl < Kv.n) kept_groups |= 1u << Kv.grp[sl];
+  __syncthreads();
+  float* part = a.partial + ((int64_t)b * a.n_q_heads + kv * nqh) * a.n_chunks * PART + (int64_t)chunk * PART;
+  for (int e = tid; e < nqh * D; e += 256) {
+    const int h = e >> 7, j = e & 127;
+    const bool kept = (kept_groups >> (j >> 5)) & 1u;
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) M = __builtin_fmaxf(M, mst[w][h]);
+    float acc = 0.0f, l = 0.0f, z = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) {
+      const float f = (mst[w][h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(mst[w][h] - M);
+      const float* aw = reinterpret_cast<const float*>(smem) + w * ACC_ROWS * AROW;
+      float v = kept ? aw[h * AROW + j] : 0.0f;
+      if constexpr (STACK) v += kept ? aw[(NH + h) * AROW + j] : 0.0f;
+      acc += f * v;
+      l += f * lst[w][h];
+      if (j < NG) z += f * zst[w][h][j];
+    }
+    float* ph = part + (int64_t)h * a.n_chunks * PART;
+    ph[8 + j] = acc;
+    if (j == 0) {
+      ph[0] = M;
+      ph[1] = l;
+    }
+    if (j < NG) ph[2 + j] = z;
+  }
+}
+
 template <int NQ, int PK, int PV, bool EXACT>
 __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   constexpr int NH = 4 * NQ;
@@ -301,7 +386,6 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
   __shared__ __attribute__((aligned(16))) uint32_t qa_s[NQ * QA_QUAD];
   __shared__ float qbar_s[16 * 4];
-  __shared__ float mst[WAVES][NH], lst[WAVES][NH], zst[WAVES][NH][NG];
 
   const int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -582,74 +666,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     __builtin_amdgcn_wave_barrier();
   }
 
-  // ---- merge the four wavefronts and write this chunk's partial ----
-#pragma unroll
-  for (int h = 0; h < NH; ++h) {
-    const float l = wave_sum_lane63(l_run[h]);
-    float z[NG];
-#pragma unroll
-    for (int g = 0; g < NG; ++g) z[g] = g < Kv.n ? wave_sum_lane63(zacc[h][g]) : 0.0f;
-    if (lane == 63) {
-      mst[wave][h] = ok ? m_run[h] : -__builtin_inff();
-      lst[wave][h] = l;
-#pragma unroll
-      for (int g = 0; g < NG; ++g) zst[wave][h][g] = 0.0f;
-      // zero-point sums are kept per slot; the partial holds them per group
-#pragma unroll
-      for (int sl = 0; sl < NG; ++sl)
-        if (sl < Kv.n) zst[wave][h][Kv.grp[sl]] = z[sl];
-    }
-  }
-  __syncthreads();  // all waves done with their tile buffers: reuse smem for the value sums
-  // per wave, MFMA row r of the value accumulators lands in row r of [ACC_ROWS][AROW]
-  // (stacked: rows NH.. hold the lo-weight sums of the same heads); every kept
-  // column of a row is written exactly once, so no read-modify-write is needed
-  constexpr int ACC_ROWS = STACK ? 2 * NH : NH;
-  float* accw = reinterpret_cast<float*>(smem) + wave * ACC_ROWS * AROW;
-#pragma unroll
-  for (int sl = 0; sl < NG; ++sl) {
-    if (sl >= Kv.n) continue;
-    // codes below 8 bits entered as 1 + c 2^-b (see value_codes2)
-    const float vscale = Kv.bits[sl] < 8 ? (float)(1u << Kv.bits[sl]) : 1.0f;
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = 4 * kq + j;
-        if (row < ACC_ROWS) accw[row * AROW + G * Kv.grp[sl] + 2 * col + c2] = vacc[sl][c2][j] * vscale;
-      }
-  }
-  uint32_t kept_groups = 0u;  // groups with no kept value coefficients have no sums
-#pragma unroll
-  for (int sl = 0; sl < NG; ++sl)
-    if (sl < Kv.n) kept_groups |= 1u << Kv.grp[sl];
-  __syncthreads();
-  float* part = a.partial + ((int64_t)b * a.n_q_heads + kv * nqh) * a.n_chunks * PART + (int64_t)chunk * PART;
-  for (int e = tid; e < nqh * D; e += 256) {
-    const int h = e >> 7, j = e & 127;
-    const bool kept = (kept_groups >> (j >> 5)) & 1u;
-    float M = -__builtin_inff();
-#pragma unroll
-    for (int w = 0; w < WAVES; ++w) M = __builtin_fmaxf(M, mst[w][h]);
-    float acc = 0.0f, l = 0.0f, z = 0.0f;
-#pragma unroll
-    for (int w = 0; w < WAVES; ++w) {
-      const float f = (mst[w][h] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(mst[w][h] - M);
-      const float* aw = reinterpret_cast<const float*>(smem) + w * ACC_ROWS * AROW;
-      float v = kept ? aw[h * AROW + j] : 0.0f;
-      if constexpr (STACK) v += kept ? aw[(NH + h) * AROW + j] : 0.0f;
-      acc += f * v;
-      l += f * lst[w][h];
-      if (j < NG) z += f * zst[w][h][j];
-    }
-    float* ph = part + (int64_t)h * a.n_chunks * PART;
-    ph[8 + j] = acc;
-    if (j == 0) {
-      ph[0] = M;
-      ph[1] = l;
-    }
-    if (j < NG) ph[2 + j] = z;
-  }
+  write_chunk_partial<NQ>(a, b, kv, chunk, tid, wave, lane, kq, col, ok, Kv, m_run, l_run, zacc, vacc, smem);
 }
 
 // ---------------------------------------------------------------------------

@@ -167,3 +167,61 @@ def test_attention_zero_query_is_value_mean():
         want = vh.mean(axis=0)
         for hq in range(h * w.n_qh, (h + 1) * w.n_qh):
             assert rel_l2(out[hq], want) <= ATTN_SAME_TOL, (h, hq, rel_l2(out[hq], want))
+
+
+def _width_signatures(words):
+    """Every tuple of kept-slot widths (1..7) whose record fits `words` words:
+    sum over slots of (b + 1) <= words, up to four slots (plus the empty one)."""
+    out = [[]]
+    for n in range(1, 5):
+        for code in range(7 ** n):
+            b = [code // 7 ** k % 7 + 1 for k in range(n)]
+            if sum(x + 1 for x in b) <= words:
+                out.append(b)
+    return out
+
+
+@pytest.mark.parametrize("words,n_qh", [(8, 4), (8, 7), (5, 4), (6, 8)])
+def test_attention_every_width_signature(words, n_qh):
+    """One KV head per width signature of records of at most 8 words (every order of
+    kept-slot widths), keys and values with different signatures and kept groups at
+    seeded, not necessarily adjacent, positions."""
+    from dataclasses import replace
+    sigs = _width_signatures(words)
+    rng = np.random.default_rng(words * 10 + n_qh)
+    n_kv = len(sigs)
+    w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=n_kv, n_q_heads=n_kv * n_qh)
+    T = 300
+    p = O.Params(budget_bits=32 * words)
+
+    def table(sig):
+        bits = [0, 0, 0, 0]
+        for g, b in zip(sorted(rng.choice(4, size=len(sig), replace=False)), sig):
+            bits[int(g)] = b
+        return bits
+
+    bits_k = [table(sigs[i]) for i in range(n_kv)]
+    bits_v = [table(sigs[(i * 7 + 3) % n_kv]) for i in range(n_kv)]
+    xk, xv = _workload_streams(w, T, 1)
+    t_cap = 320
+    codecs = []
+    for x, bits in ((xk, bits_k), (xv, bits_v)):
+        codec = S.Codec(sparams(p), n_kv)
+        S.spectra_fit_basis(codec, to_device(x, w.dtype))
+        codec.bits.copy_(torch.tensor(bits, dtype=torch.uint8))
+        codecs.append(fit_and_encode(to_device(x, w.dtype), p, t_cap, fit=False, codec=codec))
+    (ck, pk), (cv, pv) = codecs
+    q = _queries(w, 1)
+    out = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, T, to_device(q, w.dtype), n_kv).cpu().numpy()[0]
+    q64 = values_f64(q[0], w.dtype)
+    W = O.record_words(p)
+    for h in range(n_kv):
+        kb, km, kbits = codec_state(ck, h)
+        vb, vm, vbits = codec_state(cv, h)
+        assert kbits == bits_k[h] and vbits == bits_v[h]
+        kh = O.decode(records_of(pk, h, 0, T, t_cap, W), kb, km, kbits, p)
+        vh = O.decode(records_of(pv, h, 0, T, t_cap, W), vb, vm, vbits, p)
+        ref = O.attention_mode_a(q64[h * n_qh:(h + 1) * n_qh], kh[None], vh[None])
+        for i in range(n_qh):
+            e = rel_l2(out[h * n_qh + i], ref[i])
+            assert e <= ATTN_SAME_TOL, (sigs[h], sigs[(h * 7 + 3) % n_kv], i, e)
