@@ -273,6 +273,26 @@ spectra_status spectra_decode_step(const spectra_codec* ck, const spectra_codec*
                                    float* out, void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * spectra_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same step, with the split-K partials in a file-scope device array of
+ * SPECTRA_STATIC_SCRATCH_BYTES bytes that the library holds on every GPU it runs
+ * on until the process ends, instead of a workspace. Calls no hipMalloc/hipFree
+ * (the array's address is looked up once per device, on its first call there).
+ * Returns SPECTRA_EWORKSPACE when spectra_attention_workspace_bytes(batch,
+ * n_q_heads, n_kv_heads, t + 1) exceeds the array. Every call on one GPU shares
+ * that GPU's array: calls that overlap on one GPU (other streams, other threads)
+ * race and must be serialised by the caller. Other arguments and errors as
+ * spectra_decode_step. Asynchronous.
+ * ------------------------------------------------------------------------- */
+#define SPECTRA_STATIC_SCRATCH_BYTES (8u << 20)
+spectra_status spectra_decode_step_static(const spectra_codec* ck, const spectra_codec* cv, uint32_t* packed_k,
+                                          uint32_t* packed_v, int64_t t_capacity, int64_t t, const void* k_new,
+                                          const void* v_new, spectra_dtype kv_dt, const void* q,
+                                          spectra_dtype q_dt, int32_t batch, int32_t n_q_heads,
+                                          int32_t n_kv_heads, float softmax_scale, float* out, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Host-side pieces of the fit, exported so they can be checked without a GPU.
  * ------------------------------------------------------------------------- */
 

@@ -60,6 +60,8 @@ _SIGNATURES = {
                                               _P, _P, _SZ, _P]),
     "spectra_decode_step": (_I32, [_PC, _PC, _P, _P, _I64, _I64, _P, _P, _I32, _P, _I32, _I32, _I32, _I32, _F32,
                                    _P, _P, _SZ, _P]),
+    "spectra_decode_step_static": (_I32, [_PC, _PC, _P, _P, _I64, _I64, _P, _P, _I32, _P, _I32, _I32, _I32, _I32,
+                                          _F32, _P, _P]),
     "spectra_allocate_bits": (_I32, [_P, _PP, _P]),
     "spectra_eigh_host": (_I32, [_P, _I32, _P, _P]),
     "spectra_fit_from_moments_host": (_I32, [_PP, _I64, _P, _P, _P, _P, _P, _P]),

@@ -327,6 +327,27 @@ def spectra_decode_step(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: in
     return out
 
 
+
+def spectra_decode_step_static(ck: Codec, cv: Codec, packed_k, packed_v, t_capacity: int, t: int, k_new, v_new, q,
+                               n_kv_heads: int, softmax_scale: float = 0.0, out=None, stream=None):
+    """spectra_decode_step with the partials in the library's static device array (no
+    workspace, nothing allocated by the library; `out` is allocated here only when not
+    given). Calls that overlap on one GPU race."""
+    import torch
+    batch, n_q_heads, d = _attention_shapes(ck, cv, packed_k, packed_v, t_capacity, q, n_kv_heads, out)
+    _need(k_new.is_cuda and v_new.is_cuda and k_new.is_contiguous() and v_new.is_contiguous(),
+          "k_new and v_new must be contiguous device tensors")
+    _need(k_new.dtype == v_new.dtype and tuple(k_new.shape) == tuple(v_new.shape) == (batch, n_kv_heads, d),
+          f"k_new and v_new must be [{batch}, {n_kv_heads}, {d}] of one dtype")
+    if out is None:
+        out = torch.empty((batch, n_q_heads, d), dtype=torch.float32, device=q.device)
+    check(_lib.get().spectra_decode_step_static(ctypes.byref(ck.struct), ctypes.byref(cv.struct), packed_k.data_ptr(),
+                                                packed_v.data_ptr(), int(t_capacity), int(t), k_new.data_ptr(),
+                                                v_new.data_ptr(), _dtype_code(k_new), q.data_ptr(), _dtype_code(q),
+                                                batch, n_q_heads, int(n_kv_heads), float(softmax_scale),
+                                                out.data_ptr(), _stream(stream)))
+    return out
+
 def spectra_pack_codes(codec: Codec, codes, meta, packed, t_capacity: int, stream=None) -> None:
     import torch
     n = codes.shape[1]

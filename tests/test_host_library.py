@@ -165,6 +165,15 @@ def test_argument_errors_return_before_any_launch(lib):
     assert b"16-byte" in lib.spectra_last_error()
     assert lib.spectra_decode_step(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 8, 256, 256, 1, 256, 1, 1, 4, 4,
                                    0.0, 256, 256, 16, None) == -4
+    # decode step on the static array: slot outside the capacity, partials beyond the
+    # array's size (both refused before any device call)
+    assert lib.spectra_decode_step_static(ctypes.byref(c), ctypes.byref(c), 256, 256, 64, 64, 256, 256, 1, 256, 1, 1,
+                                          4, 4, 0.0, 256, None) == -1
+    big_t = 1 << 26
+    assert lib.spectra_attention_workspace_bytes(256, 4096, 256, big_t + 1) > 8 << 20
+    assert lib.spectra_decode_step_static(ctypes.byref(c), ctypes.byref(c), 256, 256, big_t + 64, big_t, 256, 256, 1,
+                                          256, 1, 256, 4096, 256, 0.0, 256, None) == -4
+    assert b"static" in lib.spectra_last_error()
     # fit from weights: d_model, layer grouping, alignment, workspace (c holds 4 streams)
     need = lib.spectra_fit_weights_workspace_bytes(ctypes.byref(c), 256)
     assert need == 4 * (128 * 128 + 128) * 8 + 4 * 256 * 128 * 8
