@@ -147,10 +147,14 @@ spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype 
                                  size_t ws_bytes, void* stream);
 
 /* Calibrate-once fit from weights (Sec. 3.1, Eqs. gweighted and gsvd; App. B). The
- * paper whitens a head's projection, M = G^{1/2} W = U S V^T, and keeps the top right
+ * paper whitens a projection, M = G^{1/2} W = U S V^T, and keeps the top right
  * singular directions; for k = h W these are the eigenvectors of E[k^T k] = W^T G W,
  * so the basis, coefficient means, centered variances and widths are those of a
  * stream whose second moment is W^T G W and whose mean is hbar W (no data pass).
+ * Both geometries: d = 128 (one KV head's projection) or the per-layer geometry (d =
+ * d_kv, the layer's KV heads side by side: W is the layer's whole key or value
+ * projection, the paper's own setting), where lscale, when set, receives the
+ * square-root split as in spectra_fit_basis.
  *   W     device fp32 [n_streams][d_model][d]: stream s's projection (k = h W);
  *   G     device fp64 [n_streams / streams_per_layer][d_model][d_model]: E[h^T h] of
  *         the input of stream s's layer, layer = s / streams_per_layer;
@@ -198,8 +202,10 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
  * sum_t softmax_t(scale q_h . k_hat_t[kv]) v_hat_t[kv], computed as q~_h = scale q_h
  * V_K[kv rows] (a d-wide latent query), scores over the kept key coefficients (the
  * constant q~_h . m_K cancels), softmax, value sums over the kept value coefficients,
- * then (a / sum + m_V) V_V[kv rows]^T. n_q_heads <= 32, records of at most 64 words, no
- * square-root split. softmax_scale <= 0 selects 1/sqrt(128). Workspace: device,
+ * then (a / sum + m_V) V_V[kv rows]^T. With the square-root split (lscale set) the
+ * cached coordinates are c_j f_j: q~_j is divided by the keys' f_j and the value sums
+ * by the values' f_j before m_V is added. n_q_heads <= 32, records of at most 64 words.
+ * softmax_scale <= 0 selects 1/sqrt(128). Workspace: device,
  * spectra_layer_attention_workspace_bytes bytes, 256-byte aligned. Asynchronous.
  * ------------------------------------------------------------------------- */
 size_t spectra_layer_attention_workspace_bytes(const spectra_codec* ck, int32_t batch, int32_t n_q_heads,

@@ -210,15 +210,16 @@ spectra_status spectra_fit_basis(spectra_codec* c, const void* x, spectra_dtype 
 }
 
 size_t spectra_fit_weights_workspace_bytes(const spectra_codec* c, int32_t d_model) {
-  if (!c || c->n_streams <= 0 || d_model <= 0) return 0;
-  return round256((size_t)c->n_streams * (size_t)kMoments * sizeof(double)) +
-         (size_t)c->n_streams * (size_t)d_model * kD * sizeof(double);
+  if (!c || c->n_streams <= 0 || d_model <= 0 || c->p.head_dim <= 0) return 0;
+  const size_t d = (size_t)c->p.head_dim;
+  return round256((size_t)c->n_streams * (d * d + d) * sizeof(double)) +
+         (size_t)c->n_streams * (size_t)d_model * d * sizeof(double);
 }
 
 spectra_status spectra_fit_weights(spectra_codec* c, const float* W, int32_t d_model, const double* G,
                                    const double* hbar, int32_t streams_per_layer, void* workspace, size_t ws_bytes,
                                    void* stream) {
-  spectra_status st = check_codec(c, "fit_weights");
+  spectra_status st = check_codec(c, "fit_weights", true);
   if (st != SPECTRA_OK) return st;
   if (!W || !G || !aligned(W, 4) || !aligned(G, 8) || (hbar && !aligned(hbar, 8)))
     return fail(SPECTRA_EINVAL, "fit_weights: W and G must be non-null and aligned (4 / 8 bytes)");
@@ -232,12 +233,15 @@ spectra_status spectra_fit_weights(spectra_codec* c, const float* W, int32_t d_m
   const size_t need = spectra_fit_weights_workspace_bytes(c, d_model);
   if (ws_bytes < need) return fail(SPECTRA_EWORKSPACE, "fit_weights workspace %zu < %zu bytes", ws_bytes, need);
   hipStream_t hs = (hipStream_t)stream;
+  const int d = c->p.head_dim;  // 128 per head; d_kv in the per-layer geometry
+  const int64_t mstride = (int64_t)d * d + d;
   double* moments = reinterpret_cast<double*>(workspace);
   double* scratch = reinterpret_cast<double*>(static_cast<char*>(workspace) +
-                                              round256((size_t)S * (size_t)kMoments * sizeof(double)));
-  hipError_t e = launch_weights_moments(W, G, hbar, d_model, (int32_t)S, streams_per_layer, scratch, moments, kMoments, hs);
+                                              round256((size_t)S * (size_t)mstride * sizeof(double)));
+  hipError_t e = launch_weights_moments(W, G, hbar, d_model, d, (int32_t)S, streams_per_layer, scratch, moments,
+                                        mstride, hs);
   if (e != hipSuccess) return hip_fail(e, "fit_weights launch");
-  std::vector<double> mom((size_t)(S * kMoments));
+  std::vector<double> mom((size_t)(S * mstride));
   e = hipMemcpyAsync(mom.data(), moments, mom.size() * sizeof(double), hipMemcpyDeviceToHost, hs);
   if (e != hipSuccess) return hip_fail(e, "fit_weights moments copy");
   e = hipStreamSynchronize(hs);
@@ -355,7 +359,6 @@ spectra_status spectra_layer_decode_attention(const spectra_codec* ck, const spe
   if (st != SPECTRA_OK) return st;
   if (!layer_geometry(ck->p) || !layer_geometry(cv->p) || ck->p.head_dim != cv->p.head_dim)
     return fail(SPECTRA_EINVAL, "%s: both codecs must use the same per-layer geometry", name);
-  if (ck->lscale || cv->lscale) return fail(SPECTRA_EUNSUPPORTED, "%s: codecs with the square-root split are not supported", name);
   const int d = ck->p.head_dim;
   if (n_kv_heads <= 0 || n_kv_heads * 128 != d)
     return fail(SPECTRA_EINVAL, "%s: n_kv_heads * 128 must equal the latent width %d", name, d);
@@ -393,6 +396,8 @@ spectra_status spectra_layer_decode_attention(const spectra_codec* ck, const spe
   a.mean_v = cv->mean;
   a.bits_k = ck->bits;
   a.bits_v = cv->bits;
+  a.lscale_k = ck->lscale;
+  a.lscale_v = cv->lscale;
   a.q = q;
   a.q_f32 = q_dt == SPECTRA_F32;
   a.batch = batch;

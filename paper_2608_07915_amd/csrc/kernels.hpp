@@ -117,10 +117,10 @@ int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_token
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
-// moments[s] = [W_s^T G W_s, hbar W_s] for W [n_streams][d_model][128] fp32 and per-layer
-// G [layers][d_model][d_model], hbar [layers][d_model] fp64 (layer = s / streams_per_layer);
-// scratch: n_streams * d_model * 128 doubles.
-hipError_t launch_weights_moments(const float* W, const double* G, const double* hbar, int32_t d_model,
+// moments[s] = [W_s^T G W_s, hbar W_s] for W [n_streams][d_model][d] fp32 (d a multiple of 64)
+// and per-layer G [layers][d_model][d_model], hbar [layers][d_model] fp64 (layer = s /
+// streams_per_layer); scratch: n_streams * d_model * d doubles.
+hipError_t launch_weights_moments(const float* W, const double* G, const double* hbar, int32_t d_model, int32_t d,
                                   int32_t n_streams, int32_t streams_per_layer, double* scratch, double* moments,
                                   int64_t mom_stride, hipStream_t st);
 }  // namespace spectra

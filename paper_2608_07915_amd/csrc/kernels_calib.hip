@@ -1,6 +1,7 @@
 // Calibration from weights (Sec. 3.1, Eqs. gweighted and gsvd; App. B): the
 // second moment E[k^T k] = W^T G W and mean E[k] = hbar W of the keys (or values)
-// k = h W a head's projection W [d_model][128] produces from layer inputs h with
+// k = h W a projection W [d_model][d] produces (one KV head, d = 128, or a layer's
+// KV heads side by side, d = d_kv) from layer inputs h with
 // second moment G = E[h^T h] and mean hbar. Both are fp64 on the GPU; the
 // eigenbasis, variances and widths follow on the host as for a data fit.
 //
@@ -71,16 +72,18 @@ __global__ __launch_bounds__(256) void wgemm_kernel(WgemmArgs g) {
 }
 
 // mu_s[j] = sum_a hbar_l[a] W_s[a][j] (zero when hbar is null): one workgroup of
-// 128 threads per stream, one output column each, ascending a.
-__global__ __launch_bounds__(128) void wmean_kernel(const float* W, const double* hbar, int32_t d_model,
+// 128 threads per stream, output columns j = tid, tid + 128, ..., ascending a.
+__global__ __launch_bounds__(128) void wmean_kernel(const float* W, const double* hbar, int32_t d_model, int32_t d,
                                                     int32_t streams_per_layer, double* moments, int64_t mom_stride) {
-  const int s = blockIdx.x, j = threadIdx.x;
-  const float* Ws = W + (int64_t)s * d_model * 128;
+  const int s = blockIdx.x;
+  const float* Ws = W + (int64_t)s * d_model * d;
   const double* h = hbar ? hbar + (int64_t)(s / streams_per_layer) * d_model : nullptr;
-  double acc = 0.0;
-  if (h)
-    for (int a = 0; a < d_model; ++a) acc = __builtin_fma(h[a], (double)Ws[(int64_t)a * 128 + j], acc);
-  moments[(int64_t)s * mom_stride + 128 * 128 + j] = acc;
+  for (int j = threadIdx.x; j < d; j += 128) {
+    double acc = 0.0;
+    if (h)
+      for (int a = 0; a < d_model; ++a) acc = __builtin_fma(h[a], (double)Ws[(int64_t)a * d + j], acc);
+    moments[(int64_t)s * mom_stride + (int64_t)d * d + j] = acc;
+  }
 }
 
 }  // namespace spectra_dev
@@ -88,9 +91,9 @@ __global__ __launch_bounds__(128) void wmean_kernel(const float* W, const double
 namespace spectra {
 using namespace spectra_dev;
 
-// moments[s] = [W_s^T G W_s (128 x 128, row-major), hbar W_s (128)]; scratch holds
-// P_s = G W_s for every stream ([n_streams][d_model][128] fp64).
-hipError_t launch_weights_moments(const float* W, const double* G, const double* hbar, int32_t d_model,
+// moments[s] = [W_s^T G W_s (d x d, row-major), hbar W_s (d)]; scratch holds
+// P_s = G W_s for every stream ([n_streams][d_model][d] fp64). d a multiple of 64.
+hipError_t launch_weights_moments(const float* W, const double* G, const double* hbar, int32_t d_model, int32_t d,
                                   int32_t n_streams, int32_t streams_per_layer, double* scratch, double* moments,
                                   int64_t mom_stride, hipStream_t st) {
   WgemmArgs p{};
@@ -98,40 +101,40 @@ hipError_t launch_weights_moments(const float* W, const double* G, const double*
   p.B = W;
   p.C = scratch;
   p.M = d_model;
-  p.N = 128;
+  p.N = d;
   p.K = d_model;
   p.a_rs = d_model;
   p.a_cs = 1;
   p.a_bs = (int64_t)d_model * d_model;
   p.a_div = streams_per_layer;
-  p.b_rs = 128;
+  p.b_rs = d;
   p.b_cs = 1;
-  p.b_bs = (int64_t)d_model * 128;
-  p.c_rs = 128;
-  p.c_bs = (int64_t)d_model * 128;
-  hipLaunchKernelGGL((wgemm_kernel<double, float>), dim3(d_model / WT, 128 / WT, n_streams), dim3(256), 0, st, p);
+  p.b_bs = (int64_t)d_model * d;
+  p.c_rs = d;
+  p.c_bs = (int64_t)d_model * d;
+  hipLaunchKernelGGL((wgemm_kernel<double, float>), dim3(d_model / WT, d / WT, n_streams), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   WgemmArgs q{};
   q.A = W;  // A(i, k) = W_s[k][i]
   q.B = scratch;
   q.C = moments;
-  q.M = 128;
-  q.N = 128;
+  q.M = d;
+  q.N = d;
   q.K = d_model;
   q.a_rs = 1;
-  q.a_cs = 128;
-  q.a_bs = (int64_t)d_model * 128;
+  q.a_cs = d;
+  q.a_bs = (int64_t)d_model * d;
   q.a_div = 1;
-  q.b_rs = 128;
+  q.b_rs = d;
   q.b_cs = 1;
-  q.b_bs = (int64_t)d_model * 128;
-  q.c_rs = 128;
+  q.b_bs = (int64_t)d_model * d;
+  q.c_rs = d;
   q.c_bs = mom_stride;
-  hipLaunchKernelGGL((wgemm_kernel<float, double>), dim3(128 / WT, 128 / WT, n_streams), dim3(256), 0, st, q);
+  hipLaunchKernelGGL((wgemm_kernel<float, double>), dim3(d / WT, d / WT, n_streams), dim3(256), 0, st, q);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(wmean_kernel, dim3(n_streams), dim3(128), 0, st, W, hbar, d_model, streams_per_layer, moments,
+  hipLaunchKernelGGL(wmean_kernel, dim3(n_streams), dim3(128), 0, st, W, hbar, d_model, d, streams_per_layer, moments,
                      mom_stride);
   return hipGetLastError();
 }

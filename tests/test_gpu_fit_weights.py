@@ -69,3 +69,63 @@ def test_fit_weights_equals_gpu_fit_of_produced_keys():
         assert np.all(cos[_clear(f.eigvals)] >= 1 - 1e-5)
         assert bitw == bitd
         assert np.abs(mw - md).max() <= 1e-4 * np.abs(md).max()
+
+
+def _layer_projection(W, heads, l):
+    """The layer's whole projection: its KV heads' columns side by side, head-major."""
+    return np.ascontiguousarray(np.concatenate([W[l * heads + h] for h in range(heads)], axis=1))
+
+
+@pytest.mark.parametrize("latent_scale", [False, True])
+def test_fit_weights_layer_geometry_matches_oracle(latent_scale):
+    """The paper's own setting: one transform from a layer's whole key projection
+    (d_kv = 4 x 128, groups of 64), with and without the square-root split."""
+    heads, d_model, L = 4, 512, 2
+    H, G, hbar, W = synth.calibration_layers(L, heads, d_model, 2048, seed=5)
+    Wl = np.stack([_layer_projection(W, heads, l) for l in range(L)])
+    d = heads * 128
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    dev = torch.device("cuda:0")
+    codec = S.Codec(sparams(p), L, latent_scale=latent_scale)
+    S.spectra_fit_weights(codec, torch.from_numpy(Wl).to(dev), torch.from_numpy(G).to(dev),
+                          torch.from_numpy(hbar).to(dev), streams_per_layer=1)
+    for l in range(L):
+        basis, mean, bits = codec_state(codec, l)
+        f = O.fit_from_weights(Wl[l], G[l], hbar[l], p, latent_scale=latent_scale)
+        V = basis.astype(np.float64)
+        assert np.abs(V.T @ V - np.eye(d)).max() <= 1e-6
+        D = V.T @ f.second_moment @ V
+        assert np.abs(D - np.diag(np.diag(D))).max() <= 1e-6 * f.eigvals[0]
+        cos = np.sum(V * f.basis.astype(np.float64), axis=0)
+        assert np.all(cos[_clear(f.eigvals)] >= 1 - 1e-6)
+        var = codec.var[l].cpu().numpy()
+        assert np.allclose(var, f.var, rtol=1e-5, atol=1e-7 * f.var.max())
+        assert np.abs(mean - f.mean).max() <= 1e-5 * np.abs(f.mean).max() + 1e-6
+        assert bits == O.allocate_bits(f.var, p)
+        if latent_scale:
+            assert np.allclose(codec.lscale[l].cpu().numpy(), f.scale, rtol=1e-5)
+
+
+def test_fit_weights_equals_gpu_fit_of_produced_keys_d1024():
+    """Through the C ABI at the Llama-3.1-8B key width (8 KV heads side by side, d_kv =
+    1024): the weight fit of a layer's projection W equals the GPU's data fit of the keys
+    k = h W it produces (G = h^T h / N exactly), in widths and separated directions."""
+    heads, d_model = 8, 1024
+    H, G, hbar, W = synth.calibration_layers(1, heads, d_model, 4096, seed=23)
+    Wl = _layer_projection(W, heads, 0)[None]
+    d = heads * 128
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    dev = torch.device("cuda:0")
+    cw = S.Codec(sparams(p), 1)
+    S.spectra_fit_weights(cw, torch.from_numpy(Wl).to(dev), torch.from_numpy(G).to(dev),
+                          torch.from_numpy(hbar).to(dev), streams_per_layer=1)
+    keys = (H[0] @ Wl[0].astype(np.float64)).astype(np.float32)
+    cd = S.Codec(sparams(p), 1)
+    S.spectra_fit_basis(cd, torch.from_numpy(keys[None]).to(dev))
+    bw, mw, bitw = codec_state(cw, 0)
+    bd, md, bitd = codec_state(cd, 0)
+    f = O.fit_from_weights(Wl[0], G[0], hbar[0], p)
+    cos = np.sum(bw.astype(np.float64) * bd.astype(np.float64), axis=0)
+    assert np.all(cos[_clear(f.eigvals)] >= 1 - 1e-5)
+    assert np.abs(mw - md).max() <= 1e-4 * np.abs(md).max()
+    assert bitw == bitd == O.allocate_bits(f.var, p)

@@ -201,6 +201,9 @@ def test_layer_geometry_argument_errors(lib):
     assert lib.spectra_codec_init(ctypes.byref(cl), ctypes.byref(pl), 2) == 0
     assert cl.record_words == 64
     cl.basis = cl.mean = cl.var = cl.bits = 256
+    # the fit from weights takes it: products of d_kv-wide projections in the workspace
+    assert lib.spectra_fit_weights_workspace_bytes(ctypes.byref(cl), 4096) == (2 * (1024 * 1024 + 1024) * 8
+                                                                                + 2 * 4096 * 1024 * 8)
     # the per-head entry points refuse it
     assert lib.spectra_decode_attention(ctypes.byref(cl), ctypes.byref(cl), 256, 256, 64, 8, 256, 1, 1, 8, 8, 0.0,
                                         256, 256, 1 << 20, None) == -2
@@ -227,5 +230,3 @@ def test_layer_geometry_argument_errors(lib):
     ch.basis = ch.mean = ch.var = ch.bits = ch.lscale = 256
     assert lib.spectra_decode(ctypes.byref(ch), 256, 64, 0, 8, 256, None) == -2
     assert b"square-root" in lib.spectra_last_error()
-    cl.lscale = 256
-    assert lib.spectra_layer_decode_attention(*args(32, 8, ws)) == -2
