@@ -4,7 +4,9 @@
 // constant that cancels in the softmax, with q~_h = q_h V_K[kv rows] a d-dimensional
 // latent query; the output is (sum_t p_t c^V_t / sum_t p_t + m_V) V_V[kv rows]^T.
 // Every query head reads the same per-token record, so one tile of records serves all
-// heads of a sequence.
+// heads of a sequence. With the square-root split (Eq. gsvd) the cached coordinate is
+// c'_j = c_j f_j: the keys' 1 / f_j folds into the latent query (q~'_j = q~_j / f_j) and
+// the values' sums are divided by f_j before m_V is added.
 //
 //   layer_qprep_kernel    q~ (scale and log2 e folded in) and its per-group sums;
 //   layer_scores_kernel   scores of all heads for a chunk of 64-token tiles: codes
@@ -95,6 +97,7 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 8; ++r) part[r] = __builtin_fmaf(qv[i + r], V[(int64_t)(i + r) * d], part[r]);
     acc = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+    if (a.lscale_k) acc /= a.lscale_k[(int64_t)b * d + j];
   }
   qtl[tid] = acc;
   if (j < d) {
@@ -550,6 +553,7 @@ __global__ __launch_bounds__(256) void layer_combine_kernel(LayerAttnArgs a) {
     if (kept)
       c = (((ps[0][tid] + ps[1][tid]) + (ps[2][tid] + ps[3][tid])) + ((pz[0][tid] + pz[1][tid]) + (pz[2][tid] + pz[3][tid]))) *
           inv_l;
+    if (a.lscale_v) c /= a.lscale_v[(int64_t)b * d + j];
     a.qt[((int64_t)b * Hq + h) * d + j] = c + a.mean_v[(int64_t)b * d + j];
   }
 }

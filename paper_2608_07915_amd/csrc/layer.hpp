@@ -63,6 +63,8 @@ struct LayerAttnArgs {
   const float* mean_v;
   const uint8_t* bits_k;
   const uint8_t* bits_v;
+  const float* lscale_k;  // NULL or [batch][d]: square-root split factors of the keys' latent
+  const float* lscale_v;  // NULL or [batch][d]: of the values' latent
   const void* q;
   int32_t q_f32;
   int32_t batch, n_q_heads, n_kv_heads, d, Wk, Wv;

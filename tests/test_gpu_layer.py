@@ -318,3 +318,36 @@ def test_layer_attention_tiny_caches(T):
         kvh = np.arange(w.n_q_heads) // (w.n_q_heads // n_kv)
         want = vh[0].reshape(n_kv, 128)[kvh]
         assert rel_l2(out[0], want) <= 1e-5
+
+
+@pytest.mark.parametrize("name,T", [("qwen_layer_8x", 900), ("llama_layer_4x", 333)])
+def test_layer_decode_attention_square_root_split(name, T):
+    """Both latents cached with Eq. gsvd's square-root split (lscale): the attention over
+    the scaled records equals Mode A over the oracle's reconstruction of the same bytes."""
+    w = synth.WORKLOADS[name]
+    xk = synth.numpy_layer_stream(w, 0, 0, 0, max(T_FIT, T))[None]
+    xv = synth.numpy_layer_stream(w, 0, 0, 1, max(T_FIT, T))[None]
+    d = xk.shape[2]
+    n_kv = d // 128
+    p = O.Params(head_dim=d, group_size=64, ratio=8.0)
+    ck = S.Codec(sparams(p), 1, latent_scale=True)
+    cv = S.Codec(sparams(p), 1, latent_scale=True)
+    S.spectra_fit_basis(ck, to_device(xk, w.dtype))
+    S.spectra_fit_basis(cv, to_device(xv, w.dtype))
+    t_cap = (T + 63) // 64 * 64
+    pk, pv = ck.empty_packed(t_cap), cv.empty_packed(t_cap)
+    pk.fill_(-1)
+    pv.fill_(-1)
+    S.spectra_encode(ck, to_device(np.ascontiguousarray(xk[:, :T]), w.dtype), 0, pk, t_cap)
+    S.spectra_encode(cv, to_device(np.ascontiguousarray(xv[:, :T]), w.dtype), 0, pv, t_cap)
+    qs = synth.numpy_query(w, 0, 0, 0)[None]
+    out = S.spectra_layer_decode_attention(ck, cv, pk, pv, t_cap, T, to_device(qs, w.dtype), n_kv).cpu().numpy()
+    W = O.record_words(p)
+    kb, km, kbits = codec_state(ck, 0)
+    vb, vm, vbits = codec_state(cv, 0)
+    fk, fv = ck.lscale[0].cpu().numpy(), cv.lscale[0].cpu().numpy()
+    kh = O.decode(records_of(pk, 0, 0, T, t_cap, W), kb, km, kbits, p, fk)
+    vh = O.decode(records_of(pv, 0, 0, T, t_cap, W), vb, vm, vbits, p, fv)
+    ref = _oracle_layer_attention(values_f64(qs[0], w.dtype), kh, vh, n_kv)
+    for h in range(w.n_q_heads):
+        assert rel_l2(out[0, h], ref[h]) <= ATTN_SAME_TOL, (h, rel_l2(out[0, h], ref[h]))
