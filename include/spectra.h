@@ -251,8 +251,8 @@ spectra_status spectra_decode_attention(const spectra_codec* ck, const spectra_c
  * spectra_decode_attention. inv_freq: device fp32 [d/2], any frequencies (base^(-2i/d)
  * or a scaled set). Angles are reduced in fp64 before fp32 cos/sin. Other arguments,
  * the workspace (spectra_attention_workspace_bytes) and the errors as
- * spectra_decode_attention; SPECTRA_EUNSUPPORTED for more than 4 query heads per KV
- * head or records wider than 16 words. Asynchronous.
+ * spectra_decode_attention; SPECTRA_EUNSUPPORTED for more than 8 query heads per KV
+ * head or records wider than 32 words. Asynchronous.
  * ------------------------------------------------------------------------- */
 spectra_status spectra_decode_attention_rope(const spectra_codec* ck, const spectra_codec* cv,
                                              const uint32_t* packed_k, const uint32_t* packed_v,

@@ -506,8 +506,8 @@ spectra_status spectra_decode_attention_rope(const spectra_codec* ck, const spec
                                               q, q_dt, batch, n_q_heads, n_kv_heads, softmax_scale, out, workspace,
                                               ws_bytes, &a);
   if (st != SPECTRA_OK) return st;
-  if (a.n_qh > 4) return fail(SPECTRA_EUNSUPPORTED, "decode_attention_rope: at most 4 query heads per kv head");
-  if (a.Wk > 16 || a.Wv > 16) return fail(SPECTRA_EUNSUPPORTED, "decode_attention_rope: records of at most 16 words");
+  if (a.n_qh > 8) return fail(SPECTRA_EUNSUPPORTED, "decode_attention_rope: at most 8 query heads per kv head");
+  if (a.Wk > 32 || a.Wv > 32) return fail(SPECTRA_EUNSUPPORTED, "decode_attention_rope: records of at most 32 words");
   if (!inv_freq || !aligned(inv_freq, 4)) return fail(SPECTRA_EINVAL, "decode_attention_rope: inv_freq must be non-null");
   if (q_position < 0) return fail(SPECTRA_EINVAL, "decode_attention_rope: q_position negative");
   a.inv_freq = inv_freq;

@@ -32,7 +32,7 @@ constexpr int RTT = 64;           // tokens per tile
 constexpr int RKROW = RTT + 4;    // floats per reconstructed-key row (dimension x token, 16-byte rows)
 constexpr int RCS2 = 2 * 64 + 2;  // floats per row of the interleaved in-tile cos/sin table
 constexpr int RCP = 136;          // bf16 per token row of the unpacked key codes (4 kept groups + pad)
-constexpr int RWMAX = 16;         // record words per tensor staged for this kernel
+constexpr int RWMAX = 32;         // record words per tensor staged for this kernel
 constexpr int RWAVES = 8;         // wavefronts per workgroup
 constexpr int RTHREADS = 64 * RWAVES;
 constexpr int RPP = 64 / RWAVES;  // dimension pairs per thread in the score step
@@ -51,7 +51,8 @@ __host__ __device__ constexpr int rope_lds_bytes(int nh) { return rope_off_wt(nh
 static_assert(rope_off_kmeta() % 16 == 0 && rope_off_kh() % 16 == 0 && rope_off_qpp(4) % 16 == 0, "16-byte reads");
 static_assert(rope_off_wt(4) % 16 == 0 && (WROW * 2) % 16 == 0, "weight rows are read 16 bytes at a time");
 static_assert(2 * (2 * 4) * AROW * 4 <= D * RKROW * 4, "value sums of both token halves reuse the key rows");
-static_assert(rope_lds_bytes(4) <= 160 * 1024, "LDS of one CU");
+static_assert(rope_lds_bytes(4) <= 160 * 1024 && rope_lds_bytes(8) <= 160 * 1024, "LDS of one CU");
+static_assert(rope_off_qpp(8) % 16 == 0 && rope_off_wt(8) % 16 == 0, "16-byte reads");
 
 // cos and sin of an angle given exactly in fp64 (a position below 2^28 times an
 // fp32 frequency needs at most 52 significant bits). Cody-Waite reduction by pi/2
@@ -506,9 +507,13 @@ hipError_t launch_attention_rope(const AttnArgs& a, hipStream_t st) {
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return e;
-  if (lds < rope_lds_bytes(4)) return hipErrorInvalidConfiguration;
+  const int nh = a.n_qh <= 4 ? 4 : 8;
+  if (lds < rope_lds_bytes(nh)) return hipErrorInvalidConfiguration;
   const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
-  hipLaunchKernelGGL(rope_attn_kernel<1>, grid, dim3(RTHREADS), rope_lds_bytes(4), st, a);
+  if (nh == 4)
+    hipLaunchKernelGGL(rope_attn_kernel<1>, grid, dim3(RTHREADS), rope_lds_bytes(4), st, a);
+  else
+    hipLaunchKernelGGL(rope_attn_kernel<2>, grid, dim3(RTHREADS), rope_lds_bytes(8), st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_combine(a, st);

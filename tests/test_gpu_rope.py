@@ -102,3 +102,21 @@ def test_zero_frequencies_match_latent_attention():
                                         torch.zeros(64, dtype=torch.float32, device="cuda")).cpu().numpy()
     b = S.spectra_decode_attention(ck, cv, pk, pv, t_cap, T, q, w.n_kv_heads).cpu().numpy()
     assert max(rel_l2(a[0, h], b[0, h]) for h in range(w.n_q_heads)) <= ATTN_SAME_TOL
+
+
+def test_rope_attention_qwen_gqa7_8x():
+    """Qwen2.5-7B's 28:4 grouping (seven query heads per KV head: two head quads) at 8x."""
+    w = synth.WORKLOADS["qwen_layer_8x"]
+    p = O.Params(ratio=8.0)
+    run_rope(w, 1300, p, p)
+
+
+@pytest.mark.parametrize("n_qh,ratio", [(8, 2.0), (5, 16.0 / 5.0)])
+def test_rope_attention_wide_records(n_qh, ratio):
+    """Records wider than 16 words (32 words at 2x, 20 at 3.2x) with five to eight query
+    heads per KV head."""
+    from dataclasses import replace
+    w = replace(synth.WORKLOADS["llama_layer_4x"], n_kv_heads=2, n_q_heads=2 * n_qh)
+    p = O.Params(ratio=ratio)
+    assert O.record_words(p) in (32, 20)
+    run_rope(w, 900, p, p)
