@@ -115,17 +115,20 @@ __device__ __forceinline__ Kept read_kept(const uint8_t* bits_s) {
 // ---------------------------------------------------------------------------
 // Packing of 16 codes held by one lane (lane half h of a 32x32 MFMA tile holds
 // in-group coefficients 16h..16h+15 of one token). The group payload of b words
-// takes the lower half's 16b bits first, then the upper half's.
+// takes the lower half's 16b bits first, then the upper half's. Code j is the
+// low B bits of q[j] (higher bits are ignored).
 // ---------------------------------------------------------------------------
 template <int B>
 __device__ __forceinline__ void pack16(const uint32_t (&q)[16], uint32_t (&P)[4]) {
+  constexpr uint32_t M = (1u << B) - 1u;
 #pragma unroll
   for (int i = 0; i < 4; ++i) P[i] = 0;
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     const int pos = j * B;
-    P[pos >> 5] |= q[j] << (pos & 31);
-    if ((pos & 31) + B > 32) P[(pos >> 5) + 1] |= q[j] >> (32 - (pos & 31));
+    const uint32_t c = q[j] & M;
+    P[pos >> 5] |= c << (pos & 31);
+    if ((pos & 31) + B > 32) P[(pos >> 5) + 1] |= c >> (32 - (pos & 31));
   }
 }
 

@@ -88,12 +88,12 @@ __device__ __forceinline__ void append_token(const AttnArgs& a, int s, int tid, 
     const int slot = wave;
     if (slot < K.n) {
       const int grp = pick4(K.grp, slot);
-      float mv[16];
+      f32x16 nm;
       const float* m = (which ? a.mean_v : a.mean_k) + (int64_t)s * D + G * grp + 16 * h;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) mv[j] = m[j];
+      for (int j = 0; j < 16; ++j) nm[j] = -m[j];
       encode_block_streamed<F32, ROWB>(xs + which * 32 * ROWB, 0, col, h, (which ? a.basis_v : a.basis_k) + (int64_t)s * D * D,
-                                       grp, mv, a.t_new, a.t_new, a.t_new + 1, sbase, W, slot, pick4(K.bits, slot),
+                                       grp, nm, a.t_new, a.t_new, a.t_new + 1, sbase, W, slot, pick4(K.bits, slot),
                                        pick4(K.pay, slot), packed);
     }
     // padding words of the record are zero

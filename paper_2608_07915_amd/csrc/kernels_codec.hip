@@ -19,45 +19,257 @@ namespace spectra_dev {
 // ---------------------------------------------------------------------------
 // Encode
 // ---------------------------------------------------------------------------
-template <bool F32IN>
-__global__ __launch_bounds__(256, 2) void encode_kernel(EncodeArgs a) {
-  constexpr int ST = F32IN ? 64 : 128;             // tokens per super-tile
-  constexpr int ROWB = F32IN ? (512 + 16) : (256 + 16);  // padded LDS row (bank spread)
-  __shared__ __attribute__((aligned(16))) uint8_t xs[ST * ROWB];
+// Super-tile st covers slots [slot0, slot0 + ST); rows [lo, hi) hold the call's
+// tokens and only the 32-row MFMA blocks [b_lo, b_hi) that meet them are
+// projected.
+struct Span {
+  int64_t slot0;
+  int lo, hi, b_lo, b_hi;
+};
+__device__ __forceinline__ Span encode_span(const EncodeArgs& a, int64_t st, int ST) {
+  const int64_t end = a.t0 + a.n;
+  Span sp;
+  sp.slot0 = ((a.t0 >> 6) << 6) + st * ST;
+  sp.lo = (int)(a.t0 > sp.slot0 ? a.t0 - sp.slot0 : 0);
+  sp.hi = (int)(end - sp.slot0 < ST ? end - sp.slot0 : ST);
+  sp.b_lo = sp.lo >> 5;
+  sp.b_hi = (sp.hi + 31) >> 5;
+  return sp;
+}
 
+// Wave roles: wpg waves per kept group, each taking every wpg-th 32-token block.
+// PIPE: the next block's MFMAs are issued before this block is quantized, so the
+// matrix cores and the vector ALU work on two blocks at once.
+// Records go to `out` + sbase, tile by tile as in HBM (out = a.packed, or the
+// LDS staging of one super-tile with sbase = 0 and slot0 taken as tile 0).
+template <bool F32IN, int ROWB, bool PIPE>
+__device__ __forceinline__ void encode_span_blocks(const EncodeArgs& a, const uint8_t* xs, const Span& sp, int phase,
+                                                   int wpg, int col, int h, const bf16x8 (&Va)[3][8],
+                                                   const f32x16& nm, uint32_t* out, int64_t sbase, int slot, int gbits,
+                                                   int gpay) {
+  if (sp.b_lo + phase >= sp.b_hi) return;
+  auto proj = [&](int beta) {
+    return project_block<F32IN, ROWB>(xs, beta, col, h, nm, [&](int p, int k) { return Va[p][k]; });
+  };
+  // record word 0 of the super-tile's first tile; row r of the super-tile is at
+  // (r / 64) * 64 W + r % 64 from it
+  uint32_t* tile0 = out == a.packed ? a.packed + sbase + (sp.slot0 >> 6) * (int64_t)(TILE * a.W) : out;
+  int beta = sp.b_lo + phase;
+  f32x16 acc = proj(beta);
+  for (;;) {
+    const int nb = beta + wpg;
+    const bool more = nb < sp.b_hi;
+    f32x16 nacc = acc;
+    if (PIPE && more) nacc = proj(nb);
+    const int r = 32 * beta + col;
+    store_block(acc, tile0 + (r >> 6) * (TILE * a.W) + (r & 63), r >= sp.lo && r < sp.hi, h, slot, gbits, gpay);
+    if (!more) break;
+    acc = PIPE ? nacc : proj(nb);
+    beta = nb;
+  }
+}
+
+// Staged variant: records go to the LDS staging of the super-tile (all rows,
+// valid or not: only the call's rows are copied out). The loop is instantiated
+// per code width, so a block's quantization is straight-line code that the
+// scheduler interleaves with the next block's MFMA chain.
+template <int B>
+__device__ __forceinline__ void encode_span_blocks_staged(const uint8_t* xs, const Span& sp, int phase, int wpg,
+                                                          int col, int h, const bf16x8 (&Va)[3][8], const f32x16& nm,
+                                                          uint32_t* rs, uint32_t* dummy, int W, int slot, int gpay) {
+  auto proj = [&](int beta) {
+    return project_block<false, 0>(xs, beta, col, h, nm, [&](int p, int k) { return Va[p][k]; });
+  };
+  auto stage = [&](const f32x16& acc, int beta) {
+    uint32_t P[4];
+    const uint32_t meta = quantize_pack<B>(acc, P);
+    const int r = 32 * beta + col;
+    stage_record_words<B>(rs + (r >> 6) * (TILE * W) + (r & 63), dummy, h, slot, gpay, meta, P);
+  };
+  int beta = sp.b_lo + phase;
+  f32x16 acc = proj(beta);
+  for (int nb = beta + wpg; nb < sp.b_hi; nb += wpg) {
+    const f32x16 nacc = proj(nb);
+    stage(acc, beta);
+    // interleave: each MFMA of the next block with a share of this block's VALU work
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // the K step's LDS operand read
+#pragma unroll
+      for (int p = 0; p < 3; ++p) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // five VALU
+      }
+    }
+    acc = nacc;
+    beta = nb;
+  }
+  stage(acc, beta);
+}
+
+// Padding words of the records of rows [lo, hi) are zero.
+__device__ __forceinline__ void encode_padding(const EncodeArgs& a, const Span& sp, int64_t sbase, int used, int tid) {
+  const int npad = a.W - used, nrow = sp.hi - sp.lo;
+  for (int c = tid; c < nrow * npad; c += 256) {
+    const int row = sp.lo + c % nrow, w = used + c / nrow;
+    a.packed[rec_word(sbase, sp.slot0 + row, a.W, w)] = 0u;
+  }
+}
+
+// bf16 tokens: super-tiles of 128 tokens (32 KB) are copied straight from HBM
+// into one of two LDS buffers (global_load_lds, 16 bytes per lane) while the
+// other buffer is projected; rows are 256 bytes with the 16-byte chunks
+// XOR-swizzled by the row index, so the MFMA operand reads of 32 rows spread
+// over the LDS banks. Rows outside the call's tokens load a clamped in-range
+// row (their blocks are not projected or their records not stored).
+//
+// STAGED: the super-tile's records (two 64-token tiles, word-major, the layout
+// they have in HBM) are assembled in LDS and written with one coalesced
+// 16-byte store per 4 tokens of a word; each wave then waits only for its
+// loads of the next super-tile (the stores it issued after them are not
+// waited for). Otherwise every lane stores its own record words.
+constexpr int EST = 128;
+
+__host__ __device__ constexpr size_t encode_bf16_lds_bytes(int W, bool staged) {
+  return (size_t)2 * EST * 256 + (staged ? (size_t)(EST * W + 256) * 4 : 0);  // + a scratch word per lane
+}
+
+// s_waitcnt with vmcnt(n) (n < 16), expcnt and lgkmcnt not waited for
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+template <bool STAGED>
+__global__ __launch_bounds__(256, 2) void encode_bf16_kernel(EncodeArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t esmem[];
+  uint8_t(*xs)[EST * 256] = reinterpret_cast<uint8_t(*)[EST * 256]>(esmem);
+  uint32_t* rs = reinterpret_cast<uint32_t*>(esmem + 2 * EST * 256);  // STAGED: [2][W][64] record words, [4][64] scratch
   const int s = blockIdx.y;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: role selection stays scalar
   const int h = lane >> 5, col = lane & 31;
-
   const int64_t first_tile = a.t0 >> 6;
-  const int64_t end = a.t0 + a.n;                       // exclusive slot
-  const int64_t n_tiles = ((end - 1) >> 6) - first_tile + 1;
+  const int64_t n_tiles = ((a.t0 + a.n - 1) >> 6) - first_tile + 1;
+  const int64_t n_st = (n_tiles * TILE + EST - 1) / EST;
+  const char* xb = reinterpret_cast<const char*>(a.x) + (int64_t)s * a.stream_stride * 2;
+  // one global_load_lds fills 1 KB: rows 4m..4m+3 of the super-tile; lane i
+  // brings chunk (i % 16) ^ (row % 16) of row 4m + i / 16. Wave w issues m = 8w..8w+7.
+  const int lrow = lane >> 4;
+  auto stage = [&](int64_t st, int b) {
+    const int64_t slot0 = (first_tile << 6) + st * EST;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int m = 8 * wave + i, row = 4 * m + lrow;
+      const int chunk = (lane & 15) ^ (row & 15);
+      int64_t t = slot0 + row - a.t0;
+      t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
+      __builtin_amdgcn_global_load_lds(xb + t * a.token_stride * 2 + chunk * 16, &xs[b][m * 1024], 16, 0, 0);
+    }
+  };
+  int64_t st = blockIdx.x;
+  if (st >= n_st) return;
+  stage(st, 0);
+
+  const Kept K = read_kept(a.bits + (int64_t)s * NG);
+  const int W = a.W;
+  if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
+  const int64_t sbase = (int64_t)s * a.t_cap * W;
+  const int wpg = K.n ? 4 / K.n : 0;
+  const bool active = K.n > 0 && wave < K.n * wpg;
+  const int slot = active ? wave / wpg : 0;
+  const int phase = active ? wave % wpg : 0;
+  const int grp = pick4(K.grp, slot);
+  const int gbits = pick4(K.bits, slot);
+  const int gpay = pick4(K.pay, slot);
+  bf16x8 Va[3][8];
+  f32x16 nm;
+  if (active) load_group_operands(a.basis + (int64_t)s * D * D, a.mean + (int64_t)s * D, grp, col, h, Va, nm);
+  if constexpr (STAGED) {
+    // padding words stay zero: no wave writes words >= K.used
+    for (int i = tid; i < EST * W; i += 256) rs[i] = 0u;
+  }
+  int buf = 0;
+  wait_vmcnt<0>();  // this super-tile is in LDS
+  __syncthreads();
+  for (;;) {
+    const int64_t st_next = st + gridDim.x;
+    if (st_next < n_st) stage(st_next, buf ^ 1);
+    const Span sp = encode_span(a, st, EST);
+    if constexpr (STAGED) {
+      if (active)
+        with_bits(gbits, [&](auto bc) {
+          encode_span_blocks_staged<decltype(bc)::value>(xs[buf], sp, phase, wpg, col, h, Va, nm, rs,
+                                                         rs + EST * W + 64 * wave, W, slot, gpay);
+        });
+      __syncthreads();  // the records of the super-tile are in LDS
+      uint32_t* dst = a.packed + sbase + (sp.slot0 >> 6) * (int64_t)(TILE * W);
+      const bool full = sp.lo == 0 && sp.hi == EST;
+      // 16-byte piece c = tid + 256 q of the 2 * 64 * W words; this wave's pieces
+      // for q < nst (the first lane of each is in range), so the wave issues
+      // exactly nst stores after its loads of the next super-tile
+      const int nst = (32 * W - 64 * wave + 255) >> 8;
+      if (full) {
+        for (int q = 0; q < nst; ++q) {
+          const int c = tid + 256 * q;
+          if (c < 32 * W) *reinterpret_cast<u32x4*>(dst + 4 * c) = *reinterpret_cast<const u32x4*>(rs + 4 * c);
+        }
+      } else {
+        for (int i = tid; i < EST * W; i += 256) {
+          const int row = ((i / (TILE * W)) << 6) + (i & 63);
+          if (row >= sp.lo && row < sp.hi) dst[i] = rs[i];
+        }
+      }
+      st = st_next;
+      if (st >= n_st) break;
+      // wait for this wave's loads of the next super-tile; the nst stores issued
+      // after them may still be in flight (vector memory operations complete in
+      // issue order; nothing else in the loop touches vector memory)
+      if (!full || nst <= 0 || nst > 5)
+        wait_vmcnt<0>();
+      else if (nst == 1)
+        wait_vmcnt<1>();
+      else if (nst == 2)
+        wait_vmcnt<2>();
+      else if (nst == 3)
+        wait_vmcnt<3>();
+      else if (nst == 4)
+        wait_vmcnt<4>();
+      else
+        wait_vmcnt<5>();
+    } else {
+      if (active) encode_span_blocks<false, 0, true>(a, xs[buf], sp, phase, wpg, col, h, Va, nm, a.packed, sbase, slot,
+                                                     gbits, gpay);
+      encode_padding(a, sp, sbase, K.used, tid);
+      st = st_next;
+      if (st >= n_st) break;
+      wait_vmcnt<0>();  // the next super-tile is in LDS
+    }
+    __syncthreads();  // ... for every wave; every wave is done with this super-tile
+    buf ^= 1;
+  }
+}
+
+// fp32 tokens: super-tiles of 64 tokens staged through registers into padded
+// LDS rows; the next super-tile's rows are loaded into registers while this one
+// is projected and quantized.
+__global__ __launch_bounds__(256, 2) void encode_f32_kernel(EncodeArgs a) {
+  constexpr int ST = 64;
+  constexpr int ROWB = 512 + 16;  // padded LDS row (bank spread)
+  __shared__ __attribute__((aligned(16))) uint8_t xs[ST * ROWB];
+  const int s = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: role selection stays scalar
+  const int h = lane >> 5, col = lane & 31;
+  const int64_t first_tile = a.t0 >> 6;
+  const int64_t n_tiles = ((a.t0 + a.n - 1) >> 6) - first_tile + 1;
   const int64_t n_st = (n_tiles * TILE + ST - 1) / ST;
   const char* xb = reinterpret_cast<const char*>(a.x);
-  constexpr int ESZ = F32IN ? 4 : 2;
-  constexpr int CPR = (D * ESZ) / 16;  // 16-byte chunks per token row
-  // Super-tile st covers slots [slot0, slot0 + ST); rows [lo, hi) hold the call's
-  // tokens and only the 32-row MFMA blocks [b_lo, b_hi) that meet them are
-  // staged and projected.
-  struct Span {
-    int64_t slot0;
-    int lo, hi, b_lo, b_hi;
-  };
-  auto span = [&](int64_t st) {
-    Span sp;
-    sp.slot0 = (first_tile << 6) + st * ST;
-    sp.lo = (int)(a.t0 > sp.slot0 ? a.t0 - sp.slot0 : 0);
-    sp.hi = (int)(end - sp.slot0 < ST ? end - sp.slot0 : ST);
-    sp.b_lo = sp.lo >> 5;
-    sp.b_hi = (sp.hi + 31) >> 5;
-    return sp;
-  };
-  // The rows of those blocks are staged in LDS in 16-byte chunks (coalesced); rows
-  // outside the call's token range are zero. A super-tile is PRE chunks per thread;
-  // the next super-tile's chunks are loaded into registers while this one is
-  // projected and quantized, then written to LDS.
+  constexpr int CPR = (D * 4) / 16;  // 16-byte chunks per token row
   constexpr int PRE = (ST * CPR) / 256;
   static_assert(PRE * 256 == ST * CPR, "staging split");
+  // rows of the projected blocks are staged (rows outside the call's tokens are zero)
   auto load_stage = [&](const Span& sp, u32x4 (&r)[PRE]) {
 #pragma unroll
     for (int i = 0; i < PRE; ++i) {
@@ -66,7 +278,7 @@ __global__ __launch_bounds__(256, 2) void encode_kernel(EncodeArgs a) {
       const int64_t t = sp.slot0 + row - a.t0;
       r[i] = u32x4{0u, 0u, 0u, 0u};
       if (row >= 32 * sp.b_lo && row < 32 * sp.b_hi && t >= 0 && t < a.n)
-        r[i] = *reinterpret_cast<const u32x4*>(xb + ((int64_t)s * a.stream_stride + t * a.token_stride) * ESZ + part * 16);
+        r[i] = *reinterpret_cast<const u32x4*>(xb + ((int64_t)s * a.stream_stride + t * a.token_stride) * 4 + part * 16);
     }
   };
   auto store_stage = [&](const Span& sp, const u32x4 (&r)[PRE]) {
@@ -79,17 +291,12 @@ __global__ __launch_bounds__(256, 2) void encode_kernel(EncodeArgs a) {
   };
   int64_t st = blockIdx.x;
   if (st >= n_st) return;
-  // The first rows are requested before the width table is needed, so their latency
-  // overlaps the basis loads (which depend on it).
   u32x4 pre[PRE];
-  load_stage(span(st), pre);
-
+  load_stage(encode_span(a, st, ST), pre);
   const Kept K = read_kept(a.bits + (int64_t)s * NG);
   const int W = a.W;
   if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
   const int64_t sbase = (int64_t)s * a.t_cap * W;
-
-  // Wave roles: wpg waves per kept group, each taking every wpg-th 32-token block.
   const int wpg = K.n ? 4 / K.n : 0;
   const bool active = K.n > 0 && wave < K.n * wpg;
   const int slot = active ? wave / wpg : 0;
@@ -97,30 +304,18 @@ __global__ __launch_bounds__(256, 2) void encode_kernel(EncodeArgs a) {
   const int grp = pick4(K.grp, slot);
   const int gbits = pick4(K.bits, slot);
   const int gpay = pick4(K.pay, slot);
-
   bf16x8 Va[3][8];
-  float mv[16];
-  if (active) load_group_operands(a.basis + (int64_t)s * D * D, a.mean + (int64_t)s * D, grp, col, h, Va, mv);
-
+  f32x16 nm;
+  if (active) load_group_operands(a.basis + (int64_t)s * D * D, a.mean + (int64_t)s * D, grp, col, h, Va, nm);
   for (;;) {
-    const Span sp = span(st);
-    const int64_t slot0 = sp.slot0;
-    const int b_lo = sp.b_lo, b_hi = sp.b_hi, lo = sp.lo, hi = sp.hi;
+    const Span sp = encode_span(a, st, ST);
     store_stage(sp, pre);
     __syncthreads();  // staged rows visible
     const int64_t st_next = st + gridDim.x;
-    if (st_next < n_st) load_stage(span(st_next), pre);
-
-    if (active) {
-      for (int beta = b_lo + phase; beta < b_hi; beta += wpg)
-        encode_block<F32IN, ROWB>(xs, beta, col, h, Va, mv, slot0, a.t0, end, sbase, W, slot, gbits, gpay, a.packed);
-    }
-    // Padding words of the record are zero.
-    const int npad = W - K.used, nrow = hi - lo;
-    for (int c = tid; c < nrow * npad; c += 256) {
-      const int row = lo + c % nrow, w = K.used + c / nrow;
-      a.packed[rec_word(sbase, slot0 + row, W, w)] = 0u;
-    }
+    if (st_next < n_st) load_stage(encode_span(a, st_next, ST), pre);
+    if (active)
+      encode_span_blocks<true, ROWB, false>(a, xs, sp, phase, wpg, col, h, Va, nm, a.packed, sbase, slot, gbits, gpay);
+    encode_padding(a, sp, sbase, K.used, tid);
     st = st_next;
     if (st >= n_st) break;
     __syncthreads();  // every wave is done with the staged rows
@@ -386,10 +581,20 @@ hipError_t launch_encode(const EncodeArgs& a, bool f32_input, hipStream_t st) {
   if (per_stream > n_st) per_stream = n_st;
   if (per_stream < 1) per_stream = 1;
   dim3 grid((unsigned)per_stream, (unsigned)a.n_streams);
-  if (f32_input)
-    hipLaunchKernelGGL(encode_kernel<true>, grid, dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(encode_kernel<false>, grid, dim3(256), 0, st, a);
+  if (f32_input) {
+    hipLaunchKernelGGL(encode_f32_kernel, grid, dim3(256), 0, st, a);
+  } else {
+    // staged records (W <= 64 words: at most 96 KB of LDS) when the device has the LDS
+    int dev = 0, lds_max = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e != hipSuccess) return e;
+    const size_t lds = encode_bf16_lds_bytes(a.W, true);
+    if (a.W <= 64 && lds <= (size_t)lds_max)
+      hipLaunchKernelGGL(encode_bf16_kernel<true>, grid, dim3(256), lds, st, a);
+    else
+      hipLaunchKernelGGL(encode_bf16_kernel<false>, grid, dim3(256), encode_bf16_lds_bytes(a.W, false), st, a);
+  }
   return hipGetLastError();
 }
 
