@@ -37,27 +37,39 @@ CALIB_BYTES = 256 << 20
 
 # HBM bytes per decode-step call from rocprofv3 counters (FETCH_SIZE and WRITE_SIZE
 # passes over `bench.py --steps 1 --warmup 0 --decode-steps 2 --no-cpu-baseline
-# --eager --copy-calibration`), scaled by the counters' reading of the 256 MiB
-# copy (FETCH_SIZE reads 131089 KiB for 256 MiB read: x2.0; WRITE_SIZE reads
+# --eager --copy-calibration --skip-configs`), scaled by the counters' reading of the
+# 256 MiB copy (FETCH_SIZE reads 131093 KiB for 256 MiB read: x2.0; WRITE_SIZE reads
 # 262148 KiB for 256 MiB written: x1.0). Valid only for the kernel sources they
 # were taken on (sha256 over DECODE_STEP_SOURCES); otherwise `traffic` is null.
 DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "encode_dev.hpp", "device_common.hpp",
                        "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "b9f6b8d34df74539f80ce511cdfd029384db6b10edf384cc3c7ffe5576ae1b9b": {
-        "fetch_bytes": 74540646, "write_bytes": 1674240,
-        "per_kernel": {"attn_kernel<1,8,8,true>": [70700646, 1657856], "combine_kernel": [3840000, 16384]}},
+    "25e8171641d32dcbbb71939be452dd334161433e5f955c888b35be1d30f1abd1": {
+        "fetch_bytes": 74476544, "write_bytes": 1674240, "mfma_busy": 0.095,
+        "per_kernel": {"attn_kernel<1,8,8,true>": [70701261, 1657856], "combine_kernel": [3775283, 16384]}},
+}
+# The same passes over the bulk encode of one codec (256 streams x 131072 tokens):
+# HBM bytes per call and the matrix cores' busy fraction (SQ_VALU_MFMA_BUSY_CYCLES
+# over GRBM_GUI_ACTIVE x 1024 SIMDs), keyed by sha256 over ENCODE_SOURCES.
+ENCODE_SOURCES = ("kernels_codec.hip", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
+MEASURED_ENCODE = {
+    "3529804415461ff5fdb2dba172de982da0167d2cb1a04d999629913f1fcdc58e": {
+        "fetch_bytes": 8665338880, "write_bytes": 1073741824, "mfma_busy": 0.348},
 }
 
 
-def decode_step_sources_sha256():
+def sources_sha256(files):
     import hashlib
     h = hashlib.sha256()
-    for f in DECODE_STEP_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, "paper_2608_07915_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def decode_step_sources_sha256():
+    return sources_sha256(DECODE_STEP_SOURCES)
 METRIC = "KV encode GB/s + compressed decode-attn tokens/s, % of HBM peak, at 8x"
 
 
@@ -527,9 +539,10 @@ def main():
     tokens_per_call = n_seq * float(np.mean([T + s + 1 for s in range(n_dec)])) if n_dec else 0.0
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     # counters were taken on the default workload with symmetric records
-    measured = (MEASURED_TRAFFIC.get(decode_step_sources_sha256())
-                if (w.name, args.kappa) == ("llama_model_131k_8x", 0.5) else None)
+    headline = (w.name, args.kappa) == ("llama_model_131k_8x", 0.5)
+    measured = MEASURED_TRAFFIC.get(decode_step_sources_sha256()) if headline else None
     traffic = (measured["fetch_bytes"] + measured["write_bytes"]) if measured else None
+    enc_counters = MEASURED_ENCODE.get(sources_sha256(ENCODE_SOURCES)) if headline else None
 
     result = {
         "metric": METRIC,
@@ -553,13 +566,18 @@ def main():
         },
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
         "encode": {"ms": round(enc_ms, 3), "GBps": round(enc_bytes / (enc_ms * 1e-3) / 1e9, 1),
-                   "frac": round(enc_bytes / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
+                   "frac": round(enc_bytes / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                   "algorithmic_bytes": enc_bytes,
+                   "traffic": (2 * (enc_counters["fetch_bytes"] + enc_counters["write_bytes"])
+                               if enc_counters else None),
+                   "mfma_busy": enc_counters["mfma_busy"] if enc_counters else None},
         "decode_step": {"ms_per_layer_call": round(att_call_ms, 4), "GBps": round(att_gbps, 1),
                              "frac": round(att_gbps / HBM_PEAK_GBPS, 4),
                              "cache_tokens_per_s": round(tokens_per_call / (att_call_ms * 1e-3), 1),
                              "generated_tokens_per_s": round(1.0 / (att_call_ms * 1e-3 * L), 2)},
         "roofline": {"bound": "hbm", "achieved": round(att_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(att_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "mfma_busy": measured["mfma_busy"] if measured else None,
                      "kernel": "decode_step (split-K scan with in-kernel query prep and append, then combine), per layer call",
                      "algorithmic_bytes_per_launch": round(att_call_bytes)},
         "traffic_detail": measured,
