@@ -68,6 +68,7 @@ struct AttnArgs {
   float scale_log2;      // softmax scale * log2(e)
   int32_t n_chunks;      // split of the token range per (batch, kv head)
   int32_t tiles_per_chunk;
+  int32_t group_major;   // scan grid order: 0 = (chunk, kv head, sequence); 1 = 1-D, chunk-major over groups
   // decode step only: the new token of every stream is encoded into slot t_new
   // of app_k / app_v (the same caches as packed_k / packed_v) before attention
   const void* k_new;     // [batch][n_kv_heads][128], fp32 if app_f32 else bf16

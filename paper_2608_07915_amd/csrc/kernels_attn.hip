@@ -387,7 +387,16 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t qa_s[NQ * QA_QUAD];
   __shared__ float qbar_s[16 * 4];
 
-  const int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  // a.group_major: one-dimensional grid, workgroup i = chunk * groups + group, so that
+  // (dispatched round-robin over the XCDs) every chunk of a (sequence, kv head) runs on
+  // the same XCD and its L2 serves that head's key basis to all of them
+  int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  if (a.group_major) {
+    const int ngr = a.n_kv_heads * a.batch, gid = (int)(blockIdx.x % (unsigned)ngr);
+    chunk = (int)(blockIdx.x / (unsigned)ngr);
+    kv = gid % a.n_kv_heads;
+    b = gid / a.n_kv_heads;
+  }
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int s = b * a.n_kv_heads + kv;
   const int nqh = a.n_qh;
@@ -795,8 +804,11 @@ static void launch_nq_pw(const AttnArgs& a, hipStream_t st) {
   size_t lds = tiles > merge ? tiles : merge;
   if ((size_t)qprep_scratch_bytes(NQ) > lds) lds = qprep_scratch_bytes(NQ);
   if (a.app_k && (size_t)append_stage_bytes(a.app_f32 != 0) > lds) lds = append_stage_bytes(a.app_f32 != 0);
-  const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
-  hipLaunchKernelGGL((attn_kernel<NQ, PK, PV, EXACT>), grid, dim3(256), lds, st, a);
+  // more (sequence, kv head) groups than XCDs: chunks of a group kept on one XCD
+  AttnArgs g = a;
+  g.group_major = a.n_kv_heads * a.batch > 8 ? 1 : 0;
+  const dim3 grid = g.group_major ? dim3(a.n_chunks * a.n_kv_heads * a.batch, 1, 1) : dim3(a.n_chunks, a.n_kv_heads, a.batch);
+  hipLaunchKernelGGL((attn_kernel<NQ, PK, PV, EXACT>), grid, dim3(256), lds, st, g);
 }
 
 // Prefetch shapes. Up to eight query heads per KV head, records of unequal width
