@@ -289,19 +289,24 @@ __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
 // ---------------------------------------------------------------------------
 // Decode (Mode A)
 // ---------------------------------------------------------------------------
-constexpr int LD_TOK = 128;       // tokens per workgroup
-constexpr int LD_CH = 128;        // output channels per workgroup
+// One workgroup: LD_CH = 64 output channels x LD_NT = 2 tiles of 128 tokens. The
+// group's basis operands and the mean term m V^T are built once per workgroup and
+// serve both tiles (the L2 reads of basis rows per token are what bound this kernel).
+constexpr int LD_TOK = 128;       // tokens per tile
+constexpr int LD_NT = 2;          // tiles per workgroup
+constexpr int LD_CH = 64;         // output channels per workgroup
 constexpr int LD_P = LG + 8;      // bf16 per LDS row (144 bytes)
+constexpr int LD_R = 2 * LD_NT;   // staged (token, 8-code) pieces per thread
 
 __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t vsl[3][LD_CH][LD_P];   // basis columns of the group, [channel][coef]
-  __shared__ __attribute__((aligned(16))) uint16_t cod[LD_TOK][LD_P];     // codes, [token][coef]
-  __shared__ __attribute__((aligned(16))) float sl[LD_TOK], zl[LD_TOK], vsum[LD_CH], bias[LD_CH];
+  __shared__ __attribute__((aligned(16))) uint16_t vsl[3][LD_CH][LD_P];          // basis columns of the group, [channel][coef]
+  __shared__ __attribute__((aligned(16))) uint16_t cod[LD_NT][LD_TOK][LD_P];     // codes, [tile][token][coef]
+  __shared__ __attribute__((aligned(16))) float sl[LD_NT][LD_TOK], zl[LD_NT][LD_TOK], vsum[LD_CH], bias[LD_CH];
   const int s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
   const int d = a.d, ng = d / LG;
   const int ch0 = blockIdx.y * LD_CH;
-  const int64_t tok0 = (int64_t)blockIdx.x * LD_TOK;
+  const int64_t tok0 = (int64_t)blockIdx.x * (LD_TOK * LD_NT);
   const int64_t sbase = (int64_t)s * a.t_cap * a.W;
   const float* Vs = a.basis + (int64_t)s * d * d;
   const uint8_t* bits_s = a.bits + (int64_t)s * ng;
@@ -309,30 +314,31 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
   if (!k0.ok || k0.used > a.W) return;  // width table inconsistent with the record: write nothing
   const int n_kept = k0.n_kept;
 
-  // per-thread shares of a slot's staging: basis row (channel tid >> 2) coefficients
-  // 16 (tid & 3) .. + 15; codes of tokens u_r = (tid + 512 r) & 127, coefficients
-  // 8 k8_r .. + 7 with k8_r = (tid + 512 r) >> 7 (uniform in a wavefront)
-  const int vc = tid >> 2, vq = tid & 3;
-  int64_t tbase[2];
+  // per-thread shares of a slot's staging: basis row (channel tid >> 3) coefficients
+  // 8 (tid & 7) .. + 7; piece r: token u_r = (tid + 512 r) & 127 of tile (tid + 512 r) >> 10,
+  // coefficients 8 k8_r .. + 7 with k8_r = ((tid + 512 r) >> 7) & 7 (uniform in a wavefront)
+  const int vc = tid >> 3, vq = tid & 7;
+  int64_t tbase[LD_R];
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int u = (tid + 512 * r) & (LD_TOK - 1);
-    tbase[r] = rec_word(sbase, a.t0 + (tok0 + u < a.n ? tok0 + u : a.n - 1), a.W, 0);
+  for (int r = 0; r < LD_R; ++r) {
+    const int e = tid + 512 * r;
+    const int64_t i = tok0 + (int64_t)(e >> 10) * LD_TOK + (e & (LD_TOK - 1));
+    tbase[r] = rec_word(sbase, a.t0 + (i < a.n ? i : a.n - 1), a.W, 0);
   }
-  float vpre[16], upre[16];
-  uint32_t wpre[2][3], mpre[2];
+  float vpre[8], upre[8];
+  uint32_t wpre[LD_R][3], mpre[LD_R];
   auto prefetch = [&](const LayerSlot& ks, int slot) {
-    const float* vr = Vs + (int64_t)(ch0 + vc) * d + LG * ks.grp + 16 * vq;
+    const float* vr = Vs + (int64_t)(ch0 + vc) * d + LG * ks.grp + 8 * vq;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) vpre[i] = vr[i];
+    for (int i = 0; i < 8; ++i) vpre[i] = vr[i];
     if (a.lscale) {
-      const float* fr = a.lscale + (int64_t)s * d + LG * ks.grp + 16 * vq;
+      const float* fr = a.lscale + (int64_t)s * d + LG * ks.grp + 8 * vq;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) upre[i] = fr[i];
+      for (int i = 0; i < 8; ++i) upre[i] = fr[i];
     }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int k8 = (tid + 512 * r) >> 7;
+    for (int r = 0; r < LD_R; ++r) {
+      const int k8 = ((tid + 512 * r) >> 7) & 7;
       const int P = 8 * k8 * ks.b, w0 = P >> 5, wl = (P + 8 * ks.b - 1) >> 5;  // payload words extract8 reads
 #pragma unroll
       for (int i = 0; i < 3; ++i) wpre[r][i] = (w0 + i <= wl) ? a.packed[tbase[r] + (int64_t)(ks.pay + w0 + i) * TILE] : 0u;
@@ -340,17 +346,17 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
     }
   };
 
-  // bias = m V^T over all d coefficients: wavefront w takes channels 16w .. 16w + 15,
+  // bias = m V^T over all d coefficients: wavefront w takes channels 8w .. 8w + 7,
   // each row read by the whole wavefront (16 values per lane), then a wavefront sum
   {
     const float* mr = a.mean + (int64_t)s * d;
     float mv[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) mv[i] = (64 * i + lane < d) ? mr[64 * i + lane] : 0.0f;
-    float part[16];
+    float part[8];
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const float* vr = Vs + (int64_t)(ch0 + 16 * wave + c) * d;
+    for (int c = 0; c < 8; ++c) {
+      const float* vr = Vs + (int64_t)(ch0 + 8 * wave + c) * d;
       float acc = 0.0f;
 #pragma unroll
       for (int i = 0; i < 16; ++i)
@@ -358,59 +364,58 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
       part[c] = acc;
     }
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
+    for (int c = 0; c < 8; ++c) {
       float v = part[c];
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-      if (lane == c) bias[16 * wave + c] = v;
+      if (lane == c) bias[8 * wave + c] = v;
     }
   }
 
-  // wavefront -> channel block cb (32 channels), token blocks 2 tp, 2 tp + 1 (32 tokens each)
-  const int cb = wave & 3, tp = wave >> 2;
+  // wavefront -> channel block cb (32 channels), tile tl, token blocks 2 tp, 2 tp + 1
+  // (32 tokens each) of that tile
+  const int cb = wave & 1, tl = (wave >> 1) >> 1, tp = (wave >> 1) & 1;
   f32x16 out[2] = {f32x16{}, f32x16{}};
   LayerSlot ks = k0;
   if (n_kept > 0) prefetch(ks, 0);
   for (int slot = 0; slot < n_kept; ++slot) {
     // stage the prefetched slot: codes as bf16 and metadata, basis parts and sums
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int e = tid + 512 * r, u = e & (LD_TOK - 1), k8 = e >> 7;
+    for (int r = 0; r < LD_R; ++r) {
+      const int e = tid + 512 * r, u = e & (LD_TOK - 1), k8 = (e >> 7) & 7, t2 = e >> 10;
       const int w0 = (8 * k8 * ks.b) >> 5;
       with_bits(ks.b, [&](auto bc) {
         constexpr int B = decltype(bc)::value;
         uint32_t cd[8];
         extract8<B>([&](int i) { return wpre[r][i - w0]; }, 8 * k8, cd);
-        *reinterpret_cast<u32x4*>(&cod[u][8 * k8]) =
+        *reinterpret_cast<u32x4*>(&cod[t2][u][8 * k8]) =
             u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]), int_to_bf16_pair(cd[4], cd[5]),
                   int_to_bf16_pair(cd[6], cd[7])};
       });
       if (k8 == 0) {
-        sl[u] = h2f(mpre[r]);
-        zl[u] = h2f(mpre[r] >> 16);
+        sl[t2][u] = h2f(mpre[r]);
+        zl[t2][u] = h2f(mpre[r] >> 16);
       }
     }
     {
       if (a.lscale) {  // square-root split: c_hat_j / f_j, folded into the basis columns
 #pragma unroll
-        for (int i = 0; i < 16; ++i) vpre[i] = vpre[i] * (1.0f / upre[i]);
+        for (int i = 0; i < 8; ++i) vpre[i] = vpre[i] * (1.0f / upre[i]);
       }
       float sum = 0.0f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sum += vpre[i];
+      for (int i = 0; i < 8; ++i) sum += vpre[i];
       sum += __shfl_xor(sum, 1);
       sum += __shfl_xor(sum, 2);
+      sum += __shfl_xor(sum, 4);
       if (vq == 0) vsum[vc] = sum;
+      uint32_t p0[8], p1[8], p2[8];
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        uint32_t p0[8], p1[8], p2[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) split3(vpre[8 * half + i], p0[i], p1[i], p2[i]);
-        const int j = 16 * vq + 8 * half;
-        *reinterpret_cast<u32x4*>(&vsl[0][vc][j]) = u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])};
-        *reinterpret_cast<u32x4*>(&vsl[1][vc][j]) = u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])};
-        *reinterpret_cast<u32x4*>(&vsl[2][vc][j]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
-      }
+      for (int i = 0; i < 8; ++i) split3(vpre[i], p0[i], p1[i], p2[i]);
+      const int j = 8 * vq;
+      *reinterpret_cast<u32x4*>(&vsl[0][vc][j]) = u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])};
+      *reinterpret_cast<u32x4*>(&vsl[1][vc][j]) = u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])};
+      *reinterpret_cast<u32x4*>(&vsl[2][vc][j]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
     }
     __syncthreads();
     if (slot + 1 < n_kept) {
@@ -421,8 +426,8 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
     f32x16 g[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const bf16x8 b0 = as_bf16x8(*reinterpret_cast<const u32x4*>(&cod[64 * tp + col][16 * k + 8 * h]));
-      const bf16x8 b1 = as_bf16x8(*reinterpret_cast<const u32x4*>(&cod[64 * tp + 32 + col][16 * k + 8 * h]));
+      const bf16x8 b0 = as_bf16x8(*reinterpret_cast<const u32x4*>(&cod[tl][64 * tp + col][16 * k + 8 * h]));
+      const bf16x8 b1 = as_bf16x8(*reinterpret_cast<const u32x4*>(&cod[tl][64 * tp + 32 + col][16 * k + 8 * h]));
 #pragma unroll
       for (int p = 0; p < 3; ++p) {
         const bf16x8 av = as_bf16x8(*reinterpret_cast<const u32x4*>(&vsl[p][32 * cb + col][16 * k + 8 * h]));
@@ -434,7 +439,7 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
 #pragma unroll
     for (int tb = 0; tb < 2; ++tb) {
       const int u = 64 * tp + 32 * tb + col;
-      const float st = sl[u], zt = zl[u];
+      const float st = sl[tl][u], zt = zl[tl][u];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const f32x4 vs4 = *reinterpret_cast<const f32x4*>(&vsum[32 * cb + 4 * h + 8 * q]);
@@ -447,7 +452,7 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
   if (n_kept == 0) __syncthreads();  // bias visible
 #pragma unroll
   for (int tb = 0; tb < 2; ++tb) {
-    const int64_t i = tok0 + 64 * tp + 32 * tb + col;
+    const int64_t i = tok0 + (int64_t)tl * LD_TOK + 64 * tp + 32 * tb + col;
     if (i < a.n) {
       float* o = a.out + ((int64_t)s * a.n + i) * d + ch0 + 32 * cb + 4 * h;
 #pragma unroll
@@ -503,7 +508,7 @@ hipError_t launch_layer_encode(const LayerEncodeArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_layer_decode(const LayerDecodeArgs& a, hipStream_t st) {
-  const dim3 grid((unsigned)((a.n + LD_TOK - 1) / LD_TOK), a.d / LD_CH, a.n_streams);
+  const dim3 grid((unsigned)((a.n + LD_TOK * LD_NT - 1) / (LD_TOK * LD_NT)), a.d / LD_CH, a.n_streams);
   hipLaunchKernelGGL(layer_decode_kernel, grid, dim3(512), 0, st, a);
   return hipGetLastError();
 }
