@@ -366,8 +366,8 @@ spectra_status spectra_layer_decode_attention(const spectra_codec* ck, const spe
     return fail(SPECTRA_EINVAL, "%s: n_q_heads must be a multiple of n_kv_heads, at most 32", name);
   if (batch <= 0 || batch > 65535 || batch > ck->n_streams || batch > cv->n_streams)
     return fail(SPECTRA_EINVAL, "%s: batch must be in [1, codec streams]", name);
-  if (ck->record_words > 64 || cv->record_words > 64)
-    return fail(SPECTRA_EUNSUPPORTED, "%s: records of at most 64 words", name);
+  if (ck->record_words > 128 || cv->record_words > 128)
+    return fail(SPECTRA_EUNSUPPORTED, "%s: records of at most 128 words", name);
   if (n_tokens <= 0) return fail(SPECTRA_EINVAL, "%s: attention needs n_tokens >= 1", name);
   st = check_slots(0, n_tokens, t_capacity);
   if (st != SPECTRA_OK) return st;

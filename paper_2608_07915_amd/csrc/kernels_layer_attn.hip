@@ -30,7 +30,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8v;
 
 constexpr int LA_H = 32;     // query heads per sequence (at most)
 constexpr int LA_ROW = 68;   // words per staged record row (64 tokens + pad)
-constexpr int LA_WMAX = 64;  // record words per tensor
+constexpr int LA_WMAX = 128;  // record words per tensor
 
 // kept groups of a per-layer stream in slot order: group, width, first payload word
 __device__ __forceinline__ int layer_slots(const uint8_t* __restrict__ bits_s, int ng, int* grp, int* bw, int* pay) {
@@ -124,22 +124,29 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
 // ---------------------------------------------------------------------------
 // Scores
 // ---------------------------------------------------------------------------
+// A score workgroup takes NHB blocks of 16 query heads: both (NHB = 2), or, when the
+// latent queries of 32 heads and the record rows would not fit the LDS together
+// (d = 1024 with records of more than ~100 words), one (NHB = 1, blockIdx.z selects it).
 __host__ __device__ constexpr int la_qp(int d) { return d + 8; }  // fp16 per staged query row
-__host__ __device__ constexpr int la_off_rec(int d) { return 2 * LA_H * la_qp(d) * 2; }
+__host__ __device__ constexpr int la_off_rec(int d, int nhb) { return 2 * 16 * nhb * la_qp(d) * 2; }
 // the record rows also hold the slot halves' scores of a tile ([4][64][8] floats) once read
 __host__ __device__ constexpr int la_rec_bytes(int Wk) { return Wk * LA_ROW * 4 > 4 * 64 * 8 * 4 ? Wk * LA_ROW * 4 : 4 * 64 * 8 * 4; }
-__host__ __device__ constexpr int la_off_qs(int d, int Wk) { return la_off_rec(d) + la_rec_bytes(Wk); }
-__host__ __device__ constexpr int la_scores_lds(int d, int Wk) { return la_off_qs(d, Wk) + LA_H * 16 * 4 + 4 * LA_H * 2 * 4; }
+__host__ __device__ constexpr int la_off_qs(int d, int Wk, int nhb) { return la_off_rec(d, nhb) + la_rec_bytes(Wk); }
+__host__ __device__ constexpr int la_scores_lds(int d, int Wk, int nhb) {
+  return la_off_qs(d, Wk, nhb) + LA_H * 16 * 4 + 4 * LA_H * 2 * 4;
+}
 
+template <int NHB>
 __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lsm[];
   const int d = a.d, ng = d / 64, QP = la_qp(d), Wk = a.Wk;
-  uint16_t* qa = reinterpret_cast<uint16_t*>(lsm);                       // [2][LA_H][QP]
-  uint32_t* rec = reinterpret_cast<uint32_t*>(lsm + la_off_rec(d));      // [Wk][LA_ROW]
-  float* qs = reinterpret_cast<float*>(lsm + la_off_qs(d, Wk));          // [LA_H][16]
+  uint16_t* qa = reinterpret_cast<uint16_t*>(lsm);                       // [2][16 NHB][QP]
+  uint32_t* rec = reinterpret_cast<uint32_t*>(lsm + la_off_rec(d, NHB)); // [Wk][LA_ROW]
+  float* qs = reinterpret_cast<float*>(lsm + la_off_qs(d, Wk, NHB));     // [LA_H][16]
   float* red = qs + LA_H * 16;                                           // [4][LA_H][2]
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
   const int chunk = blockIdx.x, b = blockIdx.y;
+  const int hb0 = NHB == 2 ? 0 : (int)blockIdx.z;  // first head block of this workgroup
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, kg = lane >> 4, c16 = lane & 15;
   const int Hq = a.n_q_heads;
   const uint8_t* bits_s = a.bits_k + (int64_t)b * ng;
@@ -151,15 +158,16 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   // copied as written by the query pass (16-byte pieces, eight in flight per thread);
   // rows of heads past n_q_heads are zero
   {
+    // staged row = part * 16 NHB + local head; source row = part * LA_H + 16 hb0 + local head
     const uint16_t* qh = a.qh + (int64_t)b * 2 * LA_H * d;
     const int pieces = nk * 8;  // 16-byte pieces per row
-    for (int i0 = 0; i0 < (2 * LA_H * 16 * 8) / 512; i0 += 8) {
+    for (int i0 = 0; i0 < (2 * 16 * NHB * 16 * 8) / 512; i0 += 8) {
       u32x4 v[8];
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
         const int e = tid + 512 * (i0 + r), row = e >> 7, pc = e & 127;
-        const int h = row & (LA_H - 1);
-        v[r] = (h < Hq && pc < pieces) ? *reinterpret_cast<const u32x4*>(qh + (int64_t)row * d + 8 * pc)
+        const int part = row / (16 * NHB), h = 16 * hb0 + row % (16 * NHB);
+        v[r] = (h < Hq && pc < pieces) ? *reinterpret_cast<const u32x4*>(qh + (int64_t)(part * LA_H + h) * d + 8 * pc)
                                        : u32x4{0u, 0u, 0u, 0u};
       }
 #pragma unroll
@@ -207,14 +215,18 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
     __syncthreads();
     if (tt + 1 < t_end) load_tile(tt + 1);
     const int u = 16 * tb + c16;
-    f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    f32x4 S[NHB];
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb) S[hb] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int sl = sh; sl < nk; sl += 2) {
       // slot tables are uniform: scalar registers, scalar branches on the width
       const int pay = __builtin_amdgcn_readfirstlane(spay[sl]);
       const int bw = __builtin_amdgcn_readfirstlane(sbw[sl]);
       const uint32_t m = rec[sl * LA_ROW + u];
       const float st = h2f(m), zt = h2f(m >> 16);
-      f32x4 g[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+      f32x4 g[NHB];
+#pragma unroll
+      for (int hb = 0; hb < NHB; ++hb) g[hb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         f16x8v bop;
@@ -227,25 +239,25 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
         });
         const int col = sl * 64 + 32 * ks + 8 * kg;
 #pragma unroll
-        for (int hb = 0; hb < 2; ++hb) {
+        for (int hb = 0; hb < NHB; ++hb) {
           const f16x8v a0 = __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (16 * hb + c16) * QP + col));
           const f16x8v a1 =
-              __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (LA_H + 16 * hb + c16) * QP + col));
+              __builtin_bit_cast(f16x8v, *reinterpret_cast<const u32x4*>(qa + (16 * NHB + 16 * hb + c16) * QP + col));
           g[hb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bop, g[hb], 0, 0, 0);
           g[hb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bop, g[hb], 0, 0, 0);
         }
       }
-      // lane: heads 16 hb + 4 kg + j, token u
+      // lane: heads 16 (hb0 + hb) + 4 kg + j, token u
 #pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
+      for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) S[hb][j] += st * g[hb][j] + zt * qs[(16 * hb + 4 * kg + j) * 16 + sl];
+        for (int j = 0; j < 4; ++j) S[hb][j] += st * g[hb][j] + zt * qs[(16 * (hb0 + hb) + 4 * kg + j) * 16 + sl];
     }
     // the two slot halves meet in LDS (over the record rows, whose reads are done)
     __syncthreads();
     if (sh == 1) {
 #pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
+      for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) sred[(tb * 64 + lane) * 8 + 4 * hb + j] = S[hb][j];
     }
@@ -253,10 +265,10 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
     if (sh == 0) {
       const int64_t t = tt * 64 + u;
 #pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
+      for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int h = 16 * hb + 4 * kg + j;
+          const int h = 16 * (hb0 + hb) + 4 * kg + j;
           const float x = S[hb][j] + sred[(tb * 64 + lane) * 8 + 4 * hb + j];
           if (t < a.n_tokens && h < Hq) {
             a.scores[((int64_t)b * Hq + h) * a.n_tokens + t] = x;
@@ -287,14 +299,15 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   __syncthreads();
   if (c16 == 0 && sh == 0) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int h = 16 * (q >> 2) + 4 * kg + (q & 3);
+    for (int q = 0; q < 4 * NHB; ++q) {
+      const int h = 16 * (hb0 + (q >> 2)) + 4 * kg + (q & 3);
       red[(tb * LA_H + h) * 2] = mloc[q];
       red[(tb * LA_H + h) * 2 + 1] = lloc[q];
     }
   }
   __syncthreads();
-  if (tid < Hq) {
+  // this workgroup's heads only (with NHB = 1 the other block is another workgroup's)
+  if (tid < Hq && tid >= 16 * hb0 && tid < 16 * (hb0 + NHB)) {
     float m = -__builtin_inff();
     for (int q = 0; q < 4; ++q) m = __builtin_fmaxf(m, red[(q * LA_H + tid) * 2]);
     float l = 0.0f;
@@ -635,13 +648,22 @@ void layer_attention_ws_layout(LayerAttnArgs& a, float* ws) {
   a.part = a.stats + r64(B * a.n_chunks * H * 2);
 }
 
-size_t layer_scores_lds_bytes(int32_t d, int32_t Wk) { return (size_t)la_scores_lds(d, Wk); }
+// the score pass with one head block per workgroup (the smaller LDS footprint)
+size_t layer_scores_lds_bytes(int32_t d, int32_t Wk) { return (size_t)la_scores_lds(d, Wk, 1); }
 
 hipError_t launch_layer_attention(const LayerAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(layer_qprep_kernel, dim3(a.n_q_heads, a.batch, (a.d + 255) / 256), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layer_scores_kernel, dim3(a.n_chunks, a.batch), dim3(512), la_scores_lds(a.d, a.Wk), st, a);
+  int dev = 0, lds_max = 0;
+  e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return e;
+  if ((size_t)la_scores_lds(a.d, a.Wk, 2) <= (size_t)lds_max)
+    hipLaunchKernelGGL(layer_scores_kernel<2>, dim3(a.n_chunks, a.batch), dim3(512), la_scores_lds(a.d, a.Wk, 2), st, a);
+  else
+    hipLaunchKernelGGL(layer_scores_kernel<1>, dim3(a.n_chunks, a.batch, 2), dim3(512), la_scores_lds(a.d, a.Wk, 1), st,
+                       a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(layer_stats_kernel, dim3(a.n_q_heads, a.batch), dim3(256), 0, st, a);

@@ -189,7 +189,10 @@ def _oracle_layer_attention(q64, kh, vh, n_kv):
 
 
 @pytest.mark.parametrize("name,T,ratio,batch", [("qwen_layer_8x", 1000, 8.0, 1), ("llama_layer_4x", 777, 8.0, 2),
-                                                 ("qwen_layer_8x", 300, 16.0, 2), ("qwen_layer_8x", 2500, 8.0, 1)])
+                                                 ("qwen_layer_8x", 300, 16.0, 2), ("qwen_layer_8x", 2500, 8.0, 1),
+                                                 # 1024-wide latent at 4x: 128-word records, the score pass
+                                                 # split over the two blocks of 16 query heads
+                                                 ("llama_layer_4x", 600, 4.0, 1)])
 def test_layer_decode_attention(name, T, ratio, batch):
     # Mode B over the per-layer latent against Mode A over the oracle's reconstruction of
     # the same bytes (arithmetic only) and of the oracle's own encoding
