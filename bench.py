@@ -45,17 +45,17 @@ DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "enco
                        "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "25e8171641d32dcbbb71939be452dd334161433e5f955c888b35be1d30f1abd1": {
-        "fetch_bytes": 74476544, "write_bytes": 1674240, "mfma_busy": 0.095,
-        "per_kernel": {"attn_kernel<1,8,8,true>": [70701261, 1657856], "combine_kernel": [3775283, 16384]}},
+    "8bf2b03fa8b47d7252d6306a613e5ea55ef3e0a467020b31bc4c5509e0ec6b7f": {
+        "fetch_bytes": 74479173, "write_bytes": 1674244, "mfma_busy": 0.096,
+        "per_kernel": {"attn_kernel<1,8,8,true>": [70702812, 1657860], "combine_kernel": [3776361, 16384]}},
 }
 # The same passes over the bulk encode of one codec (256 streams x 131072 tokens):
 # HBM bytes per call and the matrix cores' busy fraction (SQ_VALU_MFMA_BUSY_CYCLES
 # over GRBM_GUI_ACTIVE x 1024 SIMDs), keyed by sha256 over ENCODE_SOURCES.
 ENCODE_SOURCES = ("kernels_codec.hip", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
 MEASURED_ENCODE = {
-    "3529804415461ff5fdb2dba172de982da0167d2cb1a04d999629913f1fcdc58e": {
-        "fetch_bytes": 8665338880, "write_bytes": 1073741824, "mfma_busy": 0.348},
+    "2a3173d013abe8ad3b5998c2041799f2dd866f0c3a275d5e4857b5fe7370bc2d": {
+        "fetch_bytes": 8665505728, "write_bytes": 1073741824, "mfma_busy": 0.348},
 }
 
 

@@ -31,6 +31,9 @@ typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8v;
 constexpr int LA_H = 32;     // query heads per sequence (at most)
 constexpr int LA_ROW = 68;   // words per staged record row (64 tokens + pad)
 constexpr int LA_WMAX = 128;  // record words per tensor
+// record words per tile staged through registers: the kernels are instantiated for
+// records of at most 64 words and of at most LA_WMAX words
+__host__ __device__ constexpr int la_prefetch_words(int W) { return W <= 64 ? 64 : LA_WMAX; }
 
 // kept groups of a per-layer stream in slot order: group, width, first payload word
 __device__ __forceinline__ int layer_slots(const uint8_t* __restrict__ bits_s, int ng, int* grp, int* bw, int* pay) {
@@ -136,7 +139,7 @@ __host__ __device__ constexpr int la_scores_lds(int d, int Wk, int nhb) {
   return la_off_qs(d, Wk, nhb) + LA_H * 16 * 4 + 4 * LA_H * 2 * 4;
 }
 
-template <int NHB>
+template <int NHB, int WP>
 __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lsm[];
   const int d = a.d, ng = d / 64, QP = la_qp(d), Wk = a.Wk;
@@ -194,7 +197,7 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
     mloc[j] = -__builtin_inff();
     lloc[j] = 0.0f;
   }
-  constexpr int PF = 64 * LA_WMAX / 512;  // record words per thread and tile
+  constexpr int PF = 64 * WP / 512;  // record words per thread and tile
   uint32_t pre[PF];
   auto load_tile = [&](int64_t tt) {
 #pragma unroll
@@ -366,8 +369,9 @@ __global__ __launch_bounds__(256) void layer_stats_kernel(LayerAttnArgs a) {
 // Values: one workgroup per (token chunk, block of 16 query heads, sequence); wavefront w
 // takes kept value slots w and w + 8
 // ---------------------------------------------------------------------------
+template <int WP>
 __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t rec[LA_WMAX * LA_ROW];
+  __shared__ __attribute__((aligned(16))) uint32_t rec[WP * LA_ROW];
   __shared__ __attribute__((aligned(16))) float pl[16 * LA_ROW];
   __shared__ float mh[LA_H];
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
@@ -396,7 +400,7 @@ __global__ __launch_bounds__(512) void layer_values_kernel(LayerAttnArgs a) {
   const int64_t t_begin = (int64_t)chunk * a.v_tiles_per_chunk;
   const int64_t t_end = t_begin + a.v_tiles_per_chunk < n_tiles ? t_begin + a.v_tiles_per_chunk : n_tiles;
   const uint32_t* vp = a.packed_v + (int64_t)b * a.t_cap * Wv;
-  constexpr int PF = 64 * LA_WMAX / 512;       // record words per thread and tile
+  constexpr int PF = 64 * WP / 512;            // record words per thread and tile
   constexpr int PS = 16 * 64 / 512;            // scores per thread and tile
   uint32_t pre[PF];
   float spre[PS];
@@ -659,17 +663,31 @@ hipError_t launch_layer_attention(const LayerAttnArgs& a, hipStream_t st) {
   e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return e;
-  if ((size_t)la_scores_lds(a.d, a.Wk, 2) <= (size_t)lds_max)
-    hipLaunchKernelGGL(layer_scores_kernel<2>, dim3(a.n_chunks, a.batch), dim3(512), la_scores_lds(a.d, a.Wk, 2), st, a);
-  else
-    hipLaunchKernelGGL(layer_scores_kernel<1>, dim3(a.n_chunks, a.batch, 2), dim3(512), la_scores_lds(a.d, a.Wk, 1), st,
-                       a);
+  const bool k_wide = la_prefetch_words(a.Wk) > 64, v_wide = la_prefetch_words(a.Wv) > 64;
+  if ((size_t)la_scores_lds(a.d, a.Wk, 2) <= (size_t)lds_max) {
+    if (k_wide)
+      hipLaunchKernelGGL((layer_scores_kernel<2, LA_WMAX>), dim3(a.n_chunks, a.batch), dim3(512),
+                         la_scores_lds(a.d, a.Wk, 2), st, a);
+    else
+      hipLaunchKernelGGL((layer_scores_kernel<2, 64>), dim3(a.n_chunks, a.batch), dim3(512), la_scores_lds(a.d, a.Wk, 2),
+                         st, a);
+  } else {
+    if (k_wide)
+      hipLaunchKernelGGL((layer_scores_kernel<1, LA_WMAX>), dim3(a.n_chunks, a.batch, 2), dim3(512),
+                         la_scores_lds(a.d, a.Wk, 1), st, a);
+    else
+      hipLaunchKernelGGL((layer_scores_kernel<1, 64>), dim3(a.n_chunks, a.batch, 2), dim3(512),
+                         la_scores_lds(a.d, a.Wk, 1), st, a);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(layer_stats_kernel, dim3(a.n_q_heads, a.batch), dim3(256), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(layer_values_kernel, dim3(a.nv_chunks, 2, a.batch), dim3(512), 0, st, a);
+  if (v_wide)
+    hipLaunchKernelGGL(layer_values_kernel<LA_WMAX>, dim3(a.nv_chunks, 2, a.batch), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL(layer_values_kernel<64>, dim3(a.nv_chunks, 2, a.batch), dim3(512), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(layer_combine_kernel, dim3(a.n_q_heads, a.batch, a.d / 64), dim3(256), 0, st, a);
