@@ -157,15 +157,29 @@ __global__ __launch_bounds__(256, 2) void encode_bf16_kernel(EncodeArgs a) {
   // one global_load_lds fills 1 KB: rows 4m..4m+3 of the super-tile; lane i
   // brings chunk (i % 16) ^ (row % 16) of row 4m + i / 16. Wave w issues m = 8w..8w+7.
   const int lrow = lane >> 4;
+  // A super-tile whose 128 rows all hold the call's tokens: uniform row base plus a
+  // per-lane offset that does not change between super-tiles (row 32 wave + 4 i + lrow
+  // has row % 16 = 4 (i % 4) + lrow), so the copies take no per-copy vector arithmetic.
+  const int64_t ts2 = a.token_stride * 2;  // bytes from one token row to the next
+  uint32_t voff[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) voff[k] = (uint32_t)(lrow * ts2) + ((uint32_t)((lane & 15) ^ (4 * k + lrow)) << 4);
   auto stage = [&](int64_t st, int b) {
     const int64_t slot0 = (first_tile << 6) + st * EST;
+    if (slot0 >= a.t0 && slot0 + EST <= a.t0 + a.n) {
+      const char* rb = xb + (slot0 - a.t0 + 32 * wave) * ts2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_global_load_lds(rb + 4 * i * ts2 + voff[i & 3], &xs[b][(8 * wave + i) * 1024], 16, 0, 0);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int m = 8 * wave + i, row = 4 * m + lrow;
       const int chunk = (lane & 15) ^ (row & 15);
       int64_t t = slot0 + row - a.t0;
       t = t < 0 ? 0 : (t >= a.n ? a.n - 1 : t);
-      __builtin_amdgcn_global_load_lds(xb + t * a.token_stride * 2 + chunk * 16, &xs[b][m * 1024], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(xb + t * ts2 + chunk * 16, &xs[b][m * 1024], 16, 0, 0);
     }
   };
   int64_t st = blockIdx.x;
