@@ -140,6 +140,20 @@ __global__ __launch_bounds__(256) void layer_moments_kernel(LayerGramArgs g) {
 // ---------------------------------------------------------------------------
 // Encode
 // ---------------------------------------------------------------------------
+// Workgroups of a one-dimensional grid over (token range, block) are dispatched to the
+// eight XCDs in turn (workgroup i to XCD i mod 8). Numbering them i = 8 (nb r + blk) + x
+// with token range 8 r + x puts every block of a range on the same XCD, close together
+// in time, so that XCD's L2 serves the range's rows to all of them instead of every XCD
+// fetching them from HBM. Ranges past the last one (the grid is rounded up to whole
+// groups of eight) get range = -1.
+__host__ __device__ constexpr unsigned xcd_major_grid(int n_ranges, int nb) { return 8u * (unsigned)nb * (unsigned)((n_ranges + 7) / 8); }
+__device__ __forceinline__ void xcd_major_block(int n_ranges, int nb, int& range, int& blk) {
+  const int i = (int)blockIdx.x, x = i & 7, j = i >> 3;
+  blk = j % nb;
+  range = 8 * (j / nb) + x;
+  if (range >= n_ranges) range = -1;
+}
+
 constexpr int LE_TOK = 256;       // tokens per workgroup (eight wavefronts of 32)
 constexpr int LE_KC = 64;         // basis rows per staged chunk
 constexpr int LE_KP = LE_KC + 8;  // bf16 per staged row (144-byte rows, 16-byte aligned)
@@ -154,12 +168,15 @@ __device__ __forceinline__ int le_row(int c) {
 
 __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vs[3][64][LE_KP];
-  const int s = blockIdx.z, slot = blockIdx.y;
+  const int s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
   const int d = a.d, ng = d / LG;
+  int range, slot;
+  xcd_major_block((int)((a.n + LE_TOK - 1) / LE_TOK), ng, range, slot);
+  if (range < 0) return;
   const LayerSlot ks = layer_slot(a.bits + (int64_t)s * ng, ng, slot);
   const int64_t sbase = (int64_t)s * a.t_cap * a.W;
-  const int64_t wg_tok = (int64_t)blockIdx.x * LE_TOK;
+  const int64_t wg_tok = (int64_t)range * LE_TOK;
   if (!ks.ok || ks.used > a.W) return;  // width table inconsistent with the record: write nothing
 
   // words past the used ones are zero: written by the slot-0 workgroup
@@ -305,8 +322,11 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
   const int s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
   const int d = a.d, ng = d / LG;
-  const int ch0 = blockIdx.y * LD_CH;
-  const int64_t tok0 = (int64_t)blockIdx.x * (LD_TOK * LD_NT);
+  int range, cblk;
+  xcd_major_block((int)((a.n + LD_TOK * LD_NT - 1) / (LD_TOK * LD_NT)), d / LD_CH, range, cblk);
+  if (range < 0) return;
+  const int ch0 = cblk * LD_CH;
+  const int64_t tok0 = (int64_t)range * (LD_TOK * LD_NT);
   const int64_t sbase = (int64_t)s * a.t_cap * a.W;
   const float* Vs = a.basis + (int64_t)s * d * d;
   const uint8_t* bits_s = a.bits + (int64_t)s * ng;
@@ -502,13 +522,13 @@ hipError_t launch_layer_moments(const LayerGramArgs& g, bool f32_in, hipStream_t
 }
 
 hipError_t launch_layer_encode(const LayerEncodeArgs& a, hipStream_t st) {
-  const dim3 grid((unsigned)((a.n + LE_TOK - 1) / LE_TOK), a.d / LG, a.n_streams);
+  const dim3 grid(xcd_major_grid((int)((a.n + LE_TOK - 1) / LE_TOK), a.d / LG), 1, a.n_streams);
   hipLaunchKernelGGL(layer_encode_kernel, grid, dim3(512), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_layer_decode(const LayerDecodeArgs& a, hipStream_t st) {
-  const dim3 grid((unsigned)((a.n + LD_TOK * LD_NT - 1) / (LD_TOK * LD_NT)), a.d / LD_CH, a.n_streams);
+  const dim3 grid(xcd_major_grid((int)((a.n + LD_TOK * LD_NT - 1) / (LD_TOK * LD_NT)), a.d / LD_CH), 1, a.n_streams);
   hipLaunchKernelGGL(layer_decode_kernel, grid, dim3(512), 0, st, a);
   return hipGetLastError();
 }
