@@ -134,11 +134,12 @@ __host__ __device__ constexpr size_t encode_bf16_lds_bytes(int W, bool staged) {
   return (size_t)2 * EST * 256 + (staged ? (size_t)(EST * W + 256) * 4 : 0);  // + a scratch word per lane
 }
 
-// s_waitcnt with vmcnt(n) (n < 16), expcnt and lgkmcnt not waited for
+// s_waitcnt with vmcnt(n) (n < 64: low four bits at 3:0, high two at 15:14), expcnt
+// and lgkmcnt not waited for
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
 template <bool STAGED>
@@ -339,25 +340,54 @@ __global__ __launch_bounds__(256, 2) void encode_f32_kernel(EncodeArgs a) {
 // ---------------------------------------------------------------------------
 // Decode: wave w owns output channels 32w..32w+31 for every token of a super-tile.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
-  constexpr int ST = 128;
-  __shared__ uint32_t rec[2 * 64 * 64];  // two record tiles, W <= 64 words
+__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
+  // super-tile = two 64-token record tiles; records of W <= 32 words are double-buffered
+  // (the next super-tile is copied HBM -> LDS by global_load_lds while this one is
+  // decoded), wider ones go through one buffer
+  __shared__ __attribute__((aligned(16))) uint32_t rec[2 * 64 * 64];
+  __shared__ __attribute__((aligned(16))) float vsum_s[NG][D], bias_s[D];
   const int s = blockIdx.y;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, col = lane & 31;
   const Kept K = read_kept(a.bits + (int64_t)s * NG);
   const int W = a.W;
   if (!K.ok || K.used > W) return;  // width table inconsistent with the record: write nothing
   const int64_t sbase = (int64_t)s * a.t_cap * W;
-  const int ch = 32 * wave + col;  // this lane's output channel
+  const int ch = 32 * wave + col;  // channel of this lane's basis operand row
   const float* Vs = a.basis + (int64_t)s * D * D;
 
-  // B operands: column = channel ch, K = in-group coefficients 16k + 8h + i.
+  const int64_t first_tile = a.t0 >> 6;
+  const int64_t end = a.t0 + a.n;
+  const int64_t last_tile = (end - 1) >> 6;
+  const int64_t n_st = (last_tile - first_tile + 2) / 2;
+  const bool db = W <= 32;
+  // super-tile st into buffer b: its words are contiguous in HBM (tile-major), 16 bytes
+  // per lane and copy; lanes past the super-tile's last word re-read its last piece
+  // (their LDS slots are never read)
+  auto issue = [&](int64_t st, int b) {
+    const int64_t tile0 = first_tile + 2 * st;
+    const int ntile = (tile0 + 1 <= last_tile) ? 2 : 1;
+    const int np = ntile * 16 * W;  // 16-byte pieces
+    const uint32_t* src = a.packed + sbase + tile0 * (int64_t)(64 * W);
+    uint32_t* dst = rec + b * (64 * 64);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int p0 = 256 * i + 64 * wave;
+      if (p0 < np) {
+        const int pc = p0 + lane < np ? p0 + lane : np - 1;
+        __builtin_amdgcn_global_load_lds(src + 4 * pc, dst + 4 * p0, 16, 0, 0);
+      }
+    }
+  };
+  int64_t st = blockIdx.x;
+  if (st >= n_st) return;
+  issue(st, 0);
+
+  // A operands: row = channel ch, K = in-group coefficients 16k + 8h + i.
   bf16x8 Vb[NG][2][3];
-  float vsum[NG];
 #pragma unroll
   for (int sl = 0; sl < NG; ++sl) {
-    vsum[sl] = 0.0f;
     if (sl < K.n) {
       const float* vr = Vs + (int64_t)ch * D + G * K.grp[sl];
 #pragma unroll
@@ -369,9 +399,11 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         Vb[sl][k][1] = as_bf16x8(u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])});
         Vb[sl][k][2] = as_bf16x8(u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])});
       }
-      float acc = 0.0f;
-      for (int j = 0; j < G; ++j) acc += vr[j];
-      vsum[sl] = acc;
+      if (h == 0) {
+        float acc = 0.0f;
+        for (int j = 0; j < G; ++j) acc += vr[j];
+        vsum_s[sl][ch] = acc;
+      }
     } else {
 #pragma unroll
       for (int k = 0; k < 2; ++k)
@@ -379,29 +411,29 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         for (int p = 0; p < 3; ++p) Vb[sl][k][p] = bf16x8{};
     }
   }
-  float bias = 0.0f;
-  {
+  if (h == 0) {
     const float* ms = a.mean + (int64_t)s * D;
     const float* vr = Vs + (int64_t)ch * D;
+    float bias = 0.0f;
     for (int j = 0; j < D; ++j) bias += ms[j] * vr[j];
+    bias_s[ch] = bias;
   }
+  wait_vmcnt<0>();  // this wave's copies of the first super-tile (and the operand loads) done
+  __syncthreads();  // ... every wave's; vsum and bias visible
 
-  const int64_t first_tile = a.t0 >> 6;
-  const int64_t end = a.t0 + a.n;
-  const int64_t last_tile = (end - 1) >> 6;
-  const int64_t n_st = (last_tile - first_tile + 2) / 2;
-  for (int64_t st = blockIdx.x; st < n_st; st += gridDim.x) {
+  int buf = 0;
+  for (;;) {
+    const int64_t st_next = st + gridDim.x;
+    const bool more = st_next < n_st;
+    if (db && more) issue(st_next, buf ^ 1);
     const int64_t tile0 = first_tile + 2 * st;
     const int ntile = (tile0 + 1 <= last_tile) ? 2 : 1;
-    __syncthreads();
-    for (int i = tid; i < ntile * 64 * W; i += 256) rec[i] = a.packed[sbase + tile0 * (int64_t)(64 * W) + i];
-    __syncthreads();
+    const bool full = ntile == 2 && (tile0 << 6) >= a.t0 && (tile0 << 6) + 128 <= end;
+    const uint32_t* rb = rec + buf * (64 * 64);
     for (int beta = 0; beta < 2 * ntile; ++beta) {
-      const int row = 32 * beta + col;  // token of this lane's A-operand row
-      const uint32_t* rtok = rec + (row >> 6) * 64 * W + (row & 63);
-      float out[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) out[j] = bias;
+      const int row = 32 * beta + col;  // token of this lane's B-operand column
+      const uint32_t* rtok = rb + (row >> 6) * 64 * W + (row & 63);
+      f32x16 out = {};
 #pragma unroll
       for (int sl = 0; sl < NG; ++sl) {
         if (sl < K.n) {
@@ -414,29 +446,52 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
             for (int k = 0; k < 2; ++k) {
               uint32_t cd[8];
               extract8<B>(word, 16 * k + 8 * h, cd);
-              const bf16x8 A = as_bf16x8(u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]),
+              const bf16x8 C = as_bf16x8(u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]),
                                                int_to_bf16_pair(cd[4], cd[5]), int_to_bf16_pair(cd[6], cd[7])});
-              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, Vb[sl][k][0], acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, Vb[sl][k][1], acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, Vb[sl][k][2], acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Vb[sl][k][0], C, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Vb[sl][k][1], C, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Vb[sl][k][2], C, acc, 0, 0, 0);
             }
           });
-          // acc[j]: token row 8(j/4) + 4h + j%4 of this block, channel ch
+          // acc[4q + r]: channel 32 wave + 8q + 4h + r, token row (the lane's column)
+          const uint32_t m = rtok[sl * 64];
+          const float sc = h2f(m), zc = h2f(m >> 16);
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int tr = 32 * beta + 8 * (j >> 2) + 4 * h + (j & 3);
-            const uint32_t m = rec[(tr >> 6) * 64 * W + sl * 64 + (tr & 63)];
-            out[j] += h2f(m) * acc[j] + h2f(m >> 16) * vsum[sl];
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v4 = *reinterpret_cast<const f32x4*>(&vsum_s[sl][32 * wave + 8 * q + 4 * h]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[4 * q + r] = __builtin_fmaf(sc, acc[4 * q + r], __builtin_fmaf(zc, v4[r], out[4 * q + r]));
           }
         }
       }
+      const int64_t t = (tile0 << 6) + row;
+      float* o = a.out + ((int64_t)s * a.n + (t - a.t0)) * D + 32 * wave + 4 * h;
+      if (full || (t >= a.t0 && t < end)) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int tr = 32 * beta + 8 * (j >> 2) + 4 * h + (j & 3);
-        const int64_t t = (tile0 << 6) + tr;
-        if (t >= a.t0 && t < end) a.out[((int64_t)s * a.n + (t - a.t0)) * D + ch] = out[j];
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 b4 = *reinterpret_cast<const f32x4*>(&bias_s[32 * wave + 8 * q + 4 * h]);
+          *reinterpret_cast<f32x4*>(o + 8 * q) =
+              f32x4{out[4 * q] + b4[0], out[4 * q + 1] + b4[1], out[4 * q + 2] + b4[2], out[4 * q + 3] + b4[3]};
+        }
       }
     }
+    if (!more) break;
+    if (db) {
+      // this wave's copies of the next super-tile were issued before the 16 stores of a
+      // full super-tile (vector memory operations complete in issue order)
+      if (full)
+        wait_vmcnt<16>();
+      else
+        wait_vmcnt<0>();
+      __syncthreads();  // every wave's copies landed; every wave is done with rec[buf]
+      buf ^= 1;
+    } else {
+      __syncthreads();  // every wave is done with the buffer
+      issue(st_next, 0);
+      wait_vmcnt<0>();
+      __syncthreads();
+    }
+    st = st_next;
   }
 }
 
