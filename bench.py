@@ -54,8 +54,8 @@ MEASURED_TRAFFIC = {
 # over GRBM_GUI_ACTIVE x 1024 SIMDs), keyed by sha256 over ENCODE_SOURCES.
 ENCODE_SOURCES = ("kernels_codec.hip", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
 MEASURED_ENCODE = {
-    "2a3173d013abe8ad3b5998c2041799f2dd866f0c3a275d5e4857b5fe7370bc2d": {
-        "fetch_bytes": 8665505728, "write_bytes": 1073741824, "mfma_busy": 0.348},
+    "712e6e83e451649406c652c5af098a0a3196dc738a3b76e31f7081c8e43b506e": {
+        "fetch_bytes": 8666146688, "write_bytes": 1073741824, "mfma_busy": 0.359},
 }
 
 
@@ -272,6 +272,31 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
     torch.cuda.synchronize()
     latt_ms = min(e[0].elapsed_time(e[1]) for e in latt_ev[1:])
     Wl = cl.record_words
+    # the same attention over per-layer caches at 4x (128-word records)
+    pl4 = S.Params(head_dim=dl, group_size=64, ratio=4.0)
+    c4 = []
+    for tensor in (0, 1):
+        x4 = synth.device_layer_stream(w, 0, 0, tensor, n_rec, dev)
+        cc = S.Codec(pl4, 1)
+        S.spectra_fit_basis(cc, x4[:, :8192])
+        pp = cc.empty_packed(t_cap)
+        S.spectra_encode(cc, x4, 0, pp, t_cap)
+        del x4
+        c4.append((cc, pp))
+    lws4 = torch.empty(S.spectra_layer_attention_workspace_bytes(c4[0][0], 1, Hq, n_rec), dtype=torch.uint8, device=dev)
+    latt4_ev = []
+    for _ in range(4):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        S.spectra_layer_decode_attention(c4[0][0], c4[1][0], c4[0][1], c4[1][1], t_cap, n_rec, lq, H, out=lout,
+                                         workspace=lws4)
+        e[1].record()
+        latt4_ev.append(e)
+    torch.cuda.synchronize()
+    latt4_ms = min(e[0].elapsed_time(e[1]) for e in latt4_ev[1:])
+    W4 = c4[0][0].record_words
+    latt4_bytes = 2 * n_rec * W4 * 4 + 2 * (dl * dl * 4 + dl * 4) + Hq * d * 2 + Hq * d * 4
+    del c4, lws4
     lenc_bytes = n_rec * dl * 2 + n_rec * Wl * 4 + dl * dl * 4 + dl * 4
     ldec_bytes = n_rec * Wl * 4 + n_rec * dl * 4 + dl * dl * 4 + dl * 4
     kept = int((cl.bits[0] > 0).sum().item())
@@ -284,9 +309,13 @@ def outside_step(S, torch, w, layer_ck, layer_cv, layer_pk, layer_pv, t_cap, n_r
                          "decode_ms": round(ldec_ms, 4), "decode_GBps": round(ldec_bytes / (ldec_ms * 1e-3) / 1e9, 1),
                          "attention_us": round(latt_ms * 1e3, 1),
                          "attention_GBps": round(latt_bytes / (latt_ms * 1e-3) / 1e9, 1),
+                         "attention_4x_record_words": W4,
+                         "attention_4x_us": round(latt4_ms * 1e3, 1),
+                         "attention_4x_GBps": round(latt4_bytes / (latt4_ms * 1e-3) / 1e9, 1),
                          "what": "per-layer cross-head latent: spectra_encode and spectra_decode of one layer's keys "
                                  "as one d_kv stream, and spectra_layer_decode_attention of the 32 query heads "
-                                 "over that layer's keys and values, outside the step"},
+                                 "over that layer's keys and values (8x, and attention_4x_* over caches at 4x), "
+                                 "outside the step"},
         "mode_a_rope_attention": {"us_per_layer_call": round(rope_ms * 1e3, 1),
                                   "GBps": round(rope_bytes / (rope_ms * 1e-3) / 1e9, 1),
                                   "what": "spectra_decode_attention_rope (keys reconstructed and rotated) over one "
