@@ -158,6 +158,27 @@ def test_encode_decode_parity(name, tensor, T, ratio):
             assert rel_l2(dec_gpu[s], xs) <= 1e-2
 
 
+@pytest.mark.parametrize("ratio", [12.0, 8.0, 4.0, 3.0, 16.0 / 9.0])
+def test_decode_many_super_tiles_per_workgroup(ratio):
+    """Mode A decode of 32 streams over a window whose first and last 128-token
+    super-tiles are partial: the decode grid gives each stream 16 workgroups, so some
+    walk two super-tiles (records of up to 32 words double-buffered in LDS, wider ones
+    through one buffer). P6 on identical bytes against the oracle for every stream."""
+    w = synth.WORKLOADS["llama_batch16_12x"]
+    T, t0, n = 2500, 37, 2400
+    x = _streams(w, 0, T, n_streams=32)
+    p = O.Params(ratio=ratio)
+    t_cap = (T + 63) // 64 * 64
+    codec, packed = fit_and_encode(to_device(x, w.dtype), p, t_cap)
+    W = O.record_words(p)
+    dec = S.spectra_decode(codec, packed, t_cap, t0, n).cpu().numpy()
+    assert dec.shape == (32, n, 128)
+    for s in range(32):
+        basis, mean, bits = codec_state(codec, s)
+        ref = O.decode(records_of(packed, s, t0, n, t_cap, W), basis, mean, bits, p)
+        assert rel_l2(dec[s], ref) <= 1e-6, (ratio, s)
+
+
 def test_encode_in_pieces_and_appends_equal_one_shot():
     """Slots outside [t0, t0+n) are untouched: pieces, ragged offsets and single-token
     appends give the same bytes as one call; encoding twice is bit-identical."""
