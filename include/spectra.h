@@ -204,7 +204,7 @@ spectra_status spectra_decode(const spectra_codec* c, const uint32_t* packed, in
  * constant q~_h . m_K cancels), softmax, value sums over the kept value coefficients,
  * then (a / sum + m_V) V_V[kv rows]^T. With the square-root split (lscale set) the
  * cached coordinates are c_j f_j: q~_j is divided by the keys' f_j and the value sums
- * by the values' f_j before m_V is added. n_q_heads <= 32, records of at most 64 words.
+ * by the values' f_j before m_V is added. n_q_heads <= 32, records of at most 128 words.
  * softmax_scale <= 0 selects 1/sqrt(128). Workspace: device,
  * spectra_layer_attention_workspace_bytes bytes, 256-byte aligned. Asynchronous.
  * ------------------------------------------------------------------------- */
