@@ -419,7 +419,7 @@ size_t spectra_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32
   int32_t tpc;
   // one workspace serves both attention entry points (latent, and with rotary embeddings)
   const int32_t nch = std::max(attention_chunks(batch, n_kv_heads, n_tokens, &tpc),
-                               rope_attention_chunks(batch, n_kv_heads, n_tokens, &tpc));
+                               rope_attention_chunks(batch, n_kv_heads, n_tokens, &tpc, 2));
   return attention_partial_floats(batch, n_q_heads, nch) * sizeof(float);
 }
 
@@ -512,8 +512,7 @@ spectra_status spectra_decode_attention_rope(const spectra_codec* ck, const spec
   if (q_position < 0) return fail(SPECTRA_EINVAL, "decode_attention_rope: q_position negative");
   a.inv_freq = inv_freq;
   a.q_pos = q_position;
-  a.n_chunks = rope_attention_chunks(batch, n_kv_heads, n_tokens, &a.tiles_per_chunk);
-  hipError_t e = launch_attention_rope(a, (hipStream_t)stream);
+  hipError_t e = launch_attention_rope(a, (hipStream_t)stream);  // sets the chunk split of the kernel it runs
   return e == hipSuccess ? SPECTRA_OK : hip_fail(e, "attention (rope) launch");
 }
 

@@ -114,7 +114,8 @@ hipError_t launch_combine(const spectra_dev::AttnArgs& a, hipStream_t st);
 // Attention with rotary position embeddings (Mode A keys, latent values), then the
 // combine; chunk split from rope_attention_chunks.
 hipError_t launch_attention_rope(const spectra_dev::AttnArgs& a, hipStream_t st);
-int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);
+int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk,
+                              int32_t per_cu);
 // Workspace layout of decode_attention (bytes), shared by the host API and launcher.
 size_t attention_partial_floats(int32_t batch, int32_t n_q_heads, int32_t n_chunks);
 int32_t attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk);

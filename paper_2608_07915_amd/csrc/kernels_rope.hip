@@ -24,6 +24,7 @@
 //      wavefront rotates the queries for the next tile.
 #include "attn_common.hpp"
 #include "device_common.hpp"
+#include "encode_dev.hpp"
 #include "kernels.hpp"
 
 namespace spectra_dev {
@@ -485,38 +486,470 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Four-wavefront form (at most four query heads per KV head, records of at most 16
+// words): two workgroups per CU, two workgroup barriers per tile, the reconstructed
+// keys never leave the registers.
+//   1. wavefront w reconstructs dimensions 16w..16w+15 and 64+16w..64+16w+15 of the
+//      tile's 64 tokens on v_mfma_f32_32x32x16_bf16 (rows m and m + 16 of its 32-row
+//      output are the pair (16w + m, 80w... i.e. i and i + 64), so a lane holds both
+//      members of eight pairs of one token), rotates them by the token's in-tile
+//      offset r (a 64 x 64 table of cos and sin of r w_i), dots them with the tile's
+//      rotated queries and leaves its partial scores in LDS;
+//      it also stages the next tile's key words and this tile's value words;
+//   2. online softmax (lane = token) in every wavefront; wavefront w adds the
+//      softmax-weighted codes of kept value slot w over the whole tile; the next tile's
+//      key codes are unpacked and its queries rotated.
+// ---------------------------------------------------------------------------
+constexpr int R4W = 16;  // record words per tensor
+constexpr int R4T = 256;  // threads
+__host__ __device__ constexpr int r4_off_reck() { return 0; }                                   // [R4W][TROW] u32
+__host__ __device__ constexpr int r4_off_recv() { return R4W * TROW * 4; }                      // [R4W][TROW] u32
+__host__ __device__ constexpr int r4_off_codes() { return 2 * R4W * TROW * 4; }                 // [64][RCP] bf16
+__host__ __device__ constexpr int r4_off_kmeta() { return r4_off_codes() + RTT * RCP * 2; }     // [NG][64] (s, z)
+constexpr int R4TP = 65;  // (cos, sin) pairs per table row: 64 frequencies + pad, rows of distinct tokens on distinct banks
+__host__ __device__ constexpr int r4_off_tab() { return r4_off_kmeta() + NG * RTT * 8; }       // [64][R4TP] (cos, sin)
+__host__ __device__ constexpr int r4_off_vsum() { return r4_off_tab() + 64 * R4TP * 8; }       // [NG + 1][128]: sums, m V^T
+__host__ __device__ constexpr int r4_off_qs() { return r4_off_vsum() + (NG + 1) * D * 4; }     // [4][128]
+__host__ __device__ constexpr int r4_off_qpp() { return r4_off_qs() + 4 * D * 4; }             // [64][4][2]
+__host__ __device__ constexpr int r4_off_red() { return r4_off_qpp() + 64 * 4 * 2 * 4; }       // [4][4][64]
+__host__ __device__ constexpr int r4_off_wt() { return r4_off_red() + 4 * 4 * 64 * 4; }        // [4][8][WROW] bf16
+__host__ __device__ constexpr int r4_lds_bytes() { return r4_off_wt() + 4 * 8 * WROW * 2; }
+static_assert(r4_off_codes() % 16 == 0 && r4_off_kmeta() % 16 == 0 && r4_off_tab() % 16 == 0, "16-byte reads");
+static_assert(r4_off_vsum() % 16 == 0 && r4_off_qpp() % 16 == 0 && r4_off_wt() % 16 == 0, "16-byte reads");
+static_assert(2 * r4_lds_bytes() <= 160 * 1024, "two workgroups per CU");
+static_assert(8 * AROW * 4 <= RTT * RCP * 2, "the value sums of the merge fit the code rows");
+
+__global__ __launch_bounds__(R4T, 2) void rope_attn4_kernel(AttnArgs a) {
+  constexpr int NH = 4;
+  extern __shared__ __attribute__((aligned(16))) uint8_t rsm[];
+  uint32_t* recK = reinterpret_cast<uint32_t*>(rsm + r4_off_reck());
+  uint32_t* recV = reinterpret_cast<uint32_t*>(rsm + r4_off_recv());
+  uint16_t* codes = reinterpret_cast<uint16_t*>(rsm + r4_off_codes());
+  f32x2* kmeta = reinterpret_cast<f32x2*>(rsm + r4_off_kmeta());
+  f32x2* tab = reinterpret_cast<f32x2*>(rsm + r4_off_tab());
+  float* vsum = reinterpret_cast<float*>(rsm + r4_off_vsum());  // [sl][dim], row NG: m V^T
+  float* qs = reinterpret_cast<float*>(rsm + r4_off_qs());
+  float* qpp = reinterpret_cast<float*>(rsm + r4_off_qpp());
+  float* red = reinterpret_cast<float*>(rsm + r4_off_red());
+  __shared__ float lst[NH], zst[NH][NG];
+
+  const int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, c32 = lane & 31;
+  const int s = b * a.n_kv_heads + kv;
+  const int nqh = a.n_qh;
+  const int Wk = a.Wk, Wv = a.Wv;
+  const Kept Kk = read_kept(a.bits_k + (int64_t)s * NG);
+  const Kept Kv = read_kept(a.bits_v + (int64_t)s * NG);
+  const bool ok = Kk.ok && Kv.ok && Kk.used <= Wk && Kv.used <= Wv;
+  const int64_t n_tiles = (a.n_tokens + 63) >> 6;
+  const int64_t tile_begin = (int64_t)chunk * a.tiles_per_chunk;
+  const int64_t tile_end = tile_begin + a.tiles_per_chunk < n_tiles ? tile_begin + a.tiles_per_chunk : n_tiles;
+  const float* Vk = a.basis_k + (int64_t)s * D * D;
+
+  // ---- prologue: in-tile rotation table, scaled queries, group sums and m V^T of the key basis ----
+  for (int e = tid; e < 64 * 64; e += R4T) {
+    const int r = e >> 6, i = e & 63;
+    float c, sn;
+    sincos_reduced((double)r * (double)a.inv_freq[i], &c, &sn);
+    tab[r * R4TP + i] = f32x2{c, sn};
+  }
+  for (int e = tid; e < NH * 64; e += R4T) {
+    const int hh = e >> 6, i = e & 63;
+    float q0 = 0.0f, q1 = 0.0f;
+    if (hh < nqh) {
+      const int64_t qi = ((int64_t)b * a.n_q_heads + kv * nqh + hh) * D + i;
+      q0 = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi]);
+      q1 = a.q_f32 ? reinterpret_cast<const float*>(a.q)[qi + 64] : bf2f(reinterpret_cast<const uint16_t*>(a.q)[qi + 64]);
+    }
+    qs[hh * D + i] = q0 * a.scale_log2;
+    qs[hh * D + 64 + i] = q1 * a.scale_log2;
+  }
+  if (tid < D) {
+    const float* vr = Vk + (int64_t)tid * D;
+    const float* ms = a.mean_k + (int64_t)s * D;
+    float bias = 0.0f;
+    for (int j = 0; j < D; ++j) bias = __builtin_fmaf(ms[j], vr[j], bias);
+    vsum[NG * D + tid] = bias;
+#pragma unroll
+    for (int sl = 0; sl < NG; ++sl) {
+      float acc = 0.0f;
+      if (sl < Kk.n)
+        for (int j = 0; j < G; ++j) acc += vr[G * pick4(Kk.grp, sl) + j];
+      vsum[sl * D + tid] = acc;
+    }
+  }
+  // reconstruction operands of this lane (32x32x16 layout): row m = lane % 32 is
+  // dimension 16 wave + m (m < 16) or 48 + 16 wave + m (m >= 16); K = in-group
+  // coefficients 16 ks + 8 h .. + 7 of each kept key slot, as three bf16 parts
+  const int dimA = c32 < 16 ? 16 * wave + c32 : 48 + 16 * wave + c32;
+  bf16x8 Va[NG][2][3];
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      if (sl < Kk.n) {
+        const float* vr = Vk + (int64_t)dimA * D + G * pick4(Kk.grp, sl) + 16 * ks + 8 * h;
+        uint32_t p0[8], p1[8], p2[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) split3(vr[i], p0[i], p1[i], p2[i]);
+        Va[sl][ks][0] = as_bf16x8(u32x4{pack2(p0[0], p0[1]), pack2(p0[2], p0[3]), pack2(p0[4], p0[5]), pack2(p0[6], p0[7])});
+        Va[sl][ks][1] = as_bf16x8(u32x4{pack2(p1[0], p1[1]), pack2(p1[2], p1[3]), pack2(p1[4], p1[5]), pack2(p1[6], p1[7])});
+        Va[sl][ks][2] = as_bf16x8(u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])});
+      } else {
+#pragma unroll
+        for (int p = 0; p < 3; ++p) Va[sl][ks][p] = bf16x8{};
+      }
+    }
+  }
+
+  // value path of this wavefront: kept value slot `wave` over the whole tile
+  const bool vslot = wave < Kv.n;
+  const int vB = vslot ? pick4(Kv.bits, wave) : 0, vpay = vslot ? pick4(Kv.pay, wave) : 0;
+  const int vgrp = vslot ? pick4(Kv.grp, wave) : 0;
+  const int col16 = lane & 15, kq = lane >> 4;
+  const int voff = 2 * col16 * vB;
+  uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + r4_off_wt()) + wave * (2 * NH * WROW);
+
+  float m_run[NH], l_run[NH], zacc[NH];
+#pragma unroll
+  for (int hh = 0; hh < NH; ++hh) {
+    m_run[hh] = -__builtin_inff();
+    l_run[hh] = 0.0f;
+    zacc[hh] = 0.0f;
+  }
+  f32x4 vacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+
+  // record words of one tile, a quarter per thread and tensor: word w of token t is
+  // element 64 w + t of the tile (tid + 256 i)
+  const uint32_t* kps = a.packed_k + (int64_t)s * a.t_cap * Wk;
+  const uint32_t* vps = a.packed_v + (int64_t)s * a.t_cap * Wv;
+  constexpr int PF = 64 * R4W / R4T;
+  uint32_t pk[PF], pv[PF];
+  auto load_k = [&](int64_t tt) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + R4T * i;
+      pk[i] = k < 64 * Wk ? kps[tt * 64 * Wk + k] : 0u;
+    }
+  };
+  auto load_v = [&](int64_t tt) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + R4T * i;
+      pv[i] = k < 64 * Wv ? vps[tt * 64 * Wv + k] : 0u;
+    }
+  };
+  auto stage = [&](uint32_t* rec, const uint32_t (&pr)[PF], int W) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int k = tid + R4T * i;
+      if (k < 64 * W) rec[(k >> 6) * TROW + (k & 63)] = pr[i];
+    }
+  };
+  // codes of the staged key words as bf16 [token][slot * 32 + coefficient] and each
+  // token's scale and zero point [slot][token]: thread (token lane, eight coefficients
+  // of one slot); slot and coefficient octet uniform in a wavefront
+  auto unpack_k = [&]() {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int sl = r, k8 = wave;
+      if (sl < Kk.n) {
+        const int pay = pick4(Kk.pay, sl);
+        const uint32_t* rt = recK + lane;
+        with_bits(pick4(Kk.bits, sl), [&](auto bc) {
+          constexpr int B = decltype(bc)::value;
+          uint32_t cd[8];
+          extract8<B>([&](int i) { return rt[(pay + i) * TROW]; }, 8 * k8, cd);
+          *reinterpret_cast<u32x4*>(codes + lane * RCP + sl * G + 8 * k8) =
+              u32x4{int_to_bf16_pair(cd[0], cd[1]), int_to_bf16_pair(cd[2], cd[3]), int_to_bf16_pair(cd[4], cd[5]),
+                    int_to_bf16_pair(cd[6], cd[7])};
+        });
+        if (k8 == 0) {
+          const uint32_t m = rt[sl * TROW];
+          kmeta[sl * RTT + lane] = f32x2{h2f(m), h2f(m >> 16)};
+        }
+      }
+    }
+  };
+  // queries rotated by (p_q - 64 tt) w_i, [pair i][head][2] (lane = pair), by the last wavefront
+  auto rotate_queries = [&](int64_t tt) {
+    float c, sn;
+    sincos_reduced((double)(a.q_pos - tt * 64) * (double)a.inv_freq[lane], &c, &sn);
+#pragma unroll
+    for (int hh = 0; hh < NH; hh += 2) {
+      const float a0 = qs[hh * D + lane], a1 = qs[hh * D + 64 + lane];
+      const float b0 = qs[(hh + 1) * D + lane], b1 = qs[(hh + 1) * D + 64 + lane];
+      *reinterpret_cast<f32x4*>(qpp + (lane * NH + hh) * 2) =
+          f32x4{a0 * c - a1 * sn, a1 * c + a0 * sn, b0 * c - b1 * sn, b1 * c + b0 * sn};
+    }
+  };
+  __syncthreads();  // tables, queries and sums visible
+  if (ok && tile_begin < tile_end) {
+    load_k(tile_begin);
+    stage(recK, pk, Wk);
+    if (wave == 3) rotate_queries(tile_begin);
+    __syncthreads();
+    unpack_k();
+    if (tile_begin + 1 < tile_end) load_k(tile_begin + 1);
+    load_v(tile_begin);
+    __syncthreads();  // codes, scales and rotated queries of the first tile visible
+  }
+
+  for (int64_t tt = tile_begin; ok && tt < tile_end; ++tt) {
+    const bool more = tt + 1 < tile_end;
+    // keep the loop-invariant LDS operands (sums, angle tables) as reads inside the
+    // loop rather than registers held across it
+    asm volatile("" ::: "memory");
+    // this tile's value words and the next tile's key words to LDS, the loads after them
+    stage(recV, pv, Wv);
+    if (more) stage(recK, pk, Wk);
+    if (tt + 2 < tile_end) load_k(tt + 2);
+    if (more) load_v(tt + 1);
+
+    // ---- 1. reconstruction, in-tile rotation and dot products, 32 tokens at a time ----
+#pragma unroll 1
+    for (int tb = 0; tb < 2; ++tb) {
+      const int tok = 32 * tb + c32;  // the lane's token (output column)
+      f32x16 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m0 = 8 * q + 4 * h;
+        const int d0 = m0 < 16 ? 16 * wave + m0 : 48 + 16 * wave + m0;
+        const f32x4 bv = *reinterpret_cast<const f32x4*>(&vsum[NG * D + d0]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[4 * q + r] = bv[r];
+      }
+#pragma unroll
+      for (int sl = 0; sl < NG; ++sl) {
+        if (sl < Kk.n) {
+          f32x16 acc = {};
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const bf16x8 C = as_bf16x8(*reinterpret_cast<const u32x4*>(codes + tok * RCP + sl * G + 16 * ks + 8 * h));
+#pragma unroll
+            for (int p = 0; p < 3; ++p) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Va[sl][ks][p], C, acc, 0, 0, 0);
+          }
+          const f32x2 sz = kmeta[sl * RTT + tok];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int m0 = 8 * q + 4 * h;
+            const int d0 = m0 < 16 ? 16 * wave + m0 : 48 + 16 * wave + m0;
+            const f32x4 v4 = *reinterpret_cast<const f32x4*>(&vsum[sl * D + d0]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) o[4 * q + r] = __builtin_fmaf(sz[0], acc[4 * q + r], __builtin_fmaf(sz[1], v4[r], o[4 * q + r]));
+          }
+        }
+      }
+      // pairs: row m < 16 (entry j < 8) with row m + 16 (entry j + 8), i = 16 wave + m
+      const f32x2* tr = tab + tok * R4TP;
+      float sc[NH];
+#pragma unroll
+      for (int hh = 0; hh < NH; ++hh) sc[hh] = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = 16 * wave + 8 * (j >> 2) + 4 * h + (j & 3);
+        const f32x2 cs = tr[i];
+        const float c = cs[0], sn = cs[1];
+        const float x0 = o[j], x1 = o[j + 8];
+        const float r0 = x0 * c - x1 * sn, r1 = x1 * c + x0 * sn;
+        const f32x4 qa = *reinterpret_cast<const f32x4*>(qpp + (i * NH) * 2);
+        const f32x4 qb = *reinterpret_cast<const f32x4*>(qpp + (i * NH + 2) * 2);
+        sc[0] = __builtin_fmaf(qa[0], r0, __builtin_fmaf(qa[1], r1, sc[0]));
+        sc[1] = __builtin_fmaf(qa[2], r0, __builtin_fmaf(qa[3], r1, sc[1]));
+        sc[2] = __builtin_fmaf(qb[0], r0, __builtin_fmaf(qb[1], r1, sc[2]));
+        sc[3] = __builtin_fmaf(qb[2], r0, __builtin_fmaf(qb[3], r1, sc[3]));
+      }
+      // the other half of the wavefront holds the other eight pairs of the same token
+#pragma unroll
+      for (int hh = 0; hh < NH; ++hh) sc[hh] += other_half(sc[hh]);
+      if (h == 0) {
+#pragma unroll
+        for (int hh = 0; hh < NH; ++hh) red[(wave * NH + hh) * 64 + tok] = sc[hh];
+      }
+    }
+    __syncthreads();  // partial scores, value words and the next tile's key words visible
+
+    // ---- 2. online softmax over the tile (lane = token) and value sums ----
+    const bool valid = tt * 64 + lane < a.n_tokens;
+    float x[NH];
+    bool over = false;
+#pragma unroll
+    for (int hh = 0; hh < NH; ++hh) {
+      const float acc = (red[(0 * NH + hh) * 64 + lane] + red[(1 * NH + hh) * 64 + lane]) +
+                        (red[(2 * NH + hh) * 64 + lane] + red[(3 * NH + hh) * 64 + lane]);
+      x[hh] = (valid && hh < nqh) ? acc : -__builtin_inff();
+      over = over || x[hh] > m_run[hh] + RESCALE_SLACK;
+    }
+    if (__any(over)) {
+#pragma unroll
+      for (int hh = 0; hh < NH; ++hh) {
+        if (__any(x[hh] > m_run[hh] + RESCALE_SLACK)) {
+          const float mn = __builtin_fmaxf(m_run[hh], wave_max_all(x[hh]));
+          const float alpha = (m_run[hh] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(m_run[hh] - mn);
+          l_run[hh] *= alpha;
+          zacc[hh] *= alpha;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int row = 4 * kq + j;
+            const float f = (row == hh || row == NH + hh) ? alpha : 1.0f;
+            vacc[0][j] *= f;
+            vacc[1][j] *= f;
+          }
+          m_run[hh] = mn;
+        }
+      }
+    }
+    float pw[NH];
+#pragma unroll
+    for (int hh = 0; hh < NH; ++hh) {
+      pw[hh] = x[hh] != -__builtin_inff() ? __builtin_amdgcn_exp2f(x[hh] - m_run[hh]) : 0.0f;
+      l_run[hh] += pw[hh];
+    }
+    if (vslot) {
+      const uint32_t meta = valid ? recV[wave * TROW + lane] : 0u;
+      const float sv = h2f(meta), zv = h2f(meta >> 16);
+#pragma unroll
+      for (int hh = 0; hh < NH; hh += 2) {  // two heads per packed conversion
+        zacc[hh] = __builtin_fmaf(pw[hh], zv, zacc[hh]);
+        zacc[hh + 1] = __builtin_fmaf(pw[hh + 1], zv, zacc[hh + 1]);
+        const float w0 = pw[hh] * sv, w1 = pw[hh + 1] * sv;
+        const uint32_t hb2 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0, w1}, bf16x2));
+        const float h0 = __builtin_bit_cast(float, hb2 << 16), h1 = __builtin_bit_cast(float, hb2 & 0xFFFF0000u);
+        const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{w0 - h0, w1 - h1}, bf16x2));
+        ws[hh * WROW + lane] = (uint16_t)hb2;
+        ws[(hh + 1) * WROW + lane] = (uint16_t)(hb2 >> 16);
+        ws[(NH + hh) * WROW + lane] = (uint16_t)lb;
+        ws[(NH + hh + 1) * WROW + lane] = (uint16_t)(lb >> 16);
+      }
+      __builtin_amdgcn_wave_barrier();
+      // rows 0..NH-1: hi weights of the heads, NH..2NH-1: lo; MFMA rows past them
+      // re-read a weight row and are never read back
+      const int arow = col16 < 2 * NH ? col16 : col16 - 2 * NH;
+      const bf16x8 negone = as_bf16x8(u32x4{0xBF80BF80u, 0xBF80BF80u, 0xBF80BF80u, 0xBF80BF80u});
+      uint32_t vmagic = 0x3F803F80u;  // exponent of 1.0 in both halves (see value_codes2)
+      asm volatile("" : "+v"(vmagic));
+      auto body = [&](auto cls) {
+        constexpr int CLS = decltype(cls)::value;
+#pragma unroll
+        for (int th = 0; th < 2; ++th) {
+          const int tok0 = 32 * th + 8 * kq;
+          const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(ws + arow * WROW + tok0));
+          u32x4 vc[2];
+          value_codes2<CLS>(recV, vpay, Kv.used, vB, voff, tok0, vmagic, vc[0], vc[1]);
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2) {
+            f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, as_bf16x8(vc[c2]), vacc[c2], 0, 0, 0);
+            if constexpr (CLS != 2) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aw, negone, acc, 0, 0, 0);
+            vacc[c2] = acc;
+          }
+        }
+      };
+      if (vB == 8)
+        body(std::integral_constant<int, 2>{});
+      else if (vB == 1 || vB == 2 || vB == 4)
+        body(std::integral_constant<int, 0>{});
+      else
+        body(std::integral_constant<int, 1>{});
+    }
+    if (more) {
+      unpack_k();
+      if (wave == 3) rotate_queries(tt + 1);
+    }
+    __syncthreads();  // the tile's LDS reads done; the next tile's codes and queries visible
+  }
+
+  // ---- chunk partial: m, l and the zero-point sums per head, value sums per coefficient ----
+  // (every wavefront holds the same m and l: the softmax runs in all of them)
+  float zs[NH];
+#pragma unroll
+  for (int hh = 0; hh < NH; ++hh) {
+    const float l = wave_sum_lane63(l_run[hh]);
+    zs[hh] = wave_sum_lane63(zacc[hh]);
+    if (wave == 0 && lane == 63) lst[hh] = l;
+  }
+  if (tid < NH * NG) zst[tid / NG][tid % NG] = 0.0f;
+  __syncthreads();
+  if (vslot && lane == 63) {
+#pragma unroll
+    for (int hh = 0; hh < NH; ++hh) zst[hh][vgrp] = zs[hh];
+  }
+  float* accw = reinterpret_cast<float*>(codes);  // [2NH][AROW]: hi-weight rows, then lo
+  if (vslot) {
+    // codes below 8 bits entered as 1 + c 2^-b (see value_codes2)
+    const float vscale = vB < 8 ? (float)(1u << vB) : 1.0f;
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = 4 * kq + j;
+        if (row < 2 * NH) accw[row * AROW + G * vgrp + 2 * col16 + c2] = vacc[c2][j] * vscale;
+      }
+  }
+  uint32_t kept_groups = 0u;
+#pragma unroll
+  for (int sl = 0; sl < NG; ++sl)
+    if (sl < Kv.n) kept_groups |= 1u << pick4(Kv.grp, sl);
+  __syncthreads();
+  float* part = a.partial + ((int64_t)b * a.n_q_heads + kv * nqh) * a.n_chunks * PART + (int64_t)chunk * PART;
+  const bool any = ok && tile_begin < tile_end;
+  for (int e = tid; e < nqh * D; e += R4T) {
+    const int hh = e >> 7, j = e & 127;
+    const bool kept = any && ((kept_groups >> (j >> 5)) & 1u);
+    float* ph = part + (int64_t)hh * a.n_chunks * PART;
+    ph[8 + j] = kept ? accw[hh * AROW + j] + accw[(NH + hh) * AROW + j] : 0.0f;
+    if (j == 0) {
+      ph[0] = any ? m_run[hh] : -__builtin_inff();
+      ph[1] = any ? lst[hh] : 0.0f;
+    }
+    if (j < NG) ph[2 + j] = any ? zst[hh][j] : 0.0f;
+  }
+}
+
 }  // namespace spectra_dev
 
 namespace spectra {
 using namespace spectra_dev;
 
-// About one workgroup per CU in one round, at least four tiles per chunk.
-int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk) {
+// About per_cu workgroups per CU in one round, at least four tiles per chunk.
+int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_tokens, int32_t* tiles_per_chunk,
+                              int32_t per_cu) {
   const int64_t n_tiles = (n_tokens + 63) / 64;
   const int64_t groups = (int64_t)batch * n_kv_heads;
-  const int64_t want = (256 + groups - 1) / groups;
+  const int64_t want = (256 * (int64_t)per_cu + groups - 1) / groups;
   int64_t tpc = (n_tiles + want - 1) / want;
   if (tpc < 4) tpc = 4;
   *tiles_per_chunk = (int32_t)tpc;
   return (int32_t)((n_tiles + tpc - 1) / tpc);
 }
 
+// The four-wavefront kernel (two workgroups per CU) for at most four query heads per
+// KV head and records of at most 16 words; the eight-wavefront kernel otherwise.
 hipError_t launch_attention_rope(const AttnArgs& a, hipStream_t st) {
-  // the tile buffers need more than 64 KB of LDS: refuse a device that has less
   int dev = 0, lds = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return e;
-  const int nh = a.n_qh <= 4 ? 4 : 8;
-  if (lds < rope_lds_bytes(nh)) return hipErrorInvalidConfiguration;
-  const dim3 grid(a.n_chunks, a.n_kv_heads, a.batch);
-  if (nh == 4)
-    hipLaunchKernelGGL(rope_attn_kernel<1>, grid, dim3(RTHREADS), rope_lds_bytes(4), st, a);
-  else
-    hipLaunchKernelGGL(rope_attn_kernel<2>, grid, dim3(RTHREADS), rope_lds_bytes(8), st, a);
+  const bool four = a.n_qh <= 4 && a.Wk <= R4W && a.Wv <= R4W && lds >= r4_lds_bytes();
+  AttnArgs g = a;
+  g.n_chunks = rope_attention_chunks(a.batch, a.n_kv_heads, a.n_tokens, &g.tiles_per_chunk, four ? 2 : 1);
+  const dim3 grid(g.n_chunks, g.n_kv_heads, g.batch);
+  if (four) {
+    hipLaunchKernelGGL(rope_attn4_kernel, grid, dim3(R4T), r4_lds_bytes(), st, g);
+  } else {
+    // the tile buffers need more than 64 KB of LDS: refuse a device that has less
+    const int nh = a.n_qh <= 4 ? 4 : 8;
+    if (lds < rope_lds_bytes(nh)) return hipErrorInvalidConfiguration;
+    if (nh == 4)
+      hipLaunchKernelGGL(rope_attn_kernel<1>, grid, dim3(RTHREADS), rope_lds_bytes(4), st, g);
+    else
+      hipLaunchKernelGGL(rope_attn_kernel<2>, grid, dim3(RTHREADS), rope_lds_bytes(8), st, g);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_combine(a, st);
+  return launch_combine(g, st);
 }
 
 }  // namespace spectra
