@@ -5,8 +5,10 @@
 // their weighted sums run over the kept value coefficients and the chunk combine
 // (log-sum-exp merge, + m_V, one inverse rotation) is the latent kernel's.
 //
-// One workgroup of eight wavefronts per (token chunk, KV head, sequence), 64-token
-// tiles, three workgroup barriers per tile. While tile tt is processed, the record
+// Two kernels. rope_attn4_kernel (at most four query heads per KV head, records of at
+// most 16 words; described further down) keeps the reconstructed keys in registers.
+// rope_attn_kernel serves the wider shapes: one workgroup of eight wavefronts per
+// (token chunk, KV head, sequence), 64-token tiles, three workgroup barriers per tile. While tile tt is processed, the record
 // words of tile tt + 1 are staged and its key codes unpacked, once for the whole
 // workgroup, into a bf16 tile in LDS:
 //   1. wavefront w reconstructs key dimensions 16w..16w+15 of the 64 tokens,
@@ -492,7 +494,7 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
 // keys never leave the registers.
 //   1. wavefront w reconstructs dimensions 16w..16w+15 and 64+16w..64+16w+15 of the
 //      tile's 64 tokens on v_mfma_f32_32x32x16_bf16 (rows m and m + 16 of its 32-row
-//      output are the pair (16w + m, 80w... i.e. i and i + 64), so a lane holds both
+//      output are the pair (i, i + 64) with i = 16w + m, so a lane holds both
 //      members of eight pairs of one token), rotates them by the token's in-tile
 //      offset r (a 64 x 64 table of cos and sin of r w_i), dots them with the tile's
 //      rotated queries and leaves its partial scores in LDS;
