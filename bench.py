@@ -45,17 +45,17 @@ DECODE_STEP_SOURCES = ("kernels_attn.hip", "attn_common.hpp", "kplan.hpp", "enco
                        "kernels.hpp")
 # sha256 -> fetch / write bytes per call; per_kernel: [fetch, write]
 MEASURED_TRAFFIC = {
-    "8bf2b03fa8b47d7252d6306a613e5ea55ef3e0a467020b31bc4c5509e0ec6b7f": {
-        "fetch_bytes": 74479173, "write_bytes": 1674244, "mfma_busy": 0.096,
-        "per_kernel": {"attn_kernel<1,8,8,true>": [70702812, 1657860], "combine_kernel": [3776361, 16384]}},
+    "0dc6e80a2b7f61b0b562fde7cbff11884cbad20ea2f1c2a005395111734033e8": {
+        "fetch_bytes": 74542716, "write_bytes": 1674244, "mfma_busy": 0.096,
+        "per_kernel": {"attn_kernel<1,8,8,true>": [70734430, 1657860], "combine_kernel": [3808286, 16384]}},
 }
 # The same passes over the bulk encode of one codec (256 streams x 131072 tokens):
 # HBM bytes per call and the matrix cores' busy fraction (SQ_VALU_MFMA_BUSY_CYCLES
 # over GRBM_GUI_ACTIVE x 1024 SIMDs), keyed by sha256 over ENCODE_SOURCES.
 ENCODE_SOURCES = ("kernels_codec.hip", "encode_dev.hpp", "device_common.hpp", "kernels.hpp")
 MEASURED_ENCODE = {
-    "712e6e83e451649406c652c5af098a0a3196dc738a3b76e31f7081c8e43b506e": {
-        "fetch_bytes": 8666146688, "write_bytes": 1073741824, "mfma_busy": 0.359},
+    "39359687aa625a2fad9927ac1b89124751d52288a590f4d285f932dbf9896b21": {
+        "fetch_bytes": 8665222080, "write_bytes": 1073741824, "mfma_busy": 0.368},
 }
 
 
