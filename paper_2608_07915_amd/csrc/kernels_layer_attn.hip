@@ -131,12 +131,13 @@ __global__ __launch_bounds__(256) void layer_qprep_kernel(LayerAttnArgs a) {
 // latent queries of 32 heads and the record rows would not fit the LDS together
 // (d = 1024 with records of more than ~100 words), one (NHB = 1, blockIdx.z selects it).
 __host__ __device__ constexpr int la_qp(int d) { return d + 8; }  // fp16 per staged query row
+constexpr int LA_QSP = 17;  // floats per row of the group sums (16 slots + pad: the rows of four heads read together lie on distinct banks)
 __host__ __device__ constexpr int la_off_rec(int d, int nhb) { return 2 * 16 * nhb * la_qp(d) * 2; }
 // the record rows also hold the slot halves' scores of a tile ([4][64][8] floats) once read
 __host__ __device__ constexpr int la_rec_bytes(int Wk) { return Wk * LA_ROW * 4 > 4 * 64 * 8 * 4 ? Wk * LA_ROW * 4 : 4 * 64 * 8 * 4; }
 __host__ __device__ constexpr int la_off_qs(int d, int Wk, int nhb) { return la_off_rec(d, nhb) + la_rec_bytes(Wk); }
 __host__ __device__ constexpr int la_scores_lds(int d, int Wk, int nhb) {
-  return la_off_qs(d, Wk, nhb) + LA_H * 16 * 4 + 4 * LA_H * 2 * 4;
+  return la_off_qs(d, Wk, nhb) + LA_H * LA_QSP * 4 + 4 * LA_H * 2 * 4;
 }
 
 template <int NHB, int WP>
@@ -145,8 +146,8 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   const int d = a.d, ng = d / 64, QP = la_qp(d), Wk = a.Wk;
   uint16_t* qa = reinterpret_cast<uint16_t*>(lsm);                       // [2][16 NHB][QP]
   uint32_t* rec = reinterpret_cast<uint32_t*>(lsm + la_off_rec(d, NHB)); // [Wk][LA_ROW]
-  float* qs = reinterpret_cast<float*>(lsm + la_off_qs(d, Wk, NHB));     // [LA_H][16]
-  float* red = qs + LA_H * 16;                                           // [4][LA_H][2]
+  float* qs = reinterpret_cast<float*>(lsm + la_off_qs(d, Wk, NHB));     // [LA_H][LA_QSP]
+  float* red = qs + LA_H * LA_QSP;                                       // [4][LA_H][2]
   __shared__ int sgrp[16], sbw[16], spay[16], snk;
   const int chunk = blockIdx.x, b = blockIdx.y;
   const int hb0 = NHB == 2 ? 0 : (int)blockIdx.z;  // first head block of this workgroup
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
   }
   for (int e = tid; e < LA_H * 16; e += 512) {
     const int h = e >> 4, sl = e & 15;
-    qs[e] = (h < Hq && sl < nk) ? a.qsum[((int64_t)b * Hq + h) * 16 + sgrp[sl]] : 0.0f;
+    qs[h * LA_QSP + sl] = (h < Hq && sl < nk) ? a.qsum[((int64_t)b * Hq + h) * 16 + sgrp[sl]] : 0.0f;
   }
 
   const int64_t n_tiles = (a.n_tokens + 63) >> 6;
@@ -254,25 +255,24 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
 #pragma unroll
       for (int hb = 0; hb < NHB; ++hb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) S[hb][j] += st * g[hb][j] + zt * qs[(16 * (hb0 + hb) + 4 * kg + j) * 16 + sl];
+        for (int j = 0; j < 4; ++j) S[hb][j] += st * g[hb][j] + zt * qs[(16 * (hb0 + hb) + 4 * kg + j) * LA_QSP + sl];
     }
     // the two slot halves meet in LDS (over the record rows, whose reads are done)
     __syncthreads();
     if (sh == 1) {
 #pragma unroll
-      for (int hb = 0; hb < NHB; ++hb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sred[(tb * 64 + lane) * 8 + 4 * hb + j] = S[hb][j];
+      for (int hb = 0; hb < NHB; ++hb) *reinterpret_cast<f32x4*>(&sred[(tb * 64 + lane) * 8 + 4 * hb]) = S[hb];
     }
     __syncthreads();
     if (sh == 0) {
       const int64_t t = tt * 64 + u;
 #pragma unroll
-      for (int hb = 0; hb < NHB; ++hb)
+      for (int hb = 0; hb < NHB; ++hb) {
+        const f32x4 o4 = *reinterpret_cast<const f32x4*>(&sred[(tb * 64 + lane) * 8 + 4 * hb]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int h = 16 * (hb0 + hb) + 4 * kg + j;
-          const float x = S[hb][j] + sred[(tb * 64 + lane) * 8 + 4 * hb + j];
+          const float x = S[hb][j] + o4[j];
           if (t < a.n_tokens && h < Hq) {
             a.scores[((int64_t)b * Hq + h) * a.n_tokens + t] = x;
             const int q = 4 * hb + j;
@@ -284,6 +284,7 @@ __global__ __launch_bounds__(512) void layer_scores_kernel(LayerAttnArgs a) {
             }
           }
         }
+      }
     }
   }
   // chunk statistics: merge the 16 token lanes, then the four token-block wavefronts
