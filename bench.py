@@ -394,6 +394,19 @@ def config_bench(S, torch, w, dev, reps=4):
         runs.append((e0, e1))
     torch.cuda.synchronize()
     att_ms = sum(e0.elapsed_time(e1) for e0, e1 in runs) / (reps * steps)
+    # Mode A with rotary embeddings over the same caches (keys reconstructed and rotated)
+    theta = 1.0e6 if w.name.startswith("qwen") else 5.0e5
+    inv_freq = (theta ** (-torch.arange(d // 2, dtype=torch.float64, device=dev) / (d // 2))).float()
+    rope = []
+    for i in range(reps + 1):
+        kp, vp = caches[i % copies]
+        e0, e1 = ev(), ev()
+        e0.record()
+        S.spectra_decode_attention_rope(ck, cv, kp, vp, t_cap, T, qs[i % steps], H, inv_freq, out=out, workspace=ws)
+        e1.record()
+        rope.append((e0, e1))
+    torch.cuda.synchronize()
+    rope_ms = min(e0.elapsed_time(e1) for e0, e1 in rope[1:])
     del caches, g
     enc_gbps = enc_bytes / (enc_ms * 1e-3) / 1e9
     att_gbps = att_bytes / (att_ms * 1e-3) / 1e9
@@ -406,6 +419,9 @@ def config_bench(S, torch, w, dev, reps=4):
                       "cache_tokens_per_s": round(B * T / (att_ms * 1e-3), 1),
                       "sequences_per_s": round(B / (att_ms * 1e-3), 1),
                       "steps_timed": steps * reps, "distinct_cache_copies": copies},
+        "mode_a_rope_attention": {"us_per_call": round(rope_ms * 1e3, 1),
+                                  "GBps": round(att_bytes / (rope_ms * 1e-3) / 1e9, 1),
+                                  "rope_theta": theta},
         "bits_k_first": ck.bits[0].cpu().numpy().tolist(), "bits_v_first": cv.bits[0].cpu().numpy().tolist(),
     }
 

@@ -5,7 +5,7 @@
 // their weighted sums run over the kept value coefficients and the chunk combine
 // (log-sum-exp merge, + m_V, one inverse rotation) is the latent kernel's.
 //
-// Two kernels. rope_attn4_kernel (at most four query heads per KV head, records of at
+// Two kernels. rope_attn4_kernel (at most eight query heads per KV head, records of at
 // most 16 words; described further down) keeps the reconstructed keys in registers.
 // rope_attn_kernel serves the wider shapes: one workgroup of eight wavefronts per
 // (token chunk, KV head, sequence), 64-token tiles, three workgroup barriers per tile. While tile tt is processed, the record
@@ -489,14 +489,14 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Four-wavefront form (at most four query heads per KV head, records of at most 16
+// Four-wavefront form (at most eight query heads per KV head, records of at most 16
 // words): two workgroups per CU, two workgroup barriers per tile, the reconstructed
 // keys never leave the registers.
 //   1. wavefront w reconstructs dimensions 16w..16w+15 and 64+16w..64+16w+15 of the
 //      tile's 64 tokens on v_mfma_f32_32x32x16_bf16 (rows m and m + 16 of its 32-row
 //      output are the pair (i, i + 64) with i = 16w + m, so a lane holds both
 //      members of eight pairs of one token), rotates them by the token's in-tile
-//      offset r (a 64 x 64 table of cos and sin of r w_i), dots them with the tile's
+//      offset r (cos and sin of r w_i from a table), dots them with the tile's
 //      rotated queries and leaves its partial scores in LDS;
 //      it also stages the next tile's key words and this tile's value words;
 //   2. online softmax (lane = token) in every wavefront; wavefront w adds the
@@ -505,35 +505,43 @@ __global__ __launch_bounds__(RTHREADS, 1) void rope_attn_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int R4W = 16;  // record words per tensor
 constexpr int R4T = 256;  // threads
+// In-tile rotation table: with four heads one row of (cos, sin) of r w_i per in-tile
+// offset r (64 rows); with eight heads (whose query buffers take the room) two tables of
+// eight rows, b w_i and 8a w_i, composed per use (r = 8a + b). Rows hold 64 frequencies
+// + a pad, so the rows of the 32 tokens of one read start on distinct banks.
+constexpr int R4TP = 65;
+__host__ __device__ constexpr int r4_tab_rows(int nh) { return nh <= 4 ? 64 : 16; }
 __host__ __device__ constexpr int r4_off_reck() { return 0; }                                   // [R4W][TROW] u32
 __host__ __device__ constexpr int r4_off_recv() { return R4W * TROW * 4; }                      // [R4W][TROW] u32
 __host__ __device__ constexpr int r4_off_codes() { return 2 * R4W * TROW * 4; }                 // [64][RCP] bf16
 __host__ __device__ constexpr int r4_off_kmeta() { return r4_off_codes() + RTT * RCP * 2; }     // [NG][64] (s, z)
-constexpr int R4TP = 65;  // (cos, sin) pairs per table row: 64 frequencies + pad, rows of distinct tokens on distinct banks
-__host__ __device__ constexpr int r4_off_tab() { return r4_off_kmeta() + NG * RTT * 8; }       // [64][R4TP] (cos, sin)
-__host__ __device__ constexpr int r4_off_vsum() { return r4_off_tab() + 64 * R4TP * 8; }       // [NG + 1][128]: sums, m V^T
-__host__ __device__ constexpr int r4_off_qs() { return r4_off_vsum() + (NG + 1) * D * 4; }     // [4][128]
-__host__ __device__ constexpr int r4_off_qpp() { return r4_off_qs() + 4 * D * 4; }             // [64][4][2]
-__host__ __device__ constexpr int r4_off_red() { return r4_off_qpp() + 64 * 4 * 2 * 4; }       // [4][4][64]
-__host__ __device__ constexpr int r4_off_wt() { return r4_off_red() + 4 * 4 * 64 * 4; }        // [4][8][WROW] bf16
-__host__ __device__ constexpr int r4_lds_bytes() { return r4_off_wt() + 4 * 8 * WROW * 2; }
+__host__ __device__ constexpr int r4_off_tab() { return r4_off_kmeta() + NG * RTT * 8; }       // [rows][R4TP] (cos, sin)
+__host__ __device__ constexpr int r4_off_vsum(int nh) { return r4_off_tab() + r4_tab_rows(nh) * R4TP * 8; }  // [NG + 1][128]
+__host__ __device__ constexpr int r4_off_qs(int nh) { return r4_off_vsum(nh) + (NG + 1) * D * 4; }          // [nh][128]
+__host__ __device__ constexpr int r4_off_qpp(int nh) { return r4_off_qs(nh) + nh * D * 4; }                 // [64][nh][2]
+__host__ __device__ constexpr int r4_off_red(int nh) { return r4_off_qpp(nh) + 64 * nh * 2 * 4; }           // [4][nh][64]
+__host__ __device__ constexpr int r4_off_wt(int nh) { return r4_off_red(nh) + 4 * nh * 64 * 4; }            // [4][2nh][WROW]
+__host__ __device__ constexpr int r4_lds_bytes(int nh) { return r4_off_wt(nh) + 4 * 2 * nh * WROW * 2; }
 static_assert(r4_off_codes() % 16 == 0 && r4_off_kmeta() % 16 == 0 && r4_off_tab() % 16 == 0, "16-byte reads");
-static_assert(r4_off_vsum() % 16 == 0 && r4_off_qpp() % 16 == 0 && r4_off_wt() % 16 == 0, "16-byte reads");
-static_assert(2 * r4_lds_bytes() <= 160 * 1024, "two workgroups per CU");
-static_assert(8 * AROW * 4 <= RTT * RCP * 2, "the value sums of the merge fit the code rows");
+static_assert(r4_off_vsum(4) % 16 == 0 && r4_off_qpp(4) % 16 == 0 && r4_off_wt(4) % 16 == 0, "16-byte reads");
+static_assert(r4_off_vsum(8) % 16 == 0 && r4_off_qpp(8) % 16 == 0 && r4_off_wt(8) % 16 == 0, "16-byte reads");
+static_assert(2 * r4_lds_bytes(4) <= 160 * 1024 && 2 * r4_lds_bytes(8) <= 160 * 1024, "two workgroups per CU");
+static_assert(16 * AROW * 4 <= RTT * RCP * 2, "the value sums of the merge fit the code rows");
 
+template <int NQ>
 __global__ __launch_bounds__(R4T, 2) void rope_attn4_kernel(AttnArgs a) {
-  constexpr int NH = 4;
+  constexpr int NH = 4 * NQ;
+  constexpr bool FULL_TAB = NH <= 4;
   extern __shared__ __attribute__((aligned(16))) uint8_t rsm[];
   uint32_t* recK = reinterpret_cast<uint32_t*>(rsm + r4_off_reck());
   uint32_t* recV = reinterpret_cast<uint32_t*>(rsm + r4_off_recv());
   uint16_t* codes = reinterpret_cast<uint16_t*>(rsm + r4_off_codes());
   f32x2* kmeta = reinterpret_cast<f32x2*>(rsm + r4_off_kmeta());
   f32x2* tab = reinterpret_cast<f32x2*>(rsm + r4_off_tab());
-  float* vsum = reinterpret_cast<float*>(rsm + r4_off_vsum());  // [sl][dim], row NG: m V^T
-  float* qs = reinterpret_cast<float*>(rsm + r4_off_qs());
-  float* qpp = reinterpret_cast<float*>(rsm + r4_off_qpp());
-  float* red = reinterpret_cast<float*>(rsm + r4_off_red());
+  float* vsum = reinterpret_cast<float*>(rsm + r4_off_vsum(NH));  // [sl][dim], row NG: m V^T
+  float* qs = reinterpret_cast<float*>(rsm + r4_off_qs(NH));
+  float* qpp = reinterpret_cast<float*>(rsm + r4_off_qpp(NH));
+  float* red = reinterpret_cast<float*>(rsm + r4_off_red(NH));
   __shared__ float lst[NH], zst[NH][NG];
 
   const int chunk = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
@@ -551,11 +559,12 @@ __global__ __launch_bounds__(R4T, 2) void rope_attn4_kernel(AttnArgs a) {
   const int64_t tile_end = tile_begin + a.tiles_per_chunk < n_tiles ? tile_begin + a.tiles_per_chunk : n_tiles;
   const float* Vk = a.basis_k + (int64_t)s * D * D;
 
-  // ---- prologue: in-tile rotation table, scaled queries, group sums and m V^T of the key basis ----
-  for (int e = tid; e < 64 * 64; e += R4T) {
+  // ---- prologue: in-tile rotation table(s), scaled queries, group sums and m V^T of the key basis ----
+  for (int e = tid; e < r4_tab_rows(NH) * 64; e += R4T) {
     const int r = e >> 6, i = e & 63;
+    const int off = FULL_TAB ? r : (r < 8 ? r : 8 * (r - 8));  // rows 0..7: b w_i, rows 8..15: 8a w_i
     float c, sn;
-    sincos_reduced((double)r * (double)a.inv_freq[i], &c, &sn);
+    sincos_reduced((double)off * (double)a.inv_freq[i], &c, &sn);
     tab[r * R4TP + i] = f32x2{c, sn};
   }
   for (int e = tid; e < NH * 64; e += R4T) {
@@ -613,7 +622,7 @@ __global__ __launch_bounds__(R4T, 2) void rope_attn4_kernel(AttnArgs a) {
   const int vgrp = vslot ? pick4(Kv.grp, wave) : 0;
   const int col16 = lane & 15, kq = lane >> 4;
   const int voff = 2 * col16 * vB;
-  uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + r4_off_wt()) + wave * (2 * NH * WROW);
+  uint16_t* ws = reinterpret_cast<uint16_t*>(rsm + r4_off_wt(NH)) + wave * (2 * NH * WROW);
 
   float m_run[NH], l_run[NH], zacc[NH];
 #pragma unroll
@@ -746,23 +755,32 @@ __global__ __launch_bounds__(R4T, 2) void rope_attn4_kernel(AttnArgs a) {
         }
       }
       // pairs: row m < 16 (entry j < 8) with row m + 16 (entry j + 8), i = 16 wave + m
-      const f32x2* tr = tab + tok * R4TP;
+      const f32x2* tr = tab + (FULL_TAB ? tok : (tok & 7)) * R4TP;
+      const f32x2* ta = tab + (8 + (tok >> 3)) * R4TP;  // eight heads: angle 8a w_i, r = 8a + b
       float sc[NH];
 #pragma unroll
       for (int hh = 0; hh < NH; ++hh) sc[hh] = 0.0f;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int i = 16 * wave + 8 * (j >> 2) + 4 * h + (j & 3);
-        const f32x2 cs = tr[i];
-        const float c = cs[0], sn = cs[1];
+        float c, sn;
+        if constexpr (FULL_TAB) {
+          const f32x2 cs = tr[i];
+          c = cs[0];
+          sn = cs[1];
+        } else {
+          const f32x2 cb = tr[i], ca = ta[i];
+          c = ca[0] * cb[0] - ca[1] * cb[1];
+          sn = ca[1] * cb[0] + ca[0] * cb[1];
+        }
         const float x0 = o[j], x1 = o[j + 8];
         const float r0 = x0 * c - x1 * sn, r1 = x1 * c + x0 * sn;
-        const f32x4 qa = *reinterpret_cast<const f32x4*>(qpp + (i * NH) * 2);
-        const f32x4 qb = *reinterpret_cast<const f32x4*>(qpp + (i * NH + 2) * 2);
-        sc[0] = __builtin_fmaf(qa[0], r0, __builtin_fmaf(qa[1], r1, sc[0]));
-        sc[1] = __builtin_fmaf(qa[2], r0, __builtin_fmaf(qa[3], r1, sc[1]));
-        sc[2] = __builtin_fmaf(qb[0], r0, __builtin_fmaf(qb[1], r1, sc[2]));
-        sc[3] = __builtin_fmaf(qb[2], r0, __builtin_fmaf(qb[3], r1, sc[3]));
+#pragma unroll
+        for (int hh = 0; hh < NH; hh += 2) {
+          const f32x4 qv = *reinterpret_cast<const f32x4*>(qpp + (i * NH + hh) * 2);
+          sc[hh] = __builtin_fmaf(qv[0], r0, __builtin_fmaf(qv[1], r1, sc[hh]));
+          sc[hh + 1] = __builtin_fmaf(qv[2], r0, __builtin_fmaf(qv[3], r1, sc[hh + 1]));
+        }
       }
       // the other half of the wavefront holds the other eight pairs of the same token
 #pragma unroll
@@ -927,19 +945,23 @@ int32_t rope_attention_chunks(int32_t batch, int32_t n_kv_heads, int64_t n_token
   return (int32_t)((n_tiles + tpc - 1) / tpc);
 }
 
-// The four-wavefront kernel (two workgroups per CU) for at most four query heads per
+// The four-wavefront kernel (two workgroups per CU) for at most eight query heads per
 // KV head and records of at most 16 words; the eight-wavefront kernel otherwise.
 hipError_t launch_attention_rope(const AttnArgs& a, hipStream_t st) {
   int dev = 0, lds = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return e;
-  const bool four = a.n_qh <= 4 && a.Wk <= R4W && a.Wv <= R4W && lds >= r4_lds_bytes();
+  const int nq = a.n_qh <= 4 ? 1 : 2;
+  const bool four = a.n_qh <= 8 && a.Wk <= R4W && a.Wv <= R4W && lds >= r4_lds_bytes(4 * nq);
   AttnArgs g = a;
   g.n_chunks = rope_attention_chunks(a.batch, a.n_kv_heads, a.n_tokens, &g.tiles_per_chunk, four ? 2 : 1);
   const dim3 grid(g.n_chunks, g.n_kv_heads, g.batch);
   if (four) {
-    hipLaunchKernelGGL(rope_attn4_kernel, grid, dim3(R4T), r4_lds_bytes(), st, g);
+    if (nq == 1)
+      hipLaunchKernelGGL(rope_attn4_kernel<1>, grid, dim3(R4T), r4_lds_bytes(4), st, g);
+    else
+      hipLaunchKernelGGL(rope_attn4_kernel<2>, grid, dim3(R4T), r4_lds_bytes(8), st, g);
   } else {
     // the tile buffers need more than 64 KB of LDS: refuse a device that has less
     const int nh = a.n_qh <= 4 ? 4 : 8;
