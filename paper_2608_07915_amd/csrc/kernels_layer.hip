@@ -309,13 +309,16 @@ __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
 // One workgroup: LD_CH = 64 output channels x LD_NT = 2 tiles of 128 tokens. The
 // group's basis operands and the mean term m V^T are built once per workgroup and
 // serve both tiles (the L2 reads of basis rows per token are what bound this kernel).
+// Registers are capped at 128 per lane so that two workgroups (four wavefronts per
+// SIMD) share a CU and hide each other's load latency; the compiler then spills a few
+// loop-invariant offsets, which costs less than the occupancy it buys.
 constexpr int LD_TOK = 128;       // tokens per tile
 constexpr int LD_NT = 2;          // tiles per workgroup
 constexpr int LD_CH = 64;         // output channels per workgroup
 constexpr int LD_P = LG + 8;      // bf16 per LDS row (144 bytes)
 constexpr int LD_R = 2 * LD_NT;   // staged (token, 8-code) pieces per thread
 
-__global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
+__global__ __launch_bounds__(512, 4) void layer_decode_kernel(LayerDecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vsl[3][LD_CH][LD_P];          // basis columns of the group, [channel][coef]
   __shared__ __attribute__((aligned(16))) uint16_t cod[LD_NT][LD_TOK][LD_P];     // codes, [tile][token][coef]
   __shared__ __attribute__((aligned(16))) float sl[LD_NT][LD_TOK], zl[LD_NT][LD_TOK], vsum[LD_CH], bias[LD_CH];
@@ -345,17 +348,12 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
     const int64_t i = tok0 + (int64_t)(e >> 10) * LD_TOK + (e & (LD_TOK - 1));
     tbase[r] = rec_word(sbase, a.t0 + (i < a.n ? i : a.n - 1), a.W, 0);
   }
-  float vpre[8], upre[8];
+  float vpre[8];
   uint32_t wpre[LD_R][3], mpre[LD_R];
   auto prefetch = [&](const LayerSlot& ks, int slot) {
     const float* vr = Vs + (int64_t)(ch0 + vc) * d + LG * ks.grp + 8 * vq;
 #pragma unroll
     for (int i = 0; i < 8; ++i) vpre[i] = vr[i];
-    if (a.lscale) {
-      const float* fr = a.lscale + (int64_t)s * d + LG * ks.grp + 8 * vq;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) upre[i] = fr[i];
-    }
 #pragma unroll
     for (int r = 0; r < LD_R; ++r) {
       const int k8 = ((tid + 512 * r) >> 7) & 7;
@@ -419,8 +417,9 @@ __global__ __launch_bounds__(512) void layer_decode_kernel(LayerDecodeArgs a) {
     }
     {
       if (a.lscale) {  // square-root split: c_hat_j / f_j, folded into the basis columns
+        const float* fr = a.lscale + (int64_t)s * d + LG * ks.grp + 8 * vq;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) vpre[i] = vpre[i] * (1.0f / upre[i]);
+        for (int i = 0; i < 8; ++i) vpre[i] = vpre[i] * (1.0f / fr[i]);
       }
       float sum = 0.0f;
 #pragma unroll
