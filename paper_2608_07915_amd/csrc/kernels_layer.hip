@@ -166,7 +166,7 @@ __device__ __forceinline__ int le_row(int c) {
   return 32 * (c >> 5) + (cc & 3) + 4 * (cc >> 4) + 8 * ((cc >> 2) & 3);
 }
 
-__global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
+__global__ __launch_bounds__(512, 4) void layer_encode_kernel(LayerEncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vs[3][64][LE_KP];
   const int s = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
@@ -220,12 +220,9 @@ __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
       *reinterpret_cast<u32x4*>(&vs[2][srow][sk]) = u32x4{pack2(p2[0], p2[1]), pack2(p2[2], p2[3]), pack2(p2[4], p2[5]), pack2(p2[6], p2[7])};
     }
     __syncthreads();
-    u32x4 xn[4];
     if (kc + 1 < nk) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) pre[i] = V[(int64_t)((kc + 1) * LE_KC + sk + i) * d + sc];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) xn[k] = *reinterpret_cast<const u32x4*>(xr + (kc + 1) * LE_KC + 16 * k + 8 * h);
     }
     f32x16 ch0 = {}, ch1 = {};
 #pragma unroll
@@ -251,7 +248,7 @@ __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
     }
     if (kc + 1 < nk) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) xb[k] = xn[k];
+      for (int k = 0; k < 4; ++k) xb[k] = *reinterpret_cast<const u32x4*>(xr + (kc + 1) * LE_KC + 16 * k + 8 * h);
     }
     __syncthreads();
   }
@@ -310,8 +307,8 @@ __global__ __launch_bounds__(512) void layer_encode_kernel(LayerEncodeArgs a) {
 // group's basis operands and the mean term m V^T are built once per workgroup and
 // serve both tiles (the L2 reads of basis rows per token are what bound this kernel).
 // Registers are capped at 128 per lane so that two workgroups (four wavefronts per
-// SIMD) share a CU and hide each other's load latency; the compiler then spills a few
-// loop-invariant offsets, which costs less than the occupancy it buys.
+// SIMD) share a CU and hide each other's load latency; per-piece shift amounts are
+// scalar and record offsets are recomputed per slot, so almost nothing spills.
 constexpr int LD_TOK = 128;       // tokens per tile
 constexpr int LD_NT = 2;          // tiles per workgroup
 constexpr int LD_CH = 64;         // output channels per workgroup
@@ -341,26 +338,32 @@ __global__ __launch_bounds__(512, 4) void layer_decode_kernel(LayerDecodeArgs a)
   // 8 (tid & 7) .. + 7; piece r: token u_r = (tid + 512 r) & 127 of tile (tid + 512 r) >> 10,
   // coefficients 8 k8_r .. + 7 with k8_r = ((tid + 512 r) >> 7) & 7 (uniform in a wavefront)
   const int vc = tid >> 3, vq = tid & 7;
-  int64_t tbase[LD_R];
-#pragma unroll
-  for (int r = 0; r < LD_R; ++r) {
-    const int e = tid + 512 * r;
-    const int64_t i = tok0 + (int64_t)(e >> 10) * LD_TOK + (e & (LD_TOK - 1));
-    tbase[r] = rec_word(sbase, a.t0 + (i < a.n ? i : a.n - 1), a.W, 0);
-  }
+  // ((tid + 512 r) >> 7) & 7 = (kq + 4 r) & 7 with kq = tid >> 7, uniform in a wavefront:
+  // held in a scalar register, so the shift amounts derived from it are scalar too
+  const int kq = __builtin_amdgcn_readfirstlane(tid >> 7);
   float vpre[8];
   uint32_t wpre[LD_R][3], mpre[LD_R];
   auto prefetch = [&](const LayerSlot& ks, int slot) {
     const float* vr = Vs + (int64_t)(ch0 + vc) * d + LG * ks.grp + 8 * vq;
 #pragma unroll
     for (int i = 0; i < 8; ++i) vpre[i] = vr[i];
+    // record word 0 of the thread's token in each tile, recomputed per call rather than
+    // held in registers across the slot loop
+    int u = tid & (LD_TOK - 1);
+    asm volatile("" : "+v"(u));
+    int64_t tb[LD_NT];
+#pragma unroll
+    for (int t2 = 0; t2 < LD_NT; ++t2) {
+      const int64_t i = tok0 + (int64_t)t2 * LD_TOK + u;
+      tb[t2] = rec_word(sbase, a.t0 + (i < a.n ? i : a.n - 1), a.W, 0);
+    }
 #pragma unroll
     for (int r = 0; r < LD_R; ++r) {
-      const int k8 = ((tid + 512 * r) >> 7) & 7;
+      const int k8 = (kq + 4 * r) & 7, t2 = r >> 1;
       const int P = 8 * k8 * ks.b, w0 = P >> 5, wl = (P + 8 * ks.b - 1) >> 5;  // payload words extract8 reads
 #pragma unroll
-      for (int i = 0; i < 3; ++i) wpre[r][i] = (w0 + i <= wl) ? a.packed[tbase[r] + (int64_t)(ks.pay + w0 + i) * TILE] : 0u;
-      mpre[r] = a.packed[tbase[r] + (int64_t)slot * TILE];
+      for (int i = 0; i < 3; ++i) wpre[r][i] = (w0 + i <= wl) ? a.packed[tb[t2] + (int64_t)(ks.pay + w0 + i) * TILE] : 0u;
+      mpre[r] = a.packed[tb[t2] + (int64_t)slot * TILE];
     }
   };
 
@@ -398,9 +401,11 @@ __global__ __launch_bounds__(512, 4) void layer_decode_kernel(LayerDecodeArgs a)
   if (n_kept > 0) prefetch(ks, 0);
   for (int slot = 0; slot < n_kept; ++slot) {
     // stage the prefetched slot: codes as bf16 and metadata, basis parts and sums
+    int kqs = kq;
+    asm volatile("" : "+s"(kqs));  // shift amounts recomputed per slot (scalar), not hoisted
 #pragma unroll
     for (int r = 0; r < LD_R; ++r) {
-      const int e = tid + 512 * r, u = e & (LD_TOK - 1), k8 = (e >> 7) & 7, t2 = e >> 10;
+      const int u = tid & (LD_TOK - 1), k8 = (kqs + 4 * r) & 7, t2 = r >> 1;
       const int w0 = (8 * k8 * ks.b) >> 5;
       with_bits(ks.b, [&](auto bc) {
         constexpr int B = decltype(bc)::value;
