@@ -169,7 +169,8 @@ __device__ __forceinline__ int le_row(int c) {
 __global__ __launch_bounds__(512, 4) void layer_encode_kernel(LayerEncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vs[3][64][LE_KP];
   const int s = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, h = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, col = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: the staging rows are scalar
   const int d = a.d, ng = d / LG;
   int range, slot;
   xcd_major_block((int)((a.n + LE_TOK - 1) / LE_TOK), ng, range, slot);
@@ -196,7 +197,7 @@ __global__ __launch_bounds__(512, 4) void layer_encode_kernel(LayerEncodeArgs a)
   const float* V = a.basis + (int64_t)s * d * d + LG * ks.grp;
 
   // staging map: thread -> (group coefficient sc, basis rows sk .. sk + 7 of the chunk)
-  const int sc = tid & 63, sk = 8 * (tid >> 6), srow = le_row(sc);
+  const int sc = tid & 63, sk = 8 * wave, srow = le_row(sc);
   float pre[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) pre[i] = V[(int64_t)(sk + i) * d + sc];
@@ -253,20 +254,27 @@ __global__ __launch_bounds__(512, 4) void layer_encode_kernel(LayerEncodeArgs a)
     __syncthreads();
   }
 
-  // lane (h, col): coefficients 16h + i (acc0) and 32 + 16h + i (acc1) of token col
+  // lane (h, col): coefficients 16h + i (acc0) and 32 + 16h + i (acc1) of token col. The
+  // lane's token and half are recomputed here rather than held in registers across the loop.
+  int tid_e = tid;
+  asm volatile("" : "+v"(tid_e));
+  const int he = (tid_e & 63) >> 5;
+  const int64_t i_tok_e = wg_tok + 32 * wave + (tid_e & 31);
+  const bool valid_e = i_tok_e < a.n;
+  const int64_t i_ld_e = valid_e ? i_tok_e : a.n - 1;
   const float* mg = a.mean + (int64_t)s * d + LG * ks.grp;
   float c[32];
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    c[i] = (acc0[i] + sm0[i]) - mg[16 * h + i];
-    c[16 + i] = (acc1[i] + sm1[i]) - mg[32 + 16 * h + i];
+    c[i] = (acc0[i] + sm0[i]) - mg[16 * he + i];
+    c[16 + i] = (acc1[i] + sm1[i]) - mg[32 + 16 * he + i];
   }
   if (a.lscale) {  // square-root split: the cached coordinate is (x V - m)_j f_j
     const float* fg = a.lscale + (int64_t)s * d + LG * ks.grp;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      c[i] *= fg[16 * h + i];
-      c[16 + i] *= fg[32 + 16 * h + i];
+      c[i] *= fg[16 * he + i];
+      c[16 + i] *= fg[32 + 16 * he + i];
     }
   }
   float lo = c[0], hi = c[0];
@@ -277,7 +285,7 @@ __global__ __launch_bounds__(512, 4) void layer_encode_kernel(LayerEncodeArgs a)
   }
   lo = __builtin_fminf(lo, __shfl_xor(lo, 32));
   hi = __builtin_fmaxf(hi, __shfl_xor(hi, 32));
-  const int64_t base = rec_word(sbase, a.t0 + i_ld, a.W, 0);
+  const int64_t base = rec_word(sbase, a.t0 + i_ld_e, a.W, 0);
   with_bits(ks.b, [&](auto bc) {
     constexpr int B = decltype(bc)::value;
     constexpr float LEV = (float)((1 << B) - 1);
@@ -294,9 +302,9 @@ __global__ __launch_bounds__(512, 4) void layer_encode_kernel(LayerEncodeArgs a)
     }
     pack16<B>(q0, P0);
     pack16<B>(q1, P1);
-    if (h == 0 && valid) a.packed[base + (int64_t)slot * TILE] = s16 | (z16 << 16);
-    store_payload<B>(a.packed, base, ks.pay, P0, h, valid);
-    store_payload<B>(a.packed, base, ks.pay + B, P1, h, valid);
+    if (he == 0 && valid_e) a.packed[base + (int64_t)slot * TILE] = s16 | (z16 << 16);
+    store_payload<B>(a.packed, base, ks.pay, P0, he, valid_e);
+    store_payload<B>(a.packed, base, ks.pay + B, P1, he, valid_e);
   });
 }
 
