@@ -89,13 +89,13 @@ size_t fit_ws_bytes(int64_t n_streams, int64_t n_tokens) {
   return (size_t)n_streams * (size_t)(nch + 1) * (size_t)kMoments * sizeof(double);
 }
 
-// Per-layer geometry: moments [S][d*d + d], then the token-split partials [S][k_split][d*d].
+// Per-layer geometry: moments [S][d*d + d], then the token-split partials [S][k_split][d*d + d].
 size_t layer_fit_ws_bytes(int32_t d, int64_t n_streams, int64_t n_tokens) {
   int32_t ks;
   int64_t ct;
   layer_gram_layout(d, n_streams, n_tokens, &ks, &ct);
   const size_t dd = (size_t)d * d;
-  return round256((size_t)n_streams * (dd + d) * sizeof(double)) + (size_t)n_streams * ks * dd * sizeof(double);
+  return round256((size_t)n_streams * (dd + d) * sizeof(double)) + (size_t)n_streams * ks * (dd + d) * sizeof(double);
 }
 
 // Host half of a fit: eigenbasis, mean, variances and widths of every stream from

@@ -64,8 +64,11 @@ __device__ __forceinline__ double load_x(const void* x, int64_t i) {
     return (double)bf2f(reinterpret_cast<const uint16_t*>(x)[i]);
 }
 
-// partial[s][kc] (d x d) = sum over tokens [kc * ck, min(n, (kc + 1) ck)) of x_t^T x_t,
-// 64 x 64 output tile per workgroup, 16-token steps staged in LDS, 4 x 4 outputs per thread.
+// partial[s][kc] = [sum over tokens [kc * ck, min(n, (kc + 1) ck)) of x_t^T x_t (d x d),
+// then the column sums over the same tokens (d)], 64 x 64 output tile per workgroup,
+// 16-token steps staged in LDS, 4 x 4 outputs per thread. The workgroups of the first
+// tile column also sum their 64 channels: each thread over the tokens it stages (every
+// 16th), then the 16 shares of a channel in order.
 template <bool F32IN>
 __global__ __launch_bounds__(256) void layer_gram_kernel(LayerGramArgs g) {
   __shared__ double As[16][65];
@@ -76,6 +79,8 @@ __global__ __launch_bounds__(256) void layer_gram_kernel(LayerGramArgs g) {
   const int64_t t_begin = (int64_t)kc * g.chunk_tokens;
   const int64_t t_end = t_begin + g.chunk_tokens < g.n ? t_begin + g.chunk_tokens : g.n;
   const int64_t xb = (int64_t)s * g.stream_stride;
+  const bool col_sums = blockIdx.y == 0;  // uniform over the workgroup
+  double csum[4] = {0.0, 0.0, 0.0, 0.0};
   double acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
@@ -89,8 +94,10 @@ __global__ __launch_bounds__(256) void layer_gram_kernel(LayerGramArgs g) {
       const bool in = t < t_end;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        As[tk][c4 + e] = in ? load_x<F32IN>(g.x, xb + t * g.token_stride + i0 + c4 + e) : 0.0;
+        const double xa = in ? load_x<F32IN>(g.x, xb + t * g.token_stride + i0 + c4 + e) : 0.0;
+        As[tk][c4 + e] = xa;
         Bs[tk][c4 + e] = in ? load_x<F32IN>(g.x, xb + t * g.token_stride + j0 + c4 + e) : 0.0;
+        if (col_sums) csum[e] += xa;
       }
     }
     __syncthreads();
@@ -108,31 +115,37 @@ __global__ __launch_bounds__(256) void layer_gram_kernel(LayerGramArgs g) {
     }
     __syncthreads();
   }
-  double* out = g.partial + ((int64_t)s * g.k_split + kc) * g.d * g.d;
+  const int64_t dd = (int64_t)g.d * g.d;
+  double* out = g.partial + ((int64_t)s * g.k_split + kc) * (dd + g.d);
 #pragma unroll
   for (int p = 0; p < 4; ++p)
 #pragma unroll
     for (int q = 0; q < 4; ++q) out[(int64_t)(i0 + ty + 16 * p) * g.d + j0 + tx + 16 * q] = acc[p][q];
+  if (col_sums) {
+    const int tk = tid >> 4, c4 = 4 * (tid & 15);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) As[tk][c4 + e] = csum[e];  // the loop ended with a barrier
+    __syncthreads();
+    if (tid < 64) {
+      double cs = 0.0;
+      for (int k = 0; k < 16; ++k) cs += As[k][tid];
+      out[dd + i0 + tid] = cs;
+    }
+  }
 }
 
-// moments[s] = [sum_kc partial[s][kc] (d x d), column sums (d)], partials added in
-// ascending kc, column sums over ascending tokens.
+// moments[s] = sum_kc partial[s][kc] ([d x d Gram, d column sums]), partials added in
+// ascending kc.
 template <bool F32IN>
 __global__ __launch_bounds__(256) void layer_moments_kernel(LayerGramArgs g) {
   const int s = blockIdx.y;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t dd = (int64_t)g.d * g.d;
   double* mom = g.moments + (int64_t)s * (dd + g.d);
-  if (e < dd) {
-    const double* p = g.partial + (int64_t)s * g.k_split * dd + e;
+  if (e < dd + g.d) {
+    const double* p = g.partial + (int64_t)s * g.k_split * (dd + g.d) + e;
     double acc = 0.0;
-    for (int kc = 0; kc < g.k_split; ++kc) acc += p[kc * dd];
-    mom[e] = acc;
-  } else if (e < dd + g.d) {
-    const int c = (int)(e - dd);
-    const int64_t xb = (int64_t)s * g.stream_stride + c;
-    double acc = 0.0;
-    for (int64_t t = 0; t < g.n; ++t) acc += load_x<F32IN>(g.x, xb + t * g.token_stride);
+    for (int kc = 0; kc < g.k_split; ++kc) acc += p[kc * (dd + g.d)];
     mom[e] = acc;
   }
 }

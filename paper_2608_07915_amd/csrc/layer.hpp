@@ -13,7 +13,7 @@ struct LayerGramArgs {
   int32_t k_split;
   int32_t n_streams;
   int32_t d;
-  double* partial;  // [n_streams][k_split][d*d]
+  double* partial;  // [n_streams][k_split][d*d + d]: Gram, then column sums
   double* moments;  // [n_streams][d*d + d]
 };
 
