@@ -2,7 +2,9 @@
 // tridiagonal form followed by implicit symmetric QR steps with a Wilkinson
 // shift (the textbook method; e.g. Golub & Van Loan, Sec. 8.3), accumulating
 // every transformation into the eigenvector matrix. Used by the fit, which is
-// off the per-token path; 128 x 128 takes a few milliseconds.
+// off the per-token path; 128 x 128 takes a few milliseconds. The eigenvector matrix is
+// held transposed (row k = eigenvector column k), so that every reflection and rotation
+// updates whole contiguous rows.
 #include <algorithm>
 #include <cmath>
 #include <numeric>
@@ -14,11 +16,11 @@ namespace spectra {
 
 namespace {
 
-// Reduce symmetric A (n x n, row-major, overwritten) to tridiagonal T = Q^T A Q.
-void householder_tridiagonal(std::vector<double>& A, std::vector<double>& Q, int n) {
+// Reduce symmetric A (n x n, row-major, overwritten) to tridiagonal T = Q^T A Q; Qt holds
+// Q transposed.
+void householder_tridiagonal(std::vector<double>& A, std::vector<double>& Qt, int n) {
   auto a = [&](int i, int j) -> double& { return A[(size_t)i * n + j]; };
-  auto q = [&](int i, int j) -> double& { return Q[(size_t)i * n + j]; };
-  std::vector<double> v(n), pv(n), qv(n);
+  std::vector<double> v(n), pv(n), qv(n), sr(n);
   for (int k = 0; k + 2 < n; ++k) {
     const int m = n - k - 1;  // length of the column below the diagonal
     double norm2 = 0.0;
@@ -33,11 +35,15 @@ void householder_tridiagonal(std::vector<double>& A, std::vector<double>& Q, int
     if (vtv == 0.0) continue;
     const double beta = 2.0 / vtv;  // H = I - beta v v^T on indices k+1..n-1
     // p = beta * A_sub v ; K = beta/2 * v^T p ; w = p - K v ; A_sub -= v w^T + w v^T
-    for (int i = 0; i < m; ++i) {
-      double s = 0.0;
-      for (int j = 0; j < m; ++j) s += a(k + 1 + i, k + 1 + j) * v[j];
-      pv[i] = beta * s;
+    // (A_sub symmetric: row j of A_sub is its column j, so the sums run as row updates;
+    // each pv[i] still adds its terms in ascending j)
+    std::fill(pv.begin(), pv.begin() + m, 0.0);
+    for (int j = 0; j < m; ++j) {
+      const double vj = v[j];
+      const double* row = &a(k + 1 + j, k + 1);
+      for (int i = 0; i < m; ++i) pv[i] += row[i] * vj;
     }
+    for (int i = 0; i < m; ++i) pv[i] *= beta;
     double vp = 0.0;
     for (int i = 0; i < m; ++i) vp += v[i] * pv[i];
     const double K = 0.5 * beta * vp;
@@ -50,12 +56,19 @@ void householder_tridiagonal(std::vector<double>& A, std::vector<double>& Q, int
       a(k + 1 + i, k) = 0.0;
       a(k, k + 1 + i) = 0.0;
     }
-    // Q <- Q H
-    for (int r = 0; r < n; ++r) {
-      double s = 0.0;
-      for (int j = 0; j < m; ++j) s += q(r, k + 1 + j) * v[j];
-      s *= beta;
-      for (int j = 0; j < m; ++j) q(r, k + 1 + j) -= s * v[j];
+    // Q <- Q H, i.e. rows k+1.. of Qt: s_r = sum_j v_j Qt[k+1+j][r] (ascending j), then
+    // Qt[k+1+j][r] -= (beta s_r) v_j
+    std::fill(sr.begin(), sr.end(), 0.0);
+    for (int j = 0; j < m; ++j) {
+      const double vj = v[j];
+      const double* row = &Qt[(size_t)(k + 1 + j) * n];
+      for (int r = 0; r < n; ++r) sr[r] += row[r] * vj;
+    }
+    for (int r = 0; r < n; ++r) sr[r] *= beta;
+    for (int j = 0; j < m; ++j) {
+      const double vj = v[j];
+      double* row = &Qt[(size_t)(k + 1 + j) * n];
+      for (int r = 0; r < n; ++r) row[r] -= sr[r] * vj;
     }
   }
 }
@@ -64,7 +77,7 @@ void householder_tridiagonal(std::vector<double>& A, std::vector<double>& Q, int
 
 spectra_status eigh_sym(const double* a_in, int n, double* w, double* v_out) {
   if (n <= 0 || n > 1024) return fail(SPECTRA_EINVAL, "eigh: n=%d out of range", n);
-  std::vector<double> T((size_t)n * n), Q((size_t)n * n, 0.0);
+  std::vector<double> T((size_t)n * n), Qt((size_t)n * n, 0.0);
   double fro = 0.0;
   for (int i = 0; i < n; ++i)
     for (int j = 0; j < n; ++j) {
@@ -73,13 +86,14 @@ spectra_status eigh_sym(const double* a_in, int n, double* w, double* v_out) {
       T[(size_t)i * n + j] = x;
       fro += x * x;
     }
-  for (int i = 0; i < n; ++i) Q[(size_t)i * n + i] = 1.0;
-  householder_tridiagonal(T, Q, n);
+  for (int i = 0; i < n; ++i) Qt[(size_t)i * n + i] = 1.0;
+  householder_tridiagonal(T, Qt, n);
   auto t = [&](int i, int j) -> double& { return T[(size_t)i * n + j]; };
   const double eps = 2.220446049250313e-16;
   const double tiny = 1e-300 + eps * std::sqrt(fro) * 1e-3;
 
-  // Apply P = [[c, s], [-s, c]] on rows/cols (k, k+1): T <- P T P^T, Q <- Q P^T.
+  // Apply P = [[c, s], [-s, c]] on rows/cols (k, k+1): T <- P T P^T, Q <- Q P^T (rows k
+  // and k+1 of Qt).
   auto rotate = [&](int k, double c, double s, int lo, int hi) {
     const int j0 = std::max(lo, k - 1), j1 = std::min(hi, k + 2);
     for (int j = j0; j <= j1; ++j) {
@@ -92,11 +106,12 @@ spectra_status eigh_sym(const double* a_in, int n, double* w, double* v_out) {
       t(i, k) = c * c1 + s * c2;
       t(i, k + 1) = -s * c1 + c * c2;
     }
+    double* r1 = &Qt[(size_t)k * n];
+    double* r2 = &Qt[(size_t)(k + 1) * n];
     for (int r = 0; r < n; ++r) {
-      double* row = &Q[(size_t)r * n];
-      const double q1 = row[k], q2 = row[k + 1];
-      row[k] = c * q1 + s * q2;
-      row[k + 1] = -s * q1 + c * q2;
+      const double q1 = r1[r], q2 = r2[r];
+      r1[r] = c * q1 + s * q2;
+      r2[r] = -s * q1 + c * q2;
     }
   };
 
@@ -141,15 +156,16 @@ spectra_status eigh_sym(const double* a_in, int n, double* w, double* v_out) {
     w[jo] = t(j, j);
     int imax = 0;
     double vmax = -1.0;
+    const double* qj = &Qt[(size_t)j * n];
     for (int i = 0; i < n; ++i) {
-      const double x = std::fabs(Q[(size_t)i * n + j]);
+      const double x = std::fabs(qj[i]);
       if (x > vmax) {
         vmax = x;
         imax = i;
       }
     }
-    const double sg = Q[(size_t)imax * n + j] < 0 ? -1.0 : 1.0;
-    for (int i = 0; i < n; ++i) v_out[(size_t)i * n + jo] = sg * Q[(size_t)i * n + j];
+    const double sg = qj[imax] < 0 ? -1.0 : 1.0;
+    for (int i = 0; i < n; ++i) v_out[(size_t)i * n + jo] = sg * qj[i];
   }
   return SPECTRA_OK;
 }
